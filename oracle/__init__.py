@@ -1,0 +1,223 @@
+"""Python access to the fp64 CPU oracle (seer_oracle.c).
+
+TEST INFRASTRUCTURE ONLY: the independent checker of the HIP library.  It shares
+no code with paper_2410_13276_amd/ and imports nothing from it.  Only tests/,
+__graft_entry__.smoke() and the cpu_baseline leg of bench.py use it.
+
+Every function follows one step of the SeerAttention prefill path
+(arXiv 2410.13276): pooling and gate (section 3.1, Eq. 1), block selection
+(Eq. 3 TopK, Eq. 4 threshold), masked causal attention (section 3.3), and the
+MaxPool2D distillation target (Eq. 2).  The arithmetic itself lives in the C
+file; this module only marshals numpy arrays.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "seer_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+F32, BF16 = 0, 1
+POOL_AVG, POOL_MAX_MIN_AVG = 0, 1
+TOPK_RATIO, TOPK_FIXED, THRESHOLD = 0, 1, 2
+
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile liboracle.so with gcc (-O2, OpenMP, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        tmp = _LIB_PATH + f".tmp{os.getpid()}"
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+                               "-Wall", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build()
+        L = C.CDLL(_LIB_PATH)
+        p = C.c_void_p
+        i = C.c_int
+        L.orc_version.restype = i
+        L.orc_set_threads.argtypes = [i]
+        L.orc_set_threads.restype = i
+        L.orc_pool.argtypes = [p, i, i, i, i, i, p, i, i, p]
+        L.orc_pool.restype = i
+        L.orc_linear.argtypes = [p, i, i, i, i, p, i, i, p]
+        L.orc_linear.restype = None
+        L.orc_gate_logits.argtypes = [p, p, i, i, i, i, i, p]
+        L.orc_gate_logits.restype = None
+        L.orc_gate_logscore.argtypes = [p, C.c_int64, i, p]
+        L.orc_gate_logscore.restype = None
+        L.orc_topk_k.argtypes = [i, i, C.c_double, i, i]
+        L.orc_topk_k.restype = i
+        L.orc_select.argtypes = [p, i, i, i, i, C.c_double, i, p, i, i, i, p, p, p, p]
+        L.orc_select.restype = i
+        L.orc_attn.argtypes = [p, p, p, i, i, i, i, i, i, p, p, p, i, i, C.c_double,
+                               p, p, i, p, p]
+        L.orc_attn.restype = i
+        L.orc_maxpool_gt.argtypes = [p, p, i, i, i, i, i, i, p, p, i, C.c_double, p]
+        L.orc_maxpool_gt.restype = i
+        _lib = L
+    return _lib
+
+
+def set_threads(n: int) -> int:
+    """Set the OpenMP thread count (n <= 0 keeps it); returns the count in use."""
+    return lib().orc_set_threads(int(n))
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(C.c_void_p)
+
+
+def _dtype_code(x: np.ndarray) -> int:
+    if x.dtype == np.float32:
+        return F32
+    if x.dtype == np.uint16:
+        return BF16
+    raise TypeError("oracle inputs are fp32 arrays or uint16 bf16 bit patterns")
+
+
+def _strides(x: np.ndarray) -> np.ndarray:
+    """(batch, head, seq) strides in elements of a [B, H, S, D] array with unit D stride."""
+    assert x.ndim == 4 and x.strides[3] == x.itemsize
+    return np.asarray([s // x.itemsize for s in x.strides[:3]], dtype=np.int64)
+
+
+def pool(x: np.ndarray, block: int, kind: int) -> np.ndarray:
+    """Sequence pooling of [B, H, S, D]: avg -> [B,H,nb,D]; max|min|avg -> [B,H,nb,3D]."""
+    B, H, S, D = x.shape
+    nb = S // block
+    out = np.empty((B, H, nb, D if kind == POOL_AVG else 3 * D), dtype=np.float64)
+    st = _strides(x)
+    rc = lib().orc_pool(_ptr(x), _dtype_code(x), B, H, S, D, _ptr(st), block, kind, _ptr(out))
+    if rc != 0:
+        raise ValueError("seq_len must be a multiple of block")
+    return out
+
+
+def linear(pooled: np.ndarray, W: np.ndarray, w_per_head: bool = True) -> np.ndarray:
+    """Gate linear layer: [B,H,nb,din] x W[H or 1, din, dout] -> [B,H,nb,dout]."""
+    pooled = np.ascontiguousarray(pooled, dtype=np.float64)
+    W = np.ascontiguousarray(W, dtype=np.float32)
+    B, H, nb, din = pooled.shape
+    assert W.shape[1] == din
+    dout = W.shape[2]
+    out = np.empty((B, H, nb, dout), dtype=np.float64)
+    lib().orc_linear(_ptr(pooled), B, H, nb, din, _ptr(W), int(bool(w_per_head)), dout, _ptr(out))
+    return out
+
+
+def gate_logits(Qg: np.ndarray, Kg: np.ndarray) -> np.ndarray:
+    Qg = np.ascontiguousarray(Qg, dtype=np.float64)
+    Kg = np.ascontiguousarray(Kg, dtype=np.float64)
+    B, Hq, nb, Dg = Qg.shape
+    Hkv = Kg.shape[1]
+    L = np.empty((B, Hq, nb, nb), dtype=np.float64)
+    lib().orc_gate_logits(_ptr(Qg), _ptr(Kg), B, Hq, Hkv, nb, Dg, _ptr(L))
+    return L
+
+
+def gate_logscore(L: np.ndarray) -> np.ndarray:
+    L = np.ascontiguousarray(L, dtype=np.float64)
+    nb = L.shape[-1]
+    ell = np.empty_like(L)
+    lib().orc_gate_logscore(_ptr(L), L.size // nb, nb, _ptr(ell))
+    return ell
+
+
+def topk_k(mode: int, i: int, rho: float, k_fixed: int, n_forced: int) -> int:
+    return lib().orc_topk_k(mode, i, rho, k_fixed, n_forced)
+
+
+def select(ell: np.ndarray, mode: int, rho: float = 0.0, k: int = 0,
+           thresholds: Optional[np.ndarray] = None, keep_first: int = 1, keep_diag: int = 1):
+    """Block selection on log-scores [B, Hq, nb, nb].
+
+    Returns dict(mask uint8 [B,Hq,nb,nb], count int32 [B,Hq,nb],
+    idx uint16 [B,Hq,nb,nb], cut float64 [B,Hq,nb])."""
+    ell = np.ascontiguousarray(ell, dtype=np.float64)
+    B, Hq, nb, _ = ell.shape
+    thr = None
+    n_thr = 0
+    if mode == THRESHOLD:
+        thr = np.ascontiguousarray(np.atleast_1d(thresholds), dtype=np.float32)
+        n_thr = thr.size
+    mask = np.zeros((B, Hq, nb, nb), dtype=np.uint8)
+    count = np.zeros((B, Hq, nb), dtype=np.int32)
+    idx = np.zeros((B, Hq, nb, nb), dtype=np.uint16)
+    cut = np.zeros((B, Hq, nb), dtype=np.float64)
+    rc = lib().orc_select(_ptr(ell), B, Hq, nb, mode, float(rho), int(k), _ptr(thr), n_thr,
+                          int(keep_first), int(keep_diag), _ptr(mask), _ptr(count), _ptr(idx),
+                          _ptr(cut))
+    if rc != 0:
+        raise ValueError(f"orc_select failed ({rc})")
+    return dict(mask=mask, count=count, idx=idx, cut=cut)
+
+
+def gate(q: np.ndarray, k: np.ndarray, wq: np.ndarray, wk: np.ndarray, block: int = 64,
+         w_per_head: bool = True):
+    """Pool, linear and logits of the gate.  Returns (L, ell) [B, Hq, nb, nb]."""
+    qp = pool(q, block, POOL_AVG)
+    kp = pool(k, block, POOL_MAX_MIN_AVG)
+    qg = linear(qp, wq, w_per_head)
+    kg = linear(kp, wk, w_per_head)
+    L = gate_logits(qg, kg)
+    return L, gate_logscore(L)
+
+
+def attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, block: int = 64, causal: bool = True,
+         scale: Optional[float] = None, mask: Optional[np.ndarray] = None,
+         rows: Optional[np.ndarray] = None):
+    """Masked (block-sparse) causal attention in fp64.
+
+    q [B,Hq,S,D], k/v [B,Hkv,S,D] (fp32 or bf16 bits, same type); mask uint8
+    [B,Hq,nb,nb] or None (dense); rows int32 [n,3] of (b,h,i) or None (all).
+    Returns (O [n, block, D], LSE [n, block]) with n = len(rows) or B*Hq*nb."""
+    assert q.dtype == k.dtype == v.dtype
+    B, Hq, S, D = q.shape
+    Hkv = k.shape[1]
+    nb = S // block
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    if mask is not None:
+        mask = np.ascontiguousarray(mask, dtype=np.uint8)
+        assert mask.shape == (B, Hq, nb, nb)
+    n = B * Hq * nb
+    if rows is not None:
+        rows = np.ascontiguousarray(rows, dtype=np.int32).reshape(-1, 3)
+        n = rows.shape[0]
+    O = np.empty((n, block, D), dtype=np.float64)
+    lse = np.empty((n, block), dtype=np.float64)
+    rc = lib().orc_attn(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), B, Hq, Hkv, S, D,
+                        _ptr(_strides(q)), _ptr(_strides(k)), _ptr(_strides(v)), block,
+                        int(bool(causal)), float(scale), _ptr(mask), _ptr(rows),
+                        n if rows is not None else 0, _ptr(O), _ptr(lse))
+    if rc != 0:
+        raise ValueError(f"orc_attn failed ({rc})")
+    return O, lse
+
+
+def maxpool_gt(q: np.ndarray, k: np.ndarray, block: int = 64, scale: Optional[float] = None):
+    """Eq. 2 target: block-wise max of the causal attention probabilities [B,Hq,nb,nb]."""
+    B, Hq, S, D = q.shape
+    Hkv = k.shape[1]
+    nb = S // block
+    if scale is None:
+        scale = 1.0 / np.sqrt(D)
+    gt = np.empty((B, Hq, nb, nb), dtype=np.float64)
+    rc = lib().orc_maxpool_gt(_ptr(q), _ptr(k), _dtype_code(q), B, Hq, Hkv, S, D,
+                              _ptr(_strides(q)), _ptr(_strides(k)), block, float(scale), _ptr(gt))
+    if rc != 0:
+        raise ValueError(f"orc_maxpool_gt failed ({rc})")
+    return gt

@@ -1,0 +1,436 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Nothing here re-types the oracle's own formulas: each check compares the oracle
+with a closed form, an invariant stated in the paper, a hand-derived fixture
+(tests/golden/), a brute force over tiny inputs, or an independent library
+routine (torch.nn.functional pooling / scaled_dot_product_attention, in fp64).
+"""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from workload import bf16_bits_to_f32, f32_to_bf16_bits, pattern_mask
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+pytestmark = pytest.mark.filterwarnings("ignore::UserWarning")
+
+
+def _rand(shape, seed, dtype=np.float32):
+    return np.random.default_rng(seed).standard_normal(shape).astype(dtype)
+
+
+def _as_f64(x):
+    return bf16_bits_to_f32(x).astype(np.float64) if x.dtype == np.uint16 else x.astype(np.float64)
+
+
+# --------------------------------------------------------------------------
+# pooling (section 3.1)
+# --------------------------------------------------------------------------
+
+def test_pool_constant_block_closed_form():
+    x = np.repeat(np.arange(4, dtype=np.float32)[None, None, :, None], 64, axis=2)  # [1,1,256,1]
+    x = np.ascontiguousarray(np.repeat(x, 3, axis=3))
+    q = oracle.pool(x, 64, oracle.POOL_AVG)
+    k = oracle.pool(x, 64, oracle.POOL_MAX_MIN_AVG)
+    for i in range(4):
+        assert np.all(q[0, 0, i] == i)
+        assert np.all(k[0, 0, i] == i)
+
+
+def test_pool_ramp_closed_form():
+    # x[t, d] = a_d + c_d * t inside each block: mean is the midpoint, max and
+    # min sit at the block ends (which end depends on the sign of c_d).
+    block, nb, D = 64, 3, 4
+    a = np.array([0.5, -1.0, 2.0, 0.0])
+    c = np.array([0.25, -0.5, 0.0, 1.0])
+    t = np.arange(nb * block)
+    x = (a[None, :] + c[None, :] * t[:, None]).astype(np.float32)[None, None]
+    k = oracle.pool(np.ascontiguousarray(x), block, oracle.POOL_MAX_MIN_AVG)
+    for i in range(nb):
+        first = a + c * (i * block)
+        last = a + c * (i * block + block - 1)
+        np.testing.assert_allclose(k[0, 0, i, :D], np.maximum(first, last), rtol=0, atol=0)
+        np.testing.assert_allclose(k[0, 0, i, D:2 * D], np.minimum(first, last), rtol=0, atol=0)
+        np.testing.assert_allclose(k[0, 0, i, 2 * D:], (first + last) / 2, rtol=1e-15, atol=1e-15)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_pool_matches_torch_pooling(dtype):
+    B, H, S, D, blk = 2, 3, 256, 8, 64
+    xf = _rand((B, H, S, D), 1)
+    x = xf if dtype == "f32" else f32_to_bf16_bits(xf)
+    ref = torch.from_numpy(_as_f64(x))  # [B,H,S,D]
+    t = ref.permute(0, 1, 3, 2).reshape(B * H, D, S)
+    avg = F.avg_pool1d(t, blk, blk).reshape(B, H, D, -1).permute(0, 1, 3, 2)
+    mx = F.max_pool1d(t, blk, blk).reshape(B, H, D, -1).permute(0, 1, 3, 2)
+    mn = -F.max_pool1d(-t, blk, blk).reshape(B, H, D, -1).permute(0, 1, 3, 2)
+    q = oracle.pool(x, blk, oracle.POOL_AVG)
+    k = oracle.pool(x, blk, oracle.POOL_MAX_MIN_AVG)
+    np.testing.assert_allclose(q, avg.numpy(), rtol=1e-14, atol=1e-15)
+    np.testing.assert_array_equal(k[..., :D], mx.numpy())          # max first
+    np.testing.assert_array_equal(k[..., D:2 * D], mn.numpy())     # then min
+    np.testing.assert_allclose(k[..., 2 * D:], avg.numpy(), rtol=1e-14, atol=1e-15)  # then avg
+
+
+def test_pool_strided_input_matches_contiguous():
+    x = _rand((1, 4, 128, 16), 2)
+    view = x[:, ::2]  # non-contiguous head stride
+    a = oracle.pool(np.ascontiguousarray(view), 64, oracle.POOL_MAX_MIN_AVG)
+    b = oracle.pool(view, 64, oracle.POOL_MAX_MIN_AVG)
+    np.testing.assert_array_equal(a, b)
+
+
+def test_pool_rejects_ragged_sequence():
+    with pytest.raises(ValueError):
+        oracle.pool(_rand((1, 1, 100, 4), 3), 64, oracle.POOL_AVG)
+
+
+# --------------------------------------------------------------------------
+# gate (Eq. 1)
+# --------------------------------------------------------------------------
+
+def test_gate_hand_fixture():
+    g = json.load(open(os.path.join(GOLDEN, "tiny_gate.json")))
+    blk = g["block"]
+    q = np.asarray(g["q"], dtype=np.float32)[None, None]
+    k = np.asarray(g["k"], dtype=np.float32)[None, None]
+    wq = np.asarray(g["wq"], dtype=np.float32)[None]
+    wk = np.asarray(g["wk"], dtype=np.float32)[None]
+    qp = oracle.pool(q, blk, oracle.POOL_AVG)
+    kp = oracle.pool(k, blk, oracle.POOL_MAX_MIN_AVG)
+    np.testing.assert_array_equal(qp[0, 0], np.asarray(g["pooled_q"], dtype=np.float64))
+    np.testing.assert_array_equal(kp[0, 0], np.asarray(g["pooled_k"], dtype=np.float64))
+    qg = oracle.linear(qp, wq)
+    kg = oracle.linear(kp, wk)
+    np.testing.assert_array_equal(qg[0, 0], np.asarray(g["qg"], dtype=np.float64))
+    np.testing.assert_array_equal(kg[0, 0], np.asarray(g["kg"], dtype=np.float64))
+    L = oracle.gate_logits(qg, kg)
+    env = {"sqrt": math.sqrt, "exp": math.exp, "inf": math.inf}
+    want_L = np.array([[eval(s, env) for s in row] for row in g["logits"]])
+    np.testing.assert_allclose(L[0, 0], want_L, rtol=1e-15)
+    ell = oracle.gate_logscore(L)
+    want_P = np.array([[eval(s, env) for s in row] for row in g["probs"]])
+    np.testing.assert_allclose(np.exp(ell[0, 0]), want_P, rtol=1e-14, atol=0)
+    sel = oracle.select(ell, oracle.TOPK_FIXED, k=1, keep_first=0, keep_diag=0)
+    np.testing.assert_array_equal(sel["mask"][0, 0], g["topk_fixed_k1_no_forcing"])
+    for key, thr, kd in [("threshold_0p5_no_forcing", 0.5, 0), ("threshold_0p1_no_forcing", 0.1, 0),
+                         ("threshold_0p5_keep_diag", 0.5, 1)]:
+        sel = oracle.select(ell, oracle.THRESHOLD, thresholds=np.float32(thr), keep_first=0, keep_diag=kd)
+        np.testing.assert_array_equal(sel["mask"][0, 0], g[key], err_msg=key)
+
+
+def _torch_gate_special(q, k, part):
+    """Gate with Wq = I and Wk selecting one pooled part of K, built from torch ops."""
+    B, H, S, D = q.shape
+    blk = 64
+    tq = torch.from_numpy(_as_f64(q)).permute(0, 1, 3, 2).reshape(B * H, D, S)
+    tk = torch.from_numpy(_as_f64(k)).permute(0, 1, 3, 2).reshape(B * H, D, S)
+    qp = F.avg_pool1d(tq, blk, blk).reshape(B, H, D, -1).transpose(-1, -2)
+    if part == 0:
+        kp = F.max_pool1d(tk, blk, blk)
+    elif part == 1:
+        kp = -F.max_pool1d(-tk, blk, blk)
+    else:
+        kp = F.avg_pool1d(tk, blk, blk)
+    kp = kp.reshape(B, H, D, -1).transpose(-1, -2)
+    logits = qp @ kp.transpose(-1, -2) / math.sqrt(D)
+    nb = S // blk
+    causal = torch.ones(nb, nb, dtype=torch.bool).tril()
+    logits = logits.masked_fill(~causal, float("-inf"))
+    return torch.softmax(logits, dim=-1).numpy()
+
+
+@pytest.mark.parametrize("part", [0, 1, 2])  # which slot of max | min | avg Wk reads
+def test_gate_reduces_to_pooled_attention(part):
+    B, H, S, D = 1, 2, 512, 16
+    q = _rand((B, H, S, D), 10 + part)
+    k = _rand((B, H, S, D), 20 + part)
+    wq = np.broadcast_to(np.eye(D, dtype=np.float32), (H, D, D)).copy()
+    wk = np.zeros((H, 3 * D, D), dtype=np.float32)
+    wk[:, part * D:(part + 1) * D, :] = np.eye(D, dtype=np.float32)
+    L, ell = oracle.gate(q, k, wq, wk)
+    ref = _torch_gate_special(q, k, part)
+    np.testing.assert_allclose(np.exp(ell), ref, rtol=1e-12, atol=1e-300)
+
+
+def test_gate_rows_sum_to_one_and_size():
+    # the gate output of a head is [seq/B, seq/B], 1/4096 of the attention map at
+    # B = 64 (section 3.1); every softmax row sums to 1 (section 3.2)
+    B, Hq, Hkv, S, D, Dg = 1, 4, 2, 1024, 32, 24
+    q, k = _rand((B, Hq, S, D), 5), _rand((B, Hkv, S, D), 6)
+    wq, wk = _rand((Hq, D, Dg), 7) * 0.3, _rand((Hkv, 3 * D, Dg), 8) * 0.3
+    L, ell = oracle.gate(q, k, wq, wk)
+    assert L.shape[-2] * L.shape[-1] * 4096 == S * S
+    np.testing.assert_allclose(np.exp(ell).sum(-1), 1.0, rtol=1e-13)
+    assert np.all(np.isneginf(np.triu(L[0, 0], 1)[np.triu_indices(16, 1)]))
+
+
+def test_gate_gqa_equals_replicated_kv():
+    B, Hq, Hkv, S, D, Dg = 1, 6, 2, 256, 16, 8
+    q, k = _rand((B, Hq, S, D), 30), _rand((B, Hkv, S, D), 31)
+    wq, wk = _rand((Hq, D, Dg), 32), _rand((Hkv, 3 * D, Dg), 33)
+    L, _ = oracle.gate(q, k, wq, wk)
+    k_rep = np.ascontiguousarray(np.repeat(k, Hq // Hkv, axis=1))
+    wk_rep = np.ascontiguousarray(np.repeat(wk, Hq // Hkv, axis=0))
+    L_rep, _ = oracle.gate(q, k_rep, wq, wk_rep)
+    np.testing.assert_array_equal(L, L_rep)
+
+
+def test_gate_shared_weights_equal_tiled_weights():
+    B, H, S, D, Dg = 1, 3, 256, 8, 8
+    x = _rand((B, H, S, D), 40)
+    w = _rand((1, D, Dg), 41)
+    a = oracle.linear(oracle.pool(x, 64, oracle.POOL_AVG), w, w_per_head=False)
+    b = oracle.linear(oracle.pool(x, 64, oracle.POOL_AVG), np.repeat(w, H, axis=0), w_per_head=True)
+    np.testing.assert_array_equal(a, b)
+    ref = np.einsum("bhnc,cd->bhnd", oracle.pool(x, 64, oracle.POOL_AVG), w[0].astype(np.float64))
+    np.testing.assert_allclose(a, ref, rtol=1e-13, atol=1e-15)
+
+
+# --------------------------------------------------------------------------
+# selection (Eq. 3 / Eq. 4)
+# --------------------------------------------------------------------------
+
+def _rand_ell(B, H, nb, seed, ties=False):
+    rng = np.random.default_rng(seed)
+    L = rng.standard_normal((B, H, nb, nb))
+    if ties:
+        L = np.round(L * 2) / 2  # many exact ties
+    L = np.where(np.tril(np.ones((nb, nb), bool)), L, -np.inf)
+    return oracle.gate_logscore(L)
+
+
+def test_topk_schedule_fixture():
+    g = json.load(open(os.path.join(GOLDEN, "topk_schedule.json")))
+    nb = g["n_blocks"]
+    ell = _rand_ell(1, 2, nb, 50)
+    sel = oracle.select(ell, oracle.TOPK_RATIO, rho=g["ratio"])
+    for h in range(2):
+        np.testing.assert_array_equal(sel["count"][0, h], g["k"])
+        assert int(sel["mask"][0, h].sum()) == g["total"]
+    assert nb * (nb + 1) // 2 == g["causal_total"]
+
+
+@pytest.mark.parametrize("kf,kd", [(1, 1), (0, 0), (1, 0), (0, 1)])
+@pytest.mark.parametrize("ties", [False, True])
+def test_topk_brute_force(kf, kd, ties):
+    nb = 8
+    ell = _rand_ell(1, 3, nb, 60 + kf + 2 * kd, ties=ties)
+    for k in range(1, nb + 1):
+        sel = oracle.select(ell, oracle.TOPK_FIXED, k=k, keep_first=kf, keep_diag=kd)
+        for h in range(3):
+            for i in range(nb):
+                forced = set()
+                if kf:
+                    forced.add(0)
+                if kd:
+                    forced.add(i)
+                kk = min(i + 1, max(len(forced), k))
+                cands = [j for j in range(i + 1) if j not in forced]
+                best = None
+                for subset in itertools.combinations(cands, kk - len(forced)):
+                    # rank: values descending, then indices ascending on ties
+                    key = sorted(((-ell[0, h, i, j], j) for j in subset))
+                    if best is None or key < best[0]:
+                        best = (key, subset)
+                want = np.zeros(nb, np.uint8)
+                want[list(forced | set(best[1]))] = 1
+                np.testing.assert_array_equal(sel["mask"][0, h, i], want, err_msg=f"k={k} h={h} i={i}")
+                assert sel["count"][0, h, i] == kk
+
+
+def test_topk_ratio_one_keeps_all_causal_blocks():
+    nb = 12
+    sel = oracle.select(_rand_ell(1, 2, nb, 70), oracle.TOPK_RATIO, rho=1.0)
+    np.testing.assert_array_equal(sel["mask"][0, 0], np.tril(np.ones((nb, nb), np.uint8)))
+
+
+def test_topk_nested_in_k():
+    nb = 16
+    ell = _rand_ell(1, 2, nb, 71)
+    prev = None
+    for k in range(1, nb + 1):
+        m = oracle.select(ell, oracle.TOPK_FIXED, k=k)["mask"]
+        if prev is not None:
+            assert np.all(prev <= m)
+        prev = m
+
+
+def test_select_idx_is_ascending_compaction_of_mask():
+    nb = 20
+    ell = _rand_ell(2, 3, nb, 72)
+    for sel in (oracle.select(ell, oracle.TOPK_RATIO, rho=0.3),
+                oracle.select(ell, oracle.THRESHOLD, thresholds=np.float32(0.05))):
+        for b, h, i in itertools.product(range(2), range(3), range(nb)):
+            c = sel["count"][b, h, i]
+            np.testing.assert_array_equal(sel["idx"][b, h, i, :c], np.nonzero(sel["mask"][b, h, i])[0])
+
+
+def test_threshold_monotone_and_limits():
+    nb = 24
+    ell = _rand_ell(1, 4, nb, 80)
+    causal = np.tril(np.ones((nb, nb), np.uint8))
+    prev = None
+    for thr in [1e-30, 1e-4, 1e-3, 1e-2, 0.05, 0.2, 0.5, 1.0]:
+        m = oracle.select(ell, oracle.THRESHOLD, thresholds=np.float32(thr))["mask"]
+        if prev is not None:
+            assert np.all(m <= prev)
+        prev = m
+    tiny = oracle.select(ell, oracle.THRESHOLD, thresholds=np.float32(1e-30))["mask"]
+    np.testing.assert_array_equal(tiny[0, 0], causal)
+    one = oracle.select(ell, oracle.THRESHOLD, thresholds=np.float32(1.0))["mask"]
+    forced = np.zeros((nb, nb), np.uint8)
+    forced[:, 0] = 1
+    forced[np.arange(nb), np.arange(nb)] = 1
+    np.testing.assert_array_equal(one[0, 2], forced)
+    # Eq. 4 is a strict comparison: row 0 has a single causal block whose
+    # probability is exactly 1, so a threshold of 1 keeps nothing unforced
+    none = oracle.select(ell, oracle.THRESHOLD, thresholds=np.float32(1.0), keep_first=0, keep_diag=0)
+    assert none["mask"].sum() == 0 and np.all(none["count"] == 0)
+
+
+def test_threshold_per_head_equals_global_per_head():
+    nb = 16
+    ell = _rand_ell(1, 4, nb, 81)
+    thr = np.array([1e-3, 0.02, 0.1, 0.3], np.float32)
+    per = oracle.select(ell, oracle.THRESHOLD, thresholds=thr)["mask"]
+    for h in range(4):
+        one = oracle.select(ell, oracle.THRESHOLD, thresholds=thr[h])["mask"]
+        np.testing.assert_array_equal(per[0, h], one[0, h])
+
+
+# --------------------------------------------------------------------------
+# masked causal attention (section 3.3) and the dense path
+# --------------------------------------------------------------------------
+
+def _sdpa(q, k, v, attn_mask=None, causal=False):
+    Hq, Hkv = q.shape[1], k.shape[1]
+    tq = torch.from_numpy(_as_f64(q))
+    tk = torch.from_numpy(_as_f64(k)).repeat_interleave(Hq // Hkv, dim=1)
+    tv = torch.from_numpy(_as_f64(v)).repeat_interleave(Hq // Hkv, dim=1)
+    return F.scaled_dot_product_attention(tq, tk, tv, attn_mask=attn_mask, is_causal=causal).numpy()
+
+
+def _o_full(O, B, H, S, D):
+    return O.reshape(B, H, S, D)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("Hq,Hkv", [(2, 2), (4, 1), (6, 2)])
+def test_dense_causal_matches_sdpa(dtype, Hq, Hkv):
+    B, S, D = 1, 256, 32
+    mk = (lambda x: x) if dtype == "f32" else f32_to_bf16_bits
+    q, k, v = (mk(_rand((B, h, S, D), s)) for h, s in [(Hq, 1), (Hkv, 2), (Hkv, 3)])
+    O, lse = oracle.attn(q, k, v)
+    ref = _sdpa(q, k, v, causal=True)
+    np.testing.assert_allclose(_o_full(O, B, Hq, S, D), ref, rtol=1e-10, atol=1e-12)
+    # an all-ones block mask is the same thing
+    ones = np.ones((B, Hq, S // 64, S // 64), np.uint8)
+    O1, lse1 = oracle.attn(q, k, v, mask=ones)
+    np.testing.assert_array_equal(O1, O)
+    np.testing.assert_array_equal(lse1, lse)
+
+
+def test_dense_noncausal_matches_sdpa():
+    B, H, S, D = 1, 2, 192, 16
+    q, k, v = (_rand((B, H, S, D), s) for s in (4, 5, 6))
+    O, _ = oracle.attn(q, k, v, causal=False)
+    np.testing.assert_allclose(_o_full(O, B, H, S, D), _sdpa(q, k, v), rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("kind", ["a_shape", "vertical", "slash", "random"])
+def test_block_masked_matches_sdpa_with_token_mask(kind):
+    B, Hq, Hkv, S, D, blk = 1, 4, 2, 512, 16, 64
+    nb = S // blk
+    q, k, v = _rand((B, Hq, S, D), 7), _rand((B, Hkv, S, D), 8), _rand((B, Hkv, S, D), 9)
+    bm = np.stack([pattern_mask(kind, nb, 100 + h, 0.3) for h in range(Hq)])[None]
+    bm[..., np.arange(nb), np.arange(nb)] = 1  # keep the diagonal so no row is empty
+    O, lse = oracle.attn(q, k, v, mask=bm)
+    tok = np.kron(bm, np.ones((blk, blk), np.uint8)).astype(bool) & np.tril(np.ones((S, S), bool))
+    ref = _sdpa(q, k, v, attn_mask=torch.from_numpy(tok))
+    np.testing.assert_allclose(_o_full(O, B, Hq, S, D), ref, rtol=1e-10, atol=1e-12)
+    # LSE against torch.logsumexp of the masked score matrix
+    tq = torch.from_numpy(q.astype(np.float64))
+    tk = torch.from_numpy(k.astype(np.float64)).repeat_interleave(Hq // Hkv, dim=1)
+    sc = (tq @ tk.transpose(-1, -2)) / math.sqrt(D)
+    sc = sc.masked_fill(~torch.from_numpy(tok), float("-inf"))
+    np.testing.assert_allclose(lse.reshape(B, Hq, S), torch.logsumexp(sc, -1).numpy(), rtol=1e-12)
+
+
+def test_constant_v_gives_constant_output():
+    B, Hq, Hkv, S, D = 1, 2, 1, 256, 8
+    q, k = _rand((B, Hq, S, D), 11), _rand((B, Hkv, S, D), 12)
+    v = np.broadcast_to(np.linspace(-2, 3, D, dtype=np.float32), (B, Hkv, S, D)).copy()
+    bm = np.stack([pattern_mask("random", 4, h, 0.5) for h in range(Hq)])[None]
+    bm[..., np.arange(4), np.arange(4)] = 1
+    O, _ = oracle.attn(q, k, v, mask=bm)
+    np.testing.assert_allclose(O, np.broadcast_to(v[0, 0, 0], O.shape), rtol=1e-14, atol=1e-14)
+
+
+def test_diagonal_only_mask_is_local_attention():
+    # only the diagonal 64-block: each query sees keys of its own block up to itself
+    B, H, S, D, blk = 1, 1, 256, 8, 64
+    q, k, v = (_rand((B, H, S, D), s) for s in (13, 14, 15))
+    bm = np.eye(S // blk, dtype=np.uint8)[None, None]
+    O, _ = oracle.attn(q, k, v, mask=bm)
+    for i in range(S // blk):
+        sl = slice(i * blk, (i + 1) * blk)
+        ref = _sdpa(q[:, :, sl], k[:, :, sl], v[:, :, sl], causal=True)
+        np.testing.assert_allclose(O[i], ref[0, 0], rtol=1e-10, atol=1e-12)
+
+
+def test_empty_row_gives_zero_and_neg_inf():
+    B, H, S, D = 1, 1, 256, 8
+    q, k, v = (_rand((B, H, S, D), s) for s in (16, 17, 18))
+    bm = np.tril(np.ones((4, 4), np.uint8))[None, None].copy()
+    bm[0, 0, 2, :] = 0
+    O, lse = oracle.attn(q, k, v, mask=bm)
+    assert np.all(O[2] == 0.0) and np.all(np.isneginf(lse[2]))
+    assert np.all(np.isfinite(lse[[0, 1, 3]]))
+
+
+def test_gqa_attention_equals_replicated_kv():
+    B, Hq, Hkv, S, D = 1, 4, 2, 256, 16
+    q, k, v = _rand((B, Hq, S, D), 19), _rand((B, Hkv, S, D), 20), _rand((B, Hkv, S, D), 21)
+    bm = np.stack([pattern_mask("vertical", 4, h, 0.5) for h in range(Hq)])[None]
+    a, la = oracle.attn(q, k, v, mask=bm)
+    rep = lambda x: np.ascontiguousarray(np.repeat(x, Hq // Hkv, axis=1))
+    b, lb = oracle.attn(q, rep(k), rep(v), mask=bm)
+    np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(la, lb)
+
+
+def test_row_subset_equals_full():
+    B, Hq, Hkv, S, D = 2, 2, 1, 256, 8
+    q, k, v = _rand((B, Hq, S, D), 22), _rand((B, Hkv, S, D), 23), _rand((B, Hkv, S, D), 24)
+    Ofull, lfull = oracle.attn(q, k, v)
+    rows = np.array([[1, 1, 3], [0, 0, 0], [1, 0, 2]], np.int32)
+    O, l = oracle.attn(q, k, v, rows=rows)
+    for r, (b, h, i) in enumerate(rows):
+        flat = (b * Hq + h) * (S // 64) + i
+        np.testing.assert_array_equal(O[r], Ofull[flat])
+        np.testing.assert_array_equal(l[r], lfull[flat])
+
+
+# --------------------------------------------------------------------------
+# distillation target (Eq. 2)
+# --------------------------------------------------------------------------
+
+def test_maxpool_gt_matches_torch():
+    B, Hq, Hkv, S, D, blk = 1, 2, 1, 256, 16, 64
+    q, k = _rand((B, Hq, S, D), 25), _rand((B, Hkv, S, D), 26)
+    gt = oracle.maxpool_gt(q, k)
+    tq = torch.from_numpy(q.astype(np.float64))
+    tk = torch.from_numpy(k.astype(np.float64)).repeat_interleave(2, dim=1)
+    sc = (tq @ tk.transpose(-1, -2)) / math.sqrt(D)
+    sc = sc.masked_fill(~torch.ones(S, S, dtype=torch.bool).tril(), float("-inf"))
+    p = torch.softmax(sc, -1)
+    ref = F.max_pool2d(p, blk, blk).numpy()
+    np.testing.assert_allclose(gt, ref, rtol=1e-12, atol=0)
