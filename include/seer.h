@@ -1,0 +1,178 @@
+/*
+ * seer.h -- C ABI of the MI355X (gfx950) SeerAttention prefill library, libseer.so.
+ *
+ * SeerAttention (arXiv 2410.13276) adds an attention gate (AttnGate) that
+ * predicts, per attention head, which 64x64 tiles of the causal attention map
+ * matter; a block-sparse FlashAttention forward then computes only those tiles.
+ * This library provides both halves plus a dense comparison path:
+ *
+ *   seer_gate        pooled-Q/K gate scores and the block mask they select
+ *                    (section 3.1, Eq. 1; Eq. 3 TopK; Eq. 4 threshold)
+ *   seer_bsattn      block-sparse causal attention over the active tiles (section 3.3)
+ *   seer_dense_attn  the same kernel over every causal tile (the dense baseline
+ *                    the paper compares against in section 4.2)
+ *   seer_mask_from_dense  compaction of a caller-made 0/1 block mask into the
+ *                    index-list form seer_bsattn reads
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers to tensors are DEVICE pointers (HIP device memory of the current
+ *    device) unless a name ends in _host.  The caller allocates and owns every
+ *    buffer; the library allocates nothing and keeps no state between calls.
+ *  - Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *    NULL is the default stream) and never synchronises the host.  The caller
+ *    synchronises before reading results.
+ *  - Arguments are validated on the host before anything is launched.  On a
+ *    validation error the call returns a non-zero seer_status, launches
+ *    nothing and leaves every output untouched.  A launch failure reported by
+ *    the HIP runtime returns SEER_ERR_HIP.  No C++ exception crosses the ABI.
+ *  - Calls on different streams touching different outputs may overlap; the
+ *    library has no global state, so every entry point is reentrant.
+ *  - Q/K/V/O are [batch][heads][seq][head_dim] with element strides given per
+ *    (batch, head, seq) and head_dim contiguous.  Query head h reads KV head
+ *    h / (heads_q / heads_kv) (grouped-query attention, contiguous groups).
+ *  - "Causal" means aligned prefill: query t sees key s iff s <= t.
+ */
+#ifndef SEER_H
+#define SEER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SEER_ABI_VERSION 1
+#define SEER_BLOCK 64 /* the paper fixes the gate / sparse-kernel block at 64 (section 4) */
+
+typedef enum {
+  SEER_OK = 0,
+  SEER_ERR_INVALID_ARG = 1, /* NULL pointer, non-positive size, inconsistent shape */
+  SEER_ERR_UNSUPPORTED = 2, /* valid request outside what is built (see each call) */
+  SEER_ERR_WORKSPACE = 3,   /* workspace missing or smaller than required */
+  SEER_ERR_HIP = 4          /* the HIP runtime reported an error at launch */
+} seer_status;
+
+typedef enum { SEER_BF16 = 0, SEER_F32 = 1 } seer_dtype;
+
+typedef enum {
+  SEER_TOPK_RATIO = 0, /* keep ceil(topk_ratio * (i + 1)) of the i + 1 causal blocks of row i */
+  SEER_TOPK_FIXED = 1, /* keep topk_k blocks per row (capped at i + 1) */
+  SEER_THRESHOLD = 2   /* keep blocks whose gate probability is strictly above the threshold */
+} seer_select_mode;
+
+/* Shape and layout of Q, K, V and O (shared by the gate and attention). */
+typedef struct {
+  int32_t batch;
+  int32_t heads_q;
+  int32_t heads_kv;  /* heads_q % heads_kv == 0 */
+  int32_t seq_len;   /* a multiple of SEER_BLOCK */
+  int32_t head_dim;  /* 64 or 128 */
+  int32_t dtype;     /* seer_dtype of Q, K, V and O */
+  int64_t q_stride[3]; /* element strides of (batch, head, seq); head_dim stride is 1 */
+  int64_t k_stride[3];
+  int64_t v_stride[3];
+  int64_t o_stride[3];
+} seer_attn_desc;
+
+/* AttnGate parameters (section 3.1, Eq. 1; selection per Eq. 3 / Eq. 4). */
+typedef struct {
+  int32_t block;       /* pooling kernel = stride = sparse tile; must be SEER_BLOCK */
+  int32_t gate_dim;    /* Dg, output width of the gate linear layers: 32, 64 or 128 */
+  int32_t w_per_head;  /* 1: wq [heads_q][D][Dg], wk [heads_kv][3D][Dg];
+                          0: one wq [D][Dg] and one wk [3D][Dg] shared by all heads */
+  int32_t mode;        /* seer_select_mode */
+  double topk_ratio;   /* SEER_TOPK_RATIO: in (0, 1]; the product with i + 1 is formed in double */
+  int32_t topk_k;      /* SEER_TOPK_FIXED: >= 1 */
+  float threshold;     /* SEER_THRESHOLD: global threshold, used when head_thresholds is NULL */
+  const float* head_thresholds; /* SEER_THRESHOLD: device [heads_q] per-head thresholds, or NULL */
+  int32_t keep_first;  /* 1: block 0 is always kept */
+  int32_t keep_diag;   /* 1: the diagonal block i is always kept (no empty row) */
+} seer_gate_desc;
+
+/* Block mask in compacted form: for row r = (b, h, i), idx[r][0 .. count[r]-1]
+ * are the active key blocks j in strictly ascending order.  Caller-owned. */
+typedef struct {
+  int32_t n_blocks;  /* nb = seq_len / SEER_BLOCK */
+  int32_t* count;    /* device [batch][heads_q][nb] */
+  uint16_t* idx;     /* device [batch][heads_q][nb][nb] */
+  uint8_t* dense;    /* optional device [batch][heads_q][nb][nb] 0/1 copy, or NULL */
+} seer_block_mask;
+
+/* ABI version (SEER_ABI_VERSION of the built library). */
+int seer_abi_version(void);
+
+/* Static, human-readable name of a status code. */
+const char* seer_status_str(int status);
+
+/* Bytes of device workspace seer_gate needs for this shape (0 on invalid
+ * arguments): the pooled-and-projected Q and K (fp32) and, unless the caller
+ * passes logits_out, the fp32 gate logits [batch][heads_q][nb][nb]. */
+size_t seer_gate_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate,
+                                 int32_t logits_in_workspace);
+
+/* Elements of the idx array of a seer_block_mask for this shape (B*Hq*nb*nb). */
+size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block);
+
+/*
+ * AttnGate (section 3.1, Eq. 1) and block selection (Eq. 3 / Eq. 4).
+ *   Qp = average of each 64-token block of Q            [B][Hq][nb][D]
+ *   Kp = max | min | average of each block of K         [B][Hkv][nb][3D]
+ *   Qg = Qp Wq, Kg = Kp Wk (no bias)                    fp32
+ *   L[i][j] = Qg[i] . Kg[g][j] / sqrt(Dg) for j <= i    (block-causal)
+ *   P = softmax over j of L[i][.]
+ *   TopK: the forced blocks ({0} if keep_first, {i} if keep_diag) plus the best
+ *         remaining causal blocks by L, ties to the smaller j, k_i blocks in all
+ *         with k_i = min(i + 1, max(#forced, k)).
+ *   Threshold: the forced blocks plus every causal j with P[i][j] > threshold.
+ * Inputs q, k follow desc (bf16 or fp32); wq, wk are fp32 (layout in
+ * seer_gate_desc).  Writes out->count, out->idx and, when non-NULL, out->dense.
+ * logits_out (device float [B][Hq][nb][nb], or NULL) receives L for j <= i
+ * (entries above the diagonal unspecified); when NULL, L lives in the workspace.
+ * workspace: device memory of at least seer_gate_workspace_bytes(desc, gate,
+ * logits_out == NULL) bytes, 256-byte aligned.
+ * Unsupported: gate->block != 64, head_dim not in {64, 128}, gate_dim not in
+ * {32, 64, 128}, nb > 4096.
+ */
+seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate,
+                      const void* q, const void* k, const float* wq, const float* wk,
+                      seer_block_mask* out, float* logits_out,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Block-sparse FlashAttention forward (section 3.3): for each query block i of
+ * (b, h) and each active key block j of mask row (b, h, i),
+ *   O_i = softmax(sm_scale * Q_i K^T) V over the keys of the active blocks,
+ * with the causal mask applied inside the diagonal block when causal != 0.
+ * sm_scale <= 0 selects 1/sqrt(head_dim).  o follows desc (same dtype as q);
+ * lse (device float [B][Hq][seq], or NULL) receives the natural-log
+ * log-sum-exp of each query's scaled scores.  A row with no active block
+ * yields O = 0 and LSE = -inf.  When causal, list entries j > i end the row;
+ * entries j >= nb always end it, and count is clamped to nb, so a malformed
+ * mask cannot make the kernel read out of bounds.
+ * Unsupported: block != 64, head_dim not in {64, 128}.
+ */
+seer_status seer_bsattn(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
+                        int32_t causal, float sm_scale, const void* q, const void* k,
+                        const void* v, void* o, float* lse, void* stream);
+
+/*
+ * Dense attention (the comparison path): seer_bsattn with every block active
+ * (j <= i when causal, every j otherwise), without reading a mask.
+ */
+seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm_scale,
+                            const void* q, const void* k, const void* v, void* o, float* lse,
+                            void* stream);
+
+/*
+ * Compacts a 0/1 block mask dense (device uint8 [B][Hq][nb][nb]; any non-zero
+ * byte is active) into out->count / out->idx (ascending).  out->dense is ignored.
+ */
+seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, const uint8_t* dense,
+                                 seer_block_mask* out, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEER_H */

@@ -1,0 +1,271 @@
+"""Python binding of libseer.so, the MI355X (gfx950) SeerAttention prefill library.
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels (include/seer.h documents the C ABI).  PyTorch supplies device memory
+and the current stream.  Importing this package does not load the library;
+the first call does, and raises if libseer.so has not been built -- there is
+no CPU fallback.
+
+    mask = seer.gate(q, k, wq, wk, mode=seer.TOPK_RATIO, topk_ratio=0.1)
+    o, lse = seer.bsattn(q, k, v, mask)
+    o_dense, _ = seer.dense_attn(q, k, v)
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libseer.so")
+
+BLOCK = 64
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = 0, 1, 2, 3, 4
+BF16, F32 = 0, 1
+TOPK_RATIO, TOPK_FIXED, THRESHOLD = 0, 1, 2
+
+
+class AttnDesc(C.Structure):
+    _fields_ = [("batch", C.c_int32), ("heads_q", C.c_int32), ("heads_kv", C.c_int32),
+                ("seq_len", C.c_int32), ("head_dim", C.c_int32), ("dtype", C.c_int32),
+                ("q_stride", C.c_int64 * 3), ("k_stride", C.c_int64 * 3),
+                ("v_stride", C.c_int64 * 3), ("o_stride", C.c_int64 * 3)]
+
+
+class GateDesc(C.Structure):
+    _fields_ = [("block", C.c_int32), ("gate_dim", C.c_int32), ("w_per_head", C.c_int32),
+                ("mode", C.c_int32), ("topk_ratio", C.c_double), ("topk_k", C.c_int32),
+                ("threshold", C.c_float), ("head_thresholds", C.c_void_p),
+                ("keep_first", C.c_int32), ("keep_diag", C.c_int32)]
+
+
+class BlockMaskStruct(C.Structure):
+    _fields_ = [("n_blocks", C.c_int32), ("count", C.c_void_p), ("idx", C.c_void_p),
+                ("dense", C.c_void_p)]
+
+
+# every symbol include/seer.h declares, with its ctypes signature
+_P = C.c_void_p
+_SIGS = {
+    "seer_abi_version": ([], C.c_int),
+    "seer_status_str": ([C.c_int], C.c_char_p),
+    "seer_gate_workspace_bytes": ([_P, _P, C.c_int32], C.c_size_t),
+    "seer_mask_idx_elems": ([_P, C.c_int32], C.c_size_t),
+    "seer_gate": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P], C.c_int),
+    "seer_bsattn": ([_P, C.c_int32, _P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P], C.c_int),
+    "seer_dense_attn": ([_P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P], C.c_int),
+    "seer_mask_from_dense": ([_P, C.c_int32, _P, _P, _P], C.c_int),
+}
+
+_lib = None
+
+
+class SeerError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_str(status)} ({status})")
+
+
+def lib():
+    """The loaded libseer.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2410_13276_amd.build` (no CPU fallback exists)")
+        L = C.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def status_str(status: int) -> str:
+    return lib().seer_status_str(int(status)).decode()
+
+
+def abi_version() -> int:
+    return lib().seer_abi_version()
+
+
+# ---------------------------------------------------------------------------
+# marshalling helpers
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}: Q/K/V are bfloat16 or float32")
+
+
+def make_desc(q, k, v=None, o=None) -> AttnDesc:
+    """Descriptor of [B, H, S, D] tensors (element strides, D contiguous)."""
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o)):
+        if t is not None and (t.dim() != 4 or t.stride(3) != 1):
+            raise ValueError(f"{name} must be [batch, heads, seq, head_dim] with unit last stride")
+    d = AttnDesc()
+    d.batch, d.heads_q, d.seq_len, d.head_dim = q.shape[0], q.shape[1], q.shape[2], q.shape[3]
+    d.heads_kv = k.shape[1]
+    d.dtype = _dtype_code(q)
+    for field, t in (("q_stride", q), ("k_stride", k), ("v_stride", v if v is not None else k),
+                     ("o_stride", o if o is not None else q)):
+        arr = getattr(d, field)
+        for e in range(3):
+            arr[e] = t.stride(e)
+    return d
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    torch = _torch()
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise SeerError(status, where)
+
+
+@dataclass
+class BlockMask:
+    """Compacted block mask: idx[b, h, i, :count[b, h, i]] ascending (device tensors)."""
+    count: object  # int32 [B, Hq, nb]
+    idx: object    # int16 storage of uint16 [B, Hq, nb, nb]
+    dense: Optional[object] = None  # uint8 [B, Hq, nb, nb]
+
+    @property
+    def n_blocks(self) -> int:
+        return self.count.shape[-1]
+
+    def struct(self) -> BlockMaskStruct:
+        m = BlockMaskStruct()
+        m.n_blocks = self.n_blocks
+        m.count = _ptr(self.count)
+        m.idx = _ptr(self.idx)
+        m.dense = _ptr(self.dense)
+        return m
+
+    def indices(self):
+        """idx as non-negative int32 (block indices are < 65536)."""
+        return self.idx.to(_torch().int32) & 0xFFFF
+
+
+def alloc_mask(batch: int, heads_q: int, seq_len: int, device="cuda", dense: bool = False) -> BlockMask:
+    torch = _torch()
+    nb = seq_len // BLOCK
+    return BlockMask(
+        count=torch.empty((batch, heads_q, nb), dtype=torch.int32, device=device),
+        idx=torch.empty((batch, heads_q, nb, nb), dtype=torch.int16, device=device),
+        dense=torch.empty((batch, heads_q, nb, nb), dtype=torch.uint8, device=device) if dense else None)
+
+
+# ---------------------------------------------------------------------------
+# entry points
+# ---------------------------------------------------------------------------
+
+def gate_desc(gate_dim: int, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
+              threshold: float = 0.0, head_thresholds=None, keep_first: bool = True,
+              keep_diag: bool = True, w_per_head: bool = True) -> GateDesc:
+    g = GateDesc()
+    g.block = BLOCK
+    g.gate_dim = gate_dim
+    g.w_per_head = int(bool(w_per_head))
+    g.mode = mode
+    g.topk_ratio = float(topk_ratio)
+    g.topk_k = int(topk_k)
+    g.threshold = float(threshold)
+    g.head_thresholds = _ptr(head_thresholds)
+    g.keep_first = int(bool(keep_first))
+    g.keep_diag = int(bool(keep_diag))
+    return g
+
+
+def gate_workspace_bytes(q, k, gate_dim: int, mode: int = TOPK_RATIO, topk_ratio: float = 1.0,
+                         logits_in_workspace: bool = True) -> int:
+    d = make_desc(q, k)
+    g = gate_desc(gate_dim, mode, topk_ratio=topk_ratio, topk_k=1, threshold=0.0)
+    return lib().seer_gate_workspace_bytes(C.byref(d), C.byref(g), int(logits_in_workspace))
+
+
+def gate(q, k, wq, wk, *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
+         threshold: float = 0.0, head_thresholds=None, keep_first: bool = True,
+         keep_diag: bool = True, w_per_head: bool = True, mask: Optional[BlockMask] = None,
+         dense_out: bool = False, logits_out=None, workspace=None, stream=None) -> BlockMask:
+    """AttnGate + block selection (seer_gate).  Returns the block mask."""
+    torch = _torch()
+    d = make_desc(q, k)
+    gd = gate_desc(wq.shape[-1], mode, topk_ratio, topk_k, threshold, head_thresholds,
+                   keep_first, keep_diag, w_per_head)
+    if mask is None:
+        mask = alloc_mask(q.shape[0], q.shape[1], q.shape[2], q.device, dense=dense_out)
+    need = lib().seer_gate_workspace_bytes(C.byref(d), C.byref(gd), int(logits_out is None))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    ms = mask.struct()
+    st = lib().seer_gate(C.byref(d), C.byref(gd), _ptr(q), _ptr(k), _ptr(wq), _ptr(wk),
+                         C.byref(ms), _ptr(logits_out), _ptr(workspace), workspace.numel(),
+                         _stream(stream))
+    _check(st, "seer_gate")
+    return mask
+
+
+def bsattn(q, k, v, mask: BlockMask, *, causal: bool = True, sm_scale: float = 0.0, out=None,
+           lse: Optional[object] = None, want_lse: bool = False, stream=None):
+    """Block-sparse attention (seer_bsattn).  Returns (O, LSE or None)."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+    d = make_desc(q, k, v, out)
+    ms = mask.struct()
+    st = lib().seer_bsattn(C.byref(d), BLOCK, C.byref(ms), int(bool(causal)), float(sm_scale),
+                           _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
+    _check(st, "seer_bsattn")
+    return out, lse
+
+
+def dense_attn(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
+               lse: Optional[object] = None, want_lse: bool = False, stream=None):
+    """Dense attention over every (causal) block (seer_dense_attn).  Returns (O, LSE or None)."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+    d = make_desc(q, k, v, out)
+    st = lib().seer_dense_attn(C.byref(d), int(bool(causal)), float(sm_scale), _ptr(q), _ptr(k),
+                               _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
+    _check(st, "seer_dense_attn")
+    return out, lse
+
+
+def mask_from_dense(dense, heads_kv: int = 1, mask: Optional[BlockMask] = None,
+                    stream=None) -> BlockMask:
+    """Compacts a uint8 [B, Hq, nb, nb] device mask (seer_mask_from_dense)."""
+    torch = _torch()
+    B, Hq, nb, _ = dense.shape
+    if mask is None:
+        mask = alloc_mask(B, Hq, nb * BLOCK, dense.device)
+    d = AttnDesc()
+    d.batch, d.heads_q, d.heads_kv, d.seq_len, d.head_dim, d.dtype = B, Hq, heads_kv, nb * BLOCK, 128, BF16
+    ms = mask.struct()
+    st = lib().seer_mask_from_dense(C.byref(d), BLOCK, _ptr(dense.contiguous()), C.byref(ms),
+                                    _stream(stream))
+    _check(st, "seer_mask_from_dense")
+    return mask

@@ -1,0 +1,412 @@
+// gate_kernels.hip -- AttnGate kernels for gfx950 (SeerAttention, arXiv 2410.13276).
+//
+//   pool_proj_kernel    section 3.1 + Eq. 1: average-pool Q and max|min|avg-pool K
+//                       over each 64-token block, then the gate linear layers.
+//                       HBM-bound: streams Q and K once with 16-byte loads; the
+//                       GEMV reuses each weight element for every block of the
+//                       workgroup.
+//   gate_logits_kernel  Eq. 1: Qg Kg^T / sqrt(Dg) on the block-causal lower
+//                       triangle, fp32 MFMA (v_mfma_f32_32x32x2_f32), 64x64 tiles.
+//   select_kernel       Eq. 3 (TopK by exact radix select on order-preserving
+//                       keys, ties to the smaller block index) or Eq. 4 (strict
+//                       threshold on the row softmax), plus the always-kept first
+//                       and diagonal blocks; one wavefront per query-block row,
+//                       writing the ascending index list by ballot compaction.
+//   mask_from_dense_kernel  the same compaction for caller-made 0/1 masks.
+#include "device_common.h"
+#include "launch.h"
+
+namespace seer {
+
+// ---------------------------------------------------------------------------
+// pooling + gate linear layers
+// ---------------------------------------------------------------------------
+
+template <typename T>
+struct Load16;
+template <>
+struct Load16<float> {
+  static constexpr int N = 4;
+  __device__ static void get(const float* p, float* out) {
+    const f32x4 v = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) out[e] = v[e];
+  }
+};
+template <>
+struct Load16<uint16_t> {
+  static constexpr int N = 8;
+  __device__ static void get(const uint16_t* p, float* out) {
+    const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      out[2 * e] = __uint_as_float(v[e] << 16);
+      out[2 * e + 1] = __uint_as_float(v[e] & 0xFFFF0000u);
+    }
+  }
+};
+
+// One workgroup of 256 threads pools R consecutive 64-token blocks of one head
+// (each thread owns one 16-byte column chunk of one block and walks its 64 rows)
+// and then projects the R pooled rows through the head's gate weights.
+template <typename T, int D, int DG, bool IS_K>
+__device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t ss, int nb,
+                                               const float* __restrict__ W,
+                                               float* __restrict__ out, float* smem) {
+  constexpr int EPL = Load16<T>::N;  // elements per 16-byte load
+  constexpr int TPR = D / EPL;       // threads per block row
+  constexpr int R = 256 / TPR;       // blocks per workgroup
+  constexpr int WIDTH = IS_K ? 3 * D : D;
+  constexpr int RPT = R * DG / 256;  // output rows per thread in the GEMV
+  static_assert(R * TPR == 256 && RPT >= 1 && (R * DG) % 256 == 0, "bad tiling");
+
+  const int t = threadIdx.x;
+  const int r = t / TPR;
+  const int c = t % TPR;
+  const int blk = blockIdx.x * R + r;
+
+  if (blk < nb) {
+    float sum[EPL], mx[EPL], mn[EPL];
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      sum[e] = 0.f;
+      mx[e] = -INFINITY;
+      mn[e] = INFINITY;
+    }
+    const T* base = x + (int64_t)blk * kBlock * ss + c * EPL;
+#pragma unroll 8
+    for (int row = 0; row < kBlock; ++row) {
+      float v[EPL];
+      Load16<T>::get(base + row * ss, v);
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        sum[e] += v[e];
+        if (IS_K) {
+          mx[e] = fmaxf(mx[e], v[e]);
+          mn[e] = fminf(mn[e], v[e]);
+        }
+      }
+    }
+    float* prow = smem + r * WIDTH + c * EPL;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) {
+      const float avg = sum[e] * (1.0f / kBlock);
+      if (IS_K) {
+        prow[e] = mx[e];
+        prow[D + e] = mn[e];
+        prow[2 * D + e] = avg;
+      } else {
+        prow[e] = avg;
+      }
+    }
+  }
+  __syncthreads();
+
+  // GEMV: out[r][j] = sum_c pooled[r][c] * W[c][j]
+  const int j = t % DG;
+  const int r0 = t / DG;  // rows r0, r0 + 256/DG, ...
+  constexpr int RSTEP = 256 / DG;
+  float acc[RPT];
+#pragma unroll
+  for (int q = 0; q < RPT; ++q) acc[q] = 0.f;
+#pragma unroll 2
+  for (int cc = 0; cc < WIDTH; cc += 4) {
+    float w[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = W[(int64_t)(cc + e) * DG + j];
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      const f32x4 p = *reinterpret_cast<const f32x4*>(smem + (r0 + q * RSTEP) * WIDTH + cc);
+      acc[q] = fmaf(p[0], w[0], acc[q]);
+      acc[q] = fmaf(p[1], w[1], acc[q]);
+      acc[q] = fmaf(p[2], w[2], acc[q]);
+      acc[q] = fmaf(p[3], w[3], acc[q]);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < RPT; ++q) {
+    const int bb = blockIdx.x * R + r0 + q * RSTEP;
+    if (bb < nb) out[(int64_t)bb * DG + j] = acc[q];
+  }
+}
+
+template <typename T, int D, int DG>
+__global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
+  constexpr int EPL = Load16<T>::N;
+  constexpr int R = 256 / (D / EPL);
+  __shared__ __attribute__((aligned(16))) float smem[R * 3 * D];
+  const int b = blockIdx.z;
+  const int slot = blockIdx.y;
+  if (slot < a.heads_q) {
+    const int h = slot;
+    const T* x = static_cast<const T*>(a.q.ptr) + b * a.q.sb + h * a.q.sh;
+    float* out = a.qg + ((int64_t)b * a.heads_q + h) * a.n_blocks * DG;
+    pool_proj_head<T, D, DG, false>(x, a.q.ss, a.n_blocks, a.wq + h * a.wq_head_stride, out, smem);
+  } else {
+    const int g = slot - a.heads_q;
+    const T* x = static_cast<const T*>(a.k.ptr) + b * a.k.sb + g * a.k.sh;
+    float* out = a.kg + ((int64_t)b * a.heads_kv + g) * a.n_blocks * DG;
+    pool_proj_head<T, D, DG, true>(x, a.k.ss, a.n_blocks, a.wk + g * a.wk_head_stride, out, smem);
+  }
+}
+
+template <typename T, int D, int DG>
+static hipError_t pool_proj_launch(const PoolProjArgs& a, hipStream_t s) {
+  constexpr int R = 256 / (D / Load16<T>::N);
+  dim3 grid((a.n_blocks + R - 1) / R, a.heads_q + a.heads_kv, a.batch);
+  hipLaunchKernelGGL((pool_proj_kernel<T, D, DG>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t pool_proj_dg(const PoolProjArgs& a, hipStream_t s) {
+  switch (a.gate_dim) {
+    case 32: return pool_proj_launch<T, D, 32>(a, s);
+    case 64: return pool_proj_launch<T, D, 64>(a, s);
+    case 128: return pool_proj_launch<T, D, 128>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_pool_proj(const PoolProjArgs& a, hipStream_t s) {
+  if (a.bf16) {
+    if (a.head_dim == 64) return pool_proj_dg<uint16_t, 64>(a, s);
+    if (a.head_dim == 128) return pool_proj_dg<uint16_t, 128>(a, s);
+  } else {
+    if (a.head_dim == 64) return pool_proj_dg<float, 64>(a, s);
+    if (a.head_dim == 128) return pool_proj_dg<float, 128>(a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------------
+// gate logits: L = Qg Kg^T * scale on 64x64 lower-triangular tiles
+// ---------------------------------------------------------------------------
+
+// Each of the 4 wavefronts computes a 32x32 sub-tile with v_mfma_f32_32x32x2_f32.
+// Operand lanes: A (rows i of Qg) and B (rows j of Kg) both hold, in lane half
+// hf = lane/32 and MFMA step v of group u, the gate feature 8u + 4hf + v, so the
+// contraction pairs identical features.  Output lane holds column j = lane%32 and
+// rows 8*(e/4) + 4*hf + e%4 of its 32x32 sub-tile (e = accumulator index).
+template <int DG>
+__global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
+  const int nb = a.n_blocks;
+  // decode the linear lower-triangular tile index
+  const int x = blockIdx.x;
+  int I = (int)((sqrtf(8.0f * x + 1.0f) - 1.0f) * 0.5f);
+  while ((I + 1) * (I + 2) / 2 <= x) ++I;
+  while (I * (I + 1) / 2 > x) --I;
+  const int J = x - I * (I + 1) / 2;
+  const int h = blockIdx.y;
+  const int b = blockIdx.z;
+  const int g = h / (a.heads_q / a.heads_kv);
+
+  const int wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const int wi = wave / 2, wj = wave % 2;
+  if (I == J && wj > wi) return;  // sub-tile entirely above the diagonal
+  const int i0 = I * 64 + wi * 32;
+  const int j0 = J * 64 + wj * 32;
+  if (i0 >= nb || j0 >= nb) return;
+  const int hf = lane / 32;
+  const int ra = min(i0 + lane % 32, nb - 1);
+  const int rb = min(j0 + lane % 32, nb - 1);
+  const float* qrow = a.qg + (((int64_t)b * a.heads_q + h) * nb + ra) * DG + 4 * hf;
+  const float* krow = a.kg + (((int64_t)b * a.heads_kv + g) * nb + rb) * DG + 4 * hf;
+
+  f32x16 acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+#pragma unroll 4
+  for (int u = 0; u < DG / 8; ++u) {
+    const f32x4 qa = *reinterpret_cast<const f32x4*>(qrow + 8 * u);
+    const f32x4 kb = *reinterpret_cast<const f32x4*>(krow + 8 * u);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[0], kb[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[1], kb[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[2], kb[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[3], kb[3], acc, 0, 0, 0);
+  }
+  const int jcol = j0 + lane % 32;
+  if (jcol >= nb) return;
+  float* out = a.logits + ((int64_t)b * a.heads_q + h) * nb * nb;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int irow = i0 + 8 * (e / 4) + 4 * hf + (e % 4);
+    if (irow < nb) out[(int64_t)irow * nb + jcol] = acc[e] * a.scale;
+  }
+}
+
+hipError_t launch_gate_logits(const GateLogitsArgs& a, hipStream_t s) {
+  const int T = (a.n_blocks + 63) / 64;
+  dim3 grid(T * (T + 1) / 2, a.heads_q, a.batch);
+  switch (a.gate_dim) {
+    case 32: hipLaunchKernelGGL(gate_logits_kernel<32>, grid, dim3(256), 0, s, a); break;
+    case 64: hipLaunchKernelGGL(gate_logits_kernel<64>, grid, dim3(256), 0, s, a); break;
+    case 128: hipLaunchKernelGGL(gate_logits_kernel<128>, grid, dim3(256), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// block selection: one wavefront per query-block row
+// ---------------------------------------------------------------------------
+
+// Writes the ascending index list (and optional 0/1 row) of a row whose
+// selection bit for block j = 64m + lane is bit m of sel.
+template <int MAXM>
+__device__ __forceinline__ void emit_row(uint64_t sel, int nb, int64_t row, int32_t* count,
+                                         uint16_t* idx, uint8_t* dense) {
+  const int lane = threadIdx.x % kWave;
+  const uint64_t lt = lanemask_lt();
+  int base = 0;
+#pragma unroll
+  for (int m = 0; m < MAXM; ++m) {
+    const int j = 64 * m + lane;
+    const bool s = ((sel >> m) & 1) && j < nb;
+    const uint64_t bal = __ballot(s);
+    if (s) idx[row * nb + base + __popcll(bal & lt)] = (uint16_t)j;
+    if (dense && j < nb) dense[row * nb + j] = s ? 1 : 0;
+    base += __popcll(bal);
+  }
+  if (lane == 0) count[row] = base;
+}
+
+template <int MAXM>
+__global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+  const int nb = a.n_blocks;
+  const int64_t rows = (int64_t)a.batch * a.heads_q * nb;
+  if (row >= rows) return;
+  const int i = (int)(row % nb);
+  const int h = (int)((row / nb) % a.heads_q);
+  const float* L = a.logits + row * nb;
+
+  // per-lane bit m describes block j = 64m + lane
+  float v[MAXM];
+  uint64_t valid = 0, forced = 0;
+#pragma unroll
+  for (int m = 0; m < MAXM; ++m) {
+    const int j = 64 * m + lane;
+    const bool ok = j <= i;
+    v[m] = ok ? L[j] : -INFINITY;
+    valid |= (uint64_t)ok << m;
+    forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
+  }
+  uint64_t sel = forced;
+
+  if (a.mode == 2) {  // threshold on the softmax probability (Eq. 4, strict)
+    float mx = -INFINITY;
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) mx = fmaxf(mx, v[m]);
+    mx = wave_max(mx);
+    float s = 0.f;
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) s += ((valid >> m) & 1) ? __expf(v[m] - mx) : 0.f;
+    s = wave_sum(s);
+    const float lse = mx + __logf(s);
+    const float t = a.head_thresholds ? a.head_thresholds[h] : a.threshold;
+    if (t <= 0.f) {
+      sel = valid;
+    } else {
+      const float lt = __logf(t);
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m) sel |= (uint64_t)(((valid >> m) & 1) && (v[m] - lse) > lt) << m;
+    }
+  } else {  // TopK (Eq. 3) over the non-forced causal blocks
+    const int nf = (a.keep_first ? 1 : 0) + ((a.keep_diag && !(a.keep_first && i == 0)) ? 1 : 0);
+    int kk = (a.mode == 0) ? (int)ceil(a.topk_ratio * (double)(i + 1)) : a.topk_k;
+    kk = min(i + 1, max(nf, kk));
+    const int take = kk - nf;
+    const int ncand = i + 1 - nf;
+    const uint64_t cand = valid & ~forced;
+    if (take >= ncand) {
+      sel = valid;
+    } else if (take > 0) {
+      // largest T with #{candidates : key >= T} >= take, built one bit at a time
+      uint32_t T = 0;
+      for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t trial = T | (1u << bit);
+        int cnt = 0;
+#pragma unroll
+        for (int m = 0; m < MAXM; ++m)
+          cnt += __popcll(__ballot(((cand >> m) & 1) && ordered_key(v[m]) >= trial));
+        if (cnt >= take) T = trial;
+      }
+      int gt = 0;
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m) gt += __popcll(__ballot(((cand >> m) & 1) && ordered_key(v[m]) > T));
+      const int need = take - gt;  // blocks taken among those tied at T, smallest j first
+      const uint64_t lt = lanemask_lt();
+      int before = 0;
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m) {
+        const bool c = (cand >> m) & 1;
+        const uint32_t key = ordered_key(v[m]);
+        const bool eq = c && key == T;
+        const uint64_t bal = __ballot(eq);
+        const int rank = before + __popcll(bal & lt);
+        sel |= (uint64_t)(c && (key > T || (eq && rank < need))) << m;
+        before += __popcll(bal);
+      }
+    }
+  }
+  emit_row<MAXM>(sel, nb, row, a.count, a.idx, a.dense);
+}
+
+template <int MAXM>
+static hipError_t select_launch(const SelectArgs& a, hipStream_t s) {
+  const int64_t rows = (int64_t)a.batch * a.heads_q * a.n_blocks;
+  dim3 grid((unsigned)((rows + 3) / 4));
+  hipLaunchKernelGGL(select_kernel<MAXM>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
+  const int m = (a.n_blocks + 63) / 64;
+  if (m <= 1) return select_launch<1>(a, s);
+  if (m <= 2) return select_launch<2>(a, s);
+  if (m <= 4) return select_launch<4>(a, s);
+  if (m <= 8) return select_launch<8>(a, s);
+  if (m <= 16) return select_launch<16>(a, s);
+  if (m <= 32) return select_launch<32>(a, s);
+  if (m <= 64) return select_launch<64>(a, s);
+  return hipErrorInvalidValue;
+}
+
+// ---------------------------------------------------------------------------
+// dense 0/1 mask -> ascending index lists
+// ---------------------------------------------------------------------------
+
+template <int MAXM>
+__global__ __launch_bounds__(256) void mask_from_dense_kernel(MaskFromDenseArgs a) {
+  const int lane = threadIdx.x % kWave;
+  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+  if (row >= a.rows) return;
+  uint64_t sel = 0;
+#pragma unroll
+  for (int m = 0; m < MAXM; ++m) {
+    const int j = 64 * m + lane;
+    sel |= (uint64_t)(j < a.n_blocks && a.dense[row * a.n_blocks + j] != 0) << m;
+  }
+  emit_row<MAXM>(sel, a.n_blocks, row, a.count, a.idx, nullptr);
+}
+
+template <int MAXM>
+static hipError_t mfd_launch(const MaskFromDenseArgs& a, hipStream_t s) {
+  dim3 grid((unsigned)((a.rows + 3) / 4));
+  hipLaunchKernelGGL(mask_from_dense_kernel<MAXM>, grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mask_from_dense(const MaskFromDenseArgs& a, hipStream_t s) {
+  const int m = (a.n_blocks + 63) / 64;
+  if (m <= 1) return mfd_launch<1>(a, s);
+  if (m <= 4) return mfd_launch<4>(a, s);
+  if (m <= 16) return mfd_launch<16>(a, s);
+  if (m <= 64) return mfd_launch<64>(a, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace seer

@@ -1,0 +1,75 @@
+// launch.h -- internal (C++) launchers behind the C ABI in include/seer.h.
+// Arguments are validated by the ABI layer before any of these is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace seer {
+
+struct TensorView {  // [batch][heads][seq][dim], element strides of (batch, head, seq)
+  const void* ptr;
+  int64_t sb, sh, ss;
+};
+
+struct PoolProjArgs {
+  TensorView q, k;
+  int batch, heads_q, heads_kv, n_blocks, head_dim, gate_dim;
+  bool bf16;
+  const float* wq;
+  const float* wk;
+  int64_t wq_head_stride, wk_head_stride;  // 0 when one matrix is shared by all heads
+  float* qg;  // [B][Hq][nb][Dg]
+  float* kg;  // [B][Hkv][nb][Dg]
+};
+
+struct GateLogitsArgs {
+  const float* qg;
+  const float* kg;
+  int batch, heads_q, heads_kv, n_blocks, gate_dim;
+  float scale;   // 1/sqrt(Dg)
+  float* logits; // [B][Hq][nb][nb]
+};
+
+struct SelectArgs {
+  const float* logits;  // [B][Hq][nb][nb], entries j <= i of each row are read
+  int batch, heads_q, n_blocks;
+  int mode;             // 0 topk ratio, 1 topk fixed, 2 threshold
+  double topk_ratio;
+  int topk_k;
+  float threshold;
+  const float* head_thresholds;  // device [Hq] or nullptr
+  int keep_first, keep_diag;
+  int32_t* count;
+  uint16_t* idx;
+  uint8_t* dense;  // optional
+};
+
+struct MaskFromDenseArgs {
+  const uint8_t* dense;
+  int64_t rows;
+  int n_blocks;
+  int32_t* count;
+  uint16_t* idx;
+};
+
+struct AttnArgs {
+  TensorView q, k, v;
+  void* o;
+  int64_t osb, osh, oss;
+  float* lse;  // [B][Hq][S] or nullptr
+  int batch, heads_q, heads_kv, n_blocks, head_dim;
+  bool bf16;
+  bool causal;
+  float scale;
+  const int32_t* count;  // nullptr: dense (every causal block)
+  const uint16_t* idx;
+};
+
+hipError_t launch_pool_proj(const PoolProjArgs& a, hipStream_t s);
+hipError_t launch_gate_logits(const GateLogitsArgs& a, hipStream_t s);
+hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_mask_from_dense(const MaskFromDenseArgs& a, hipStream_t s);
+hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
+
+}  // namespace seer

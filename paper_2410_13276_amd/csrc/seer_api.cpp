@@ -1,0 +1,254 @@
+// seer_api.cpp -- the C ABI of libseer.so (declared in include/seer.h).
+//
+// Every entry point validates its arguments on the host before launching
+// anything, then enqueues kernels on the caller's stream and returns without
+// synchronising.  The library owns no memory and keeps no state.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "launch.h"
+#include "seer.h"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t elem_size(int32_t dtype) { return dtype == SEER_F32 ? 4 : 2; }
+
+// Checks shared by every call that takes a seer_attn_desc.  `tensors` selects
+// which stride triples are used: bit 0 q, 1 k, 2 v, 3 o.
+seer_status check_desc(const seer_attn_desc* d, int tensors) {
+  if (!d) return SEER_ERR_INVALID_ARG;
+  if (d->batch <= 0 || d->heads_q <= 0 || d->heads_kv <= 0 || d->seq_len <= 0 || d->head_dim <= 0)
+    return SEER_ERR_INVALID_ARG;
+  if (d->heads_q % d->heads_kv != 0) return SEER_ERR_INVALID_ARG;
+  if (d->dtype != SEER_BF16 && d->dtype != SEER_F32) return SEER_ERR_INVALID_ARG;
+  if (d->head_dim != 64 && d->head_dim != 128) return SEER_ERR_UNSUPPORTED;
+  if (d->seq_len % SEER_BLOCK != 0) return SEER_ERR_UNSUPPORTED;
+  const int64_t vec = 16 / (int64_t)elem_size(d->dtype);  // elements per 16-byte access
+  const int64_t* st[4] = {d->q_stride, d->k_stride, d->v_stride, d->o_stride};
+  for (int t = 0; t < 4; ++t) {
+    if (!(tensors & (1 << t))) continue;
+    for (int e = 0; e < 3; ++e)
+      if (st[t][e] < 0 || st[t][e] % vec != 0) return SEER_ERR_UNSUPPORTED;
+    if (st[t][2] < d->head_dim) return SEER_ERR_INVALID_ARG;  // rows may not overlap
+  }
+  const int64_t tasks = (int64_t)d->batch * d->heads_q * (d->seq_len / SEER_BLOCK);
+  if (tasks > INT32_MAX / 2) return SEER_ERR_UNSUPPORTED;
+  return SEER_OK;
+}
+
+seer::TensorView view(const void* p, const int64_t* st) { return {p, st[0], st[1], st[2]}; }
+
+seer_status check_gate(const seer_attn_desc* d, const seer_gate_desc* g) {
+  seer_status s = check_desc(d, 0x3);
+  if (s != SEER_OK) return s;
+  if (!g) return SEER_ERR_INVALID_ARG;
+  if (g->block != SEER_BLOCK) return SEER_ERR_UNSUPPORTED;
+  if (g->gate_dim != 32 && g->gate_dim != 64 && g->gate_dim != 128) return SEER_ERR_UNSUPPORTED;
+  if (d->seq_len / SEER_BLOCK > 4096) return SEER_ERR_UNSUPPORTED;
+  switch (g->mode) {
+    case SEER_TOPK_RATIO:
+      if (!(g->topk_ratio > 0.0 && g->topk_ratio <= 1.0)) return SEER_ERR_INVALID_ARG;
+      break;
+    case SEER_TOPK_FIXED:
+      if (g->topk_k < 1) return SEER_ERR_INVALID_ARG;
+      break;
+    case SEER_THRESHOLD:
+      if (!g->head_thresholds && std::isnan(g->threshold)) return SEER_ERR_INVALID_ARG;
+      break;
+    default:
+      return SEER_ERR_INVALID_ARG;
+  }
+  return SEER_OK;
+}
+
+struct GateLayout {
+  size_t qg, kg, logits, total;
+};
+
+GateLayout gate_layout(const seer_attn_desc* d, const seer_gate_desc* g, bool logits_in_ws) {
+  const size_t nb = (size_t)(d->seq_len / SEER_BLOCK);
+  GateLayout L;
+  L.qg = 0;
+  L.kg = round_up((size_t)d->batch * d->heads_q * nb * g->gate_dim * 4);
+  L.logits = L.kg + round_up((size_t)d->batch * d->heads_kv * nb * g->gate_dim * 4);
+  L.total = L.logits + (logits_in_ws ? round_up((size_t)d->batch * d->heads_q * nb * nb * 4) : 0);
+  return L;
+}
+
+seer_status from_hip(hipError_t e) { return e == hipSuccess ? SEER_OK : SEER_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int seer_abi_version(void) { return SEER_ABI_VERSION; }
+
+const char* seer_status_str(int status) {
+  switch (status) {
+    case SEER_OK: return "SEER_OK";
+    case SEER_ERR_INVALID_ARG: return "SEER_ERR_INVALID_ARG";
+    case SEER_ERR_UNSUPPORTED: return "SEER_ERR_UNSUPPORTED";
+    case SEER_ERR_WORKSPACE: return "SEER_ERR_WORKSPACE";
+    case SEER_ERR_HIP: return "SEER_ERR_HIP";
+    default: return "SEER_ERR_UNKNOWN";
+  }
+}
+
+size_t seer_gate_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate,
+                                 int32_t logits_in_workspace) {
+  if (check_gate(desc, gate) != SEER_OK) return 0;
+  return gate_layout(desc, gate, logits_in_workspace != 0).total;
+}
+
+size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block) {
+  if (!desc || block != SEER_BLOCK || desc->batch <= 0 || desc->heads_q <= 0 || desc->seq_len <= 0 ||
+      desc->seq_len % SEER_BLOCK != 0)
+    return 0;
+  const size_t nb = (size_t)(desc->seq_len / SEER_BLOCK);
+  return (size_t)desc->batch * desc->heads_q * nb * nb;
+}
+
+seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, const void* q,
+                      const void* k, const float* wq, const float* wk, seer_block_mask* out,
+                      float* logits_out, void* workspace, size_t workspace_bytes, void* stream) {
+  seer_status s = check_gate(desc, gate);
+  if (s != SEER_OK) return s;
+  if (!q || !k || !wq || !wk || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
+  const int nb = desc->seq_len / SEER_BLOCK;
+  if (out->n_blocks != nb) return SEER_ERR_INVALID_ARG;
+  const bool logits_in_ws = logits_out == nullptr;
+  const GateLayout L = gate_layout(desc, gate, logits_in_ws);
+  if (!workspace || workspace_bytes < L.total) return SEER_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
+
+  char* ws = static_cast<char*>(workspace);
+  float* qg = reinterpret_cast<float*>(ws + L.qg);
+  float* kg = reinterpret_cast<float*>(ws + L.kg);
+  float* logits = logits_in_ws ? reinterpret_cast<float*>(ws + L.logits) : logits_out;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int D = desc->head_dim, Dg = gate->gate_dim;
+
+  seer::PoolProjArgs pa;
+  pa.q = view(q, desc->q_stride);
+  pa.k = view(k, desc->k_stride);
+  pa.batch = desc->batch;
+  pa.heads_q = desc->heads_q;
+  pa.heads_kv = desc->heads_kv;
+  pa.n_blocks = nb;
+  pa.head_dim = D;
+  pa.gate_dim = Dg;
+  pa.bf16 = desc->dtype == SEER_BF16;
+  pa.wq = wq;
+  pa.wk = wk;
+  pa.wq_head_stride = gate->w_per_head ? (int64_t)D * Dg : 0;
+  pa.wk_head_stride = gate->w_per_head ? (int64_t)3 * D * Dg : 0;
+  pa.qg = qg;
+  pa.kg = kg;
+  if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
+
+  seer::GateLogitsArgs la;
+  la.qg = qg;
+  la.kg = kg;
+  la.batch = desc->batch;
+  la.heads_q = desc->heads_q;
+  la.heads_kv = desc->heads_kv;
+  la.n_blocks = nb;
+  la.gate_dim = Dg;
+  la.scale = (float)(1.0 / std::sqrt((double)Dg));
+  la.logits = logits;
+  if ((s = from_hip(seer::launch_gate_logits(la, st))) != SEER_OK) return s;
+
+  seer::SelectArgs sa;
+  sa.logits = logits;
+  sa.batch = desc->batch;
+  sa.heads_q = desc->heads_q;
+  sa.n_blocks = nb;
+  sa.mode = gate->mode;
+  sa.topk_ratio = gate->topk_ratio;
+  sa.topk_k = gate->topk_k;
+  sa.threshold = gate->threshold;
+  sa.head_thresholds = gate->mode == SEER_THRESHOLD ? gate->head_thresholds : nullptr;
+  sa.keep_first = gate->keep_first ? 1 : 0;
+  sa.keep_diag = gate->keep_diag ? 1 : 0;
+  sa.count = out->count;
+  sa.idx = out->idx;
+  sa.dense = out->dense;
+  return from_hip(seer::launch_select(sa, st));
+}
+
+static seer_status attn_common(const seer_attn_desc* desc, const seer_block_mask* mask,
+                               int32_t causal, float sm_scale, const void* q, const void* k,
+                               const void* v, void* o, float* lse, void* stream) {
+  seer_status s = check_desc(desc, 0xF);
+  if (s != SEER_OK) return s;
+  if (!q || !k || !v || !o) return SEER_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return SEER_ERR_INVALID_ARG;
+  if (std::isnan(sm_scale) || std::isinf(sm_scale)) return SEER_ERR_INVALID_ARG;
+  const int nb = desc->seq_len / SEER_BLOCK;
+  if (mask) {
+    if (!mask->count || !mask->idx || mask->n_blocks != nb) return SEER_ERR_INVALID_ARG;
+    if (nb > 65536) return SEER_ERR_UNSUPPORTED;
+  }
+  seer::AttnArgs a;
+  a.q = view(q, desc->q_stride);
+  a.k = view(k, desc->k_stride);
+  a.v = view(v, desc->v_stride);
+  a.o = o;
+  a.osb = desc->o_stride[0];
+  a.osh = desc->o_stride[1];
+  a.oss = desc->o_stride[2];
+  a.lse = lse;
+  a.batch = desc->batch;
+  a.heads_q = desc->heads_q;
+  a.heads_kv = desc->heads_kv;
+  a.n_blocks = nb;
+  a.head_dim = desc->head_dim;
+  a.bf16 = desc->dtype == SEER_BF16;
+  a.causal = causal != 0;
+  a.scale = sm_scale > 0.f ? sm_scale : (float)(1.0 / std::sqrt((double)desc->head_dim));
+  a.count = mask ? mask->count : nullptr;
+  a.idx = mask ? mask->idx : nullptr;
+  return from_hip(seer::launch_attn(a, static_cast<hipStream_t>(stream)));
+}
+
+seer_status seer_bsattn(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
+                        int32_t causal, float sm_scale, const void* q, const void* k,
+                        const void* v, void* o, float* lse, void* stream) {
+  if (block != SEER_BLOCK) return desc ? SEER_ERR_UNSUPPORTED : SEER_ERR_INVALID_ARG;
+  if (!mask) return SEER_ERR_INVALID_ARG;
+  return attn_common(desc, mask, causal, sm_scale, q, k, v, o, lse, stream);
+}
+
+seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm_scale,
+                            const void* q, const void* k, const void* v, void* o, float* lse,
+                            void* stream) {
+  return attn_common(desc, nullptr, causal, sm_scale, q, k, v, o, lse, stream);
+}
+
+seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, const uint8_t* dense,
+                                 seer_block_mask* out, void* stream) {
+  if (!desc || !dense || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
+  if (desc->batch <= 0 || desc->heads_q <= 0 || desc->seq_len <= 0) return SEER_ERR_INVALID_ARG;
+  if (block != SEER_BLOCK || desc->seq_len % SEER_BLOCK != 0) return SEER_ERR_UNSUPPORTED;
+  const int nb = desc->seq_len / SEER_BLOCK;
+  if (out->n_blocks != nb) return SEER_ERR_INVALID_ARG;
+  if (nb > 4096) return SEER_ERR_UNSUPPORTED;
+  seer::MaskFromDenseArgs a;
+  a.dense = dense;
+  a.rows = (int64_t)desc->batch * desc->heads_q * nb;
+  a.n_blocks = nb;
+  a.count = out->count;
+  a.idx = out->idx;
+  return from_hip(seer::launch_mask_from_dense(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,146 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports every
+symbol include/seer.h declares, and rejects invalid arguments before any launch.
+
+Every call below returns from argument validation, which touches no device."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "seer.h")
+
+seer = pytest.importorskip("paper_2410_13276_amd")
+if not os.path.exists(seer.LIB_PATH):
+    pytest.skip("libseer.so not built", allow_module_level=True)
+
+
+def declared_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(seer_[a-z_]+)\s*\(", txt)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) == 8, names
+    L = C.CDLL(seer.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(seer._SIGS)
+
+
+def test_version_and_status_strings():
+    assert seer.abi_version() == 1
+    assert seer.status_str(0) == "SEER_OK"
+    assert seer.status_str(3) == "SEER_ERR_WORKSPACE"
+    assert seer.status_str(99) == "SEER_ERR_UNKNOWN"
+
+
+def _desc(B=1, Hq=4, Hkv=2, S=1024, D=128, dtype=0):
+    d = seer.AttnDesc()
+    d.batch, d.heads_q, d.heads_kv, d.seq_len, d.head_dim, d.dtype = B, Hq, Hkv, S, D, dtype
+    for f, H in (("q_stride", Hq), ("k_stride", Hkv), ("v_stride", Hkv), ("o_stride", Hq)):
+        arr = getattr(d, f)
+        arr[0], arr[1], arr[2] = H * S * D, S * D, D
+    return d
+
+
+def _gate(**kw):
+    g = seer.gate_desc(128, seer.TOPK_RATIO, topk_ratio=0.5)
+    for k, v in kw.items():
+        setattr(g, k, v)
+    return g
+
+
+FAKE = 0x1000  # a 16-byte aligned non-NULL address; never dereferenced on these paths
+
+
+def _call_gate(d, g, ws_bytes=1 << 40, mask_nb=None, q=FAKE, ws=FAKE * 16):
+    L = seer.lib()
+    m = seer.BlockMaskStruct()
+    m.n_blocks = (d.seq_len // 64) if mask_nb is None else mask_nb
+    m.count, m.idx, m.dense = FAKE, FAKE, None
+    return L.seer_gate(C.byref(d), C.byref(g), q, FAKE, FAKE, FAKE, C.byref(m), None, ws, ws_bytes, None)
+
+
+def test_workspace_size_formula():
+    d, g = _desc(B=2, Hq=4, Hkv=2, S=1024), _gate()
+    L = seer.lib()
+    nb = 16
+    up = lambda x: (x + 255) // 256 * 256
+    want = up(2 * 4 * nb * 128 * 4) + up(2 * 2 * nb * 128 * 4)
+    assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 0) == want
+    assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 1) == want + up(2 * 4 * nb * nb * 4)
+    assert L.seer_mask_idx_elems(C.byref(d), 64) == 2 * 4 * nb * nb
+    assert L.seer_mask_idx_elems(C.byref(d), 128) == 0
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("heads_kv", 3, seer.ERR_INVALID_ARG),     # heads_q % heads_kv != 0
+    ("seq_len", 1000, seer.ERR_UNSUPPORTED),   # not a multiple of 64
+    ("head_dim", 96, seer.ERR_UNSUPPORTED),
+    ("dtype", 7, seer.ERR_INVALID_ARG),
+    ("batch", 0, seer.ERR_INVALID_ARG),
+])
+def test_gate_rejects_bad_desc(field, value, status):
+    d = _desc()
+    setattr(d, field, value)
+    assert _call_gate(d, _gate()) == status
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("block", 128, seer.ERR_UNSUPPORTED),
+    ("gate_dim", 48, seer.ERR_UNSUPPORTED),
+    ("mode", 9, seer.ERR_INVALID_ARG),
+    ("topk_ratio", 0.0, seer.ERR_INVALID_ARG),
+    ("topk_ratio", 1.5, seer.ERR_INVALID_ARG),
+])
+def test_gate_rejects_bad_gate(field, value, status):
+    assert _call_gate(_desc(), _gate(**{field: value})) == status
+
+
+def test_gate_rejects_fixed_k_zero_and_nan_threshold():
+    assert _call_gate(_desc(), _gate(mode=seer.TOPK_FIXED, topk_k=0)) == seer.ERR_INVALID_ARG
+    assert _call_gate(_desc(), _gate(mode=seer.THRESHOLD, threshold=float("nan"))) == seer.ERR_INVALID_ARG
+
+
+def test_gate_rejects_short_workspace_null_and_mask_shape():
+    d, g = _desc(), _gate()
+    need = seer.lib().seer_gate_workspace_bytes(C.byref(d), C.byref(g), 1)
+    assert _call_gate(d, g, ws_bytes=need - 1) == seer.ERR_WORKSPACE
+    assert _call_gate(d, g, ws=None) == seer.ERR_WORKSPACE
+    assert _call_gate(d, g, q=None) == seer.ERR_INVALID_ARG
+    assert _call_gate(d, g, q=FAKE + 2) == seer.ERR_INVALID_ARG  # misaligned
+    assert _call_gate(d, g, mask_nb=15) == seer.ERR_INVALID_ARG
+
+
+def test_attention_rejects_bad_args():
+    L = seer.lib()
+    d = _desc()
+    m = seer.BlockMaskStruct()
+    m.n_blocks, m.count, m.idx, m.dense = 16, FAKE, FAKE, None
+    args = (FAKE, FAKE, FAKE, FAKE, None, None)
+    assert L.seer_bsattn(C.byref(d), 128, C.byref(m), 1, 0.0, *args) == seer.ERR_UNSUPPORTED
+    assert L.seer_bsattn(C.byref(d), 64, None, 1, 0.0, *args) == seer.ERR_INVALID_ARG
+    m.n_blocks = 8
+    assert L.seer_bsattn(C.byref(d), 64, C.byref(m), 1, 0.0, *args) == seer.ERR_INVALID_ARG
+    assert L.seer_dense_attn(C.byref(d), 1, float("nan"), *args) == seer.ERR_INVALID_ARG
+    assert L.seer_dense_attn(C.byref(d), 1, 0.0, None, FAKE, FAKE, FAKE, None, None) == seer.ERR_INVALID_ARG
+    d.q_stride[2] = 100  # not a multiple of 8 bf16 elements (16 bytes)
+    assert L.seer_dense_attn(C.byref(d), 1, 0.0, *args) == seer.ERR_UNSUPPORTED
+    d = _desc()
+    d.o_stride[2] = 64  # rows would overlap (stride < head_dim)
+    assert L.seer_dense_attn(C.byref(d), 1, 0.0, *args) == seer.ERR_INVALID_ARG
+
+
+def test_mask_from_dense_rejects_bad_args():
+    L = seer.lib()
+    d = _desc()
+    m = seer.BlockMaskStruct()
+    m.n_blocks, m.count, m.idx, m.dense = 16, FAKE, FAKE, None
+    assert L.seer_mask_from_dense(C.byref(d), 64, None, C.byref(m), None) == seer.ERR_INVALID_ARG
+    assert L.seer_mask_from_dense(C.byref(d), 32, FAKE, C.byref(m), None) == seer.ERR_UNSUPPORTED
+    m.n_blocks = 3
+    assert L.seer_mask_from_dense(C.byref(d), 64, FAKE, C.byref(m), None) == seer.ERR_INVALID_ARG
