@@ -110,6 +110,9 @@ def main() -> int:
     ap.add_argument("--dense-runs", type=int, default=3)
     ap.add_argument("--cpu-rows", type=int, default=1024, help="oracle sample size (q-block rows)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device-to-device copy three times (the known-size "
+                         "reference for scaling HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -121,6 +124,15 @@ def main() -> int:
 
     import torch
     import paper_2410_13276_amd as seer
+
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": src.numel() * 4, "copies": 3}))
+        return 0
 
     w = W.WORKLOADS[args.workload]
     torch.cuda.set_device(0)

@@ -33,16 +33,21 @@ struct Task {
   int b, h, i;
 };
 
-// Task order: query-block rows heaviest first (i descending), the query heads
-// of one KV head adjacent, and each KV-head group kept on one XCD (workgroups
-// are dispatched round-robin over the 8 XCDs, each with its own L2), so the
-// K/V tiles of a group are shared through one L2.  Groups are split over
-// several XCDs by row residue when there are fewer than 8.
+// Task order.  Workgroups are dispatched round-robin over the 8 XCDs (each
+// with its own L2), so workgroup w runs on XCD w % 8 and is that XCD's
+// (w / 8)-th task.  The order keeps the K/V working set of each L2 small:
+//  - the KV-head groups (batch x KV head) are processed in phases of `gpp`
+//    groups whose K and V fit the Infinity Cache together;
+//  - in a phase each group owns R = 8 / gpp XCDs, split by query-block residue
+//    i % R, so one group's K/V tiles are shared through those XCDs' L2;
+//  - within an XCD, query-block rows run heaviest first (i descending) with
+//    the query heads of the group adjacent (they read the same K/V).
+// Shapes that do not fit this scheme use the plain heaviest-first order.
 struct TaskMap {
   int batch, heads_q, heads_kv, nb;
-  int R;        // XCDs per KV group (row residue classes); 0 selects linear order
-  int lanes_x;  // (group, residue) lanes per XCD
-  int per_xcd;  // tasks per XCD
+  int R;    // XCDs per group; 0 selects the plain order
+  int gpp;  // groups per phase (R * gpp == 8)
+  int tpp;  // tasks per XCD per phase = (nb / R) * G
 };
 
 __device__ __forceinline__ Task decode_task(const TaskMap& m, int wg) {
@@ -51,15 +56,15 @@ __device__ __forceinline__ Task decode_task(const TaskMap& m, int wg) {
   if (m.R > 0) {
     const int x = wg % 8;
     const int u = wg / 8;
-    const int hh = u % G;
-    const int lam_l = (u / G) % m.lanes_x;
-    const int nu = u / (G * m.lanes_x);
-    const int lam = x * m.lanes_x + lam_l;
-    const int s = lam / m.R;
-    const int rho = lam % m.R;
+    const int ph = u / m.tpp;
+    const int rem = u % m.tpp;
+    const int nu = rem / G;
+    const int hh = rem % G;
+    const int slot = ph * m.gpp + x / m.R;
+    const int rho = x % m.R;
     t.i = m.nb - 1 - (nu * m.R + rho);
-    t.b = s / m.heads_kv;
-    t.h = (s % m.heads_kv) * G + hh;
+    t.b = slot / m.heads_kv;
+    t.h = (slot % m.heads_kv) * G + hh;
   } else {
     const int bh = m.batch * m.heads_q;
     const int nu = wg / bh;
@@ -138,117 +143,117 @@ __device__ __forceinline__ float softmax_tile(f32x16 (&s)[2], float& m_run, floa
 // ---------------------------------------------------------------------------
 // bf16 kernel
 // ---------------------------------------------------------------------------
+//
+// Tiles reach LDS by direct global->LDS loads (global_load_lds_dwordx4: lane l
+// of a wavefront writes its 16 bytes at base + 16 l), so no registers stage
+// them.  K and V are both kept row-major (one row per key, D features), with
+// the 16-byte chunks of each row XOR-swizzled so that every operand read is
+// free of LDS bank conflicts on gfx950 (64 banks, 16 lanes per pass); the
+// gather permutation is applied on the global side of the load.
+//  - K chunk c of row r sits at chunk c ^ fk(r): the S^T operand read (16
+//    lanes = 16 consecutive rows, one chunk each) hits 16 distinct bank groups.
+//  - V chunk c of row r sits at chunk c ^ fv(r): the V^T operand is read with
+//    ds_read_b64_tr_b16, where 16 lanes read 8 bytes each from 4 consecutive
+//    rows x 32 bytes; fv moves those 4 row segments onto distinct banks.
+//
+// ds_read_b64_tr_b16 semantics (within each group of 16 lanes): view the 16
+// lanes' 8-byte reads as a 16 x 4 matrix C of 16-bit values; lane 4a + b
+// receives C[a][b], C[a+4][b], C[a+8][b], C[a+12][b].  With lane 16g + r
+// pointing at key row base + r/4, feature 4(r%4) + 16(g%2) + 32dt, output lane
+// L receives the four consecutive keys base..base+3 of feature 32dt + L%32 --
+// exactly four k-slots of the V^T operand of the 32x32x16 MFMA.
 
 template <int D>
 struct Bf16Layout {
-  static constexpr int KSTR = D + 8;   // LDS row stride of K (bf16 elements), conflict-free b128 reads
-  static constexpr int VSTR = 64 + 4;  // LDS row stride of V^T (one row per feature d)
-  static constexpr int OSTR = D + 8;   // LDS row stride of the output staging tile
-  static constexpr int K_BYTES = 64 * KSTR * 2;
-  static constexpr int V_BYTES = D * VSTR * 2;
-  static constexpr int VBL = D / 64;   // (4 keys x 8 features) V blocks per thread per tile
-  static_assert(64 * OSTR * 2 <= K_BYTES + V_BYTES, "output staging must fit");
+  static constexpr int CPR = D / 8;           // 16-byte chunks per row
+  static constexpr int RP = 16 / CPR;         // rows per 256 bytes (the 64-bank span)
+  static constexpr int TILE = 64 * D;         // bf16 elements per K or V tile
+  static constexpr int LOADS = D / 16;        // direct 16-byte loads per thread per tile
+  static constexpr int OSTR = D + 8;          // output staging row
+  static_assert(64 * OSTR <= 2 * TILE, "output staging must fit");
+  __device__ static int fk(int r) { return (r / RP) & (CPR - 1); }
+  __device__ static int fv(int r) { return 2 * ((r / RP) & 3); }
 };
 
-// One thread's share of a K or V tile in flight (16-byte chunks; 128 threads).
-template <int D>
-struct StageRegs {
-  static constexpr int N = D / 16;  // == 4 * VBL as well
-  u32x4 r[N];
-};
-
-template <int D>
-__device__ __forceinline__ void load_k(StageRegs<D>& st, const uint16_t* __restrict__ kp,
-                                       int64_t kss, int j, int tid) {
-  constexpr int CPR = D / 8;  // 16-byte chunks per row
-#pragma unroll
-  for (int e = 0; e < StageRegs<D>::N; ++e) {
-    const int q = tid + 128 * e;
-    const int key = q / CPR, c = q % CPR;
-    st.r[e] = *reinterpret_cast<const u32x4*>(kp + (int64_t)(64 * j + key) * kss + 8 * c);
-  }
+// One 16-byte direct global->LDS load per lane (global_load_lds_dwordx4): lane
+// l writes LDS bytes [lds_base + 16 l, +16).  Issued through inline assembly so
+// that the compiler does not add conservative vmcnt waits in front of every LDS
+// read; the kernel waits for its own loads explicitly (wait_loads) before the
+// barrier that publishes them.
+__device__ __forceinline__ void dma16(uint32_t lds_base, const void* gptr) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_base), "v"(gptr)
+               : "memory", "m0");
 }
 
-template <int D>
-__device__ __forceinline__ void store_k(const StageRegs<D>& st, uint16_t* sK, int tid) {
+__device__ __forceinline__ void wait_loads() {
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's direct loads have landed
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+// Direct load of one 64-row tile: wavefront w, load e covers LDS chunks
+// q = 64 (2e + w) + lane, i.e. row q / CPR, physical chunk q % CPR, which holds
+// global chunk (q % CPR) ^ f(row).
+template <int D, bool IS_V>
+__device__ __forceinline__ void load_tile_lds(uint32_t lds, const uint16_t* __restrict__ tile,
+                                              int ss, int wave_u, int lane) {
   using Lay = Bf16Layout<D>;
-  constexpr int CPR = D / 8;
 #pragma unroll
-  for (int e = 0; e < StageRegs<D>::N; ++e) {
-    const int q = tid + 128 * e;
-    const int key = q / CPR, c = q % CPR;
-    *reinterpret_cast<u32x4*>(sK + key * Lay::KSTR + 8 * c) = st.r[e];
+  for (int e = 0; e < Lay::LOADS; ++e) {
+    const int q = 64 * (2 * e + wave_u) + lane;
+    const int r = q / Lay::CPR;
+    const int pc = q % Lay::CPR;
+    const int gc = pc ^ (IS_V ? Lay::fv(r) : Lay::fk(r));
+    dma16(lds + 1024u * (2 * e + wave_u), tile + r * ss + 8 * gc);
   }
 }
 
-// V is loaded as blocks of 4 consecutive keys x 8 features (four 16-byte rows)
-template <int D>
-__device__ __forceinline__ void load_v(StageRegs<D>& st, const uint16_t* __restrict__ vp,
-                                       int64_t vss, int j, int tid) {
-  constexpr int CPR = D / 8;
-#pragma unroll
-  for (int e = 0; e < Bf16Layout<D>::VBL; ++e) {
-    const int bq = tid + 128 * e;
-    const int kq = bq / CPR, c = bq % CPR;
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr)
-      st.r[4 * e + rr] =
-          *reinterpret_cast<const u32x4*>(vp + (int64_t)(64 * j + 4 * kq + rr) * vss + 8 * c);
-  }
-}
-
-// V^T in LDS: feature row d = 8c + f holds keys 4kq..4kq+3 as one 8-byte store
-template <int D>
-__device__ __forceinline__ void store_v(const StageRegs<D>& st, uint16_t* sVt, int tid) {
-  using Lay = Bf16Layout<D>;
-  constexpr int CPR = D / 8;
-#pragma unroll
-  for (int e = 0; e < Lay::VBL; ++e) {
-    const int bq = tid + 128 * e;
-    const int kq = bq / CPR, c = bq % CPR;
-#pragma unroll
-    for (int f = 0; f < 8; ++f) {
-      const uint32_t sel = (f & 1) ? 0x07060302u : 0x05040100u;
-      const int w = f >> 1;
-      u32x2 pk;
-      pk[0] = __builtin_amdgcn_perm(st.r[4 * e + 1][w], st.r[4 * e + 0][w], sel);
-      pk[1] = __builtin_amdgcn_perm(st.r[4 * e + 3][w], st.r[4 * e + 2][w], sel);
-      *reinterpret_cast<u32x2*>(sVt + (8 * c + f) * Lay::VSTR + 4 * kq) = pk;
-    }
-  }
-}
+// Sparse rows read their key-block list through a 256-entry LDS window, so the
+// loop issues no vector-memory loads of its own (whose waits would also drain
+// the tile loads in flight).
+constexpr int kListChunk = 256;
 
 // Two workgroups' worth of wavefronts per SIMD (<= 256 registers per lane) so
 // that one wavefront's softmax overlaps another's MFMA work.
 //
-// Pipeline per key tile n (single LDS buffer, two barriers):
-//   S = K_n Q^T from LDS                    (K_{n+1} loads in flight)
-//   barrier A -> store K_{n+1}; issue V_{n+1} loads
-//   softmax, O += V_n^T P^T from LDS
-//   barrier B -> store V_{n+1}; issue K_{n+2} loads
-// K_{n+1} becomes visible to S_{n+1} through barrier B, V_{n+1} to PV_{n+1}
-// through the next barrier A; K and V staging share one set of registers.
+// Pipeline per key tile n (one K and one V buffer, two barriers):
+//   S = K_n Q^T from LDS                  (V_n landing)
+//   wait + barrier A -> issue K_{n+1}     (V_n visible; K_n consumed)
+//   softmax, O += V_n^T P^T from LDS      (K_{n+1} landing)
+//   wait + barrier B -> issue V_{n+1}     (K_{n+1} visible; V_n consumed)
+// Operand reads are issued two MFMAs ahead of their use.
+//
+// Softmax rescaling is lazy: the running max of a query only moves (and O, l
+// are only rescaled) when some lane's tile max exceeds it by more than 2^8 in
+// the exp2 domain; otherwise probabilities up to 2^8 are accumulated against
+// the stale max, which leaves O / l unchanged.
 template <int D, bool SPARSE>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_bf16_kernel(KernelArgs ka) {
   using Lay = Bf16Layout<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[(Lay::K_BYTES + Lay::V_BYTES) / 2];
-  uint16_t* sK = smem;
-  uint16_t* sVt = smem + Lay::K_BYTES / 2;
+  __shared__ __attribute__((aligned(16))) uint16_t sK[Lay::TILE];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[Lay::TILE];
+  __shared__ uint16_t sList[SPARSE ? kListChunk : 1];
 
   const AttnArgs& a = ka.a;
   const Task t = decode_task(ka.map, blockIdx.x);
   const int tid = threadIdx.x;
   const int wave = tid / 64;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const int lane = tid % 64;
   const int hf = lane / 32;
   const int col = lane % 32;
   const int G = a.heads_q / a.heads_kv;
   const int g = t.h / G;
+  const int kss = (int)a.k.ss, vss = (int)a.v.ss;
+  const uint32_t sK_a = lds_addr(sK), sV_a = lds_addr(sV);
 
   const uint16_t* qp = static_cast<const uint16_t*>(a.q.ptr) + t.b * a.q.sb + t.h * a.q.sh;
   const uint16_t* kp = static_cast<const uint16_t*>(a.k.ptr) + t.b * a.k.sb + g * a.k.sh;
   const uint16_t* vp = static_cast<const uint16_t*>(a.v.ptr) + t.b * a.v.sb + g * a.v.sh;
+  const int64_t ktile = 64 * a.k.ss, vtile = 64 * a.v.ss;
 
   // Q^T operand: lane holds query q0 + col, features 16ks + 8hf .. +7
   const int qrow = 64 * t.i + 32 * wave + col;
@@ -265,47 +270,87 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   float m_run = -INFINITY, l_run = 0.f;
   const float c = ka.scale_log2;
 
-  // key blocks are read one step ahead; the first out-of-range entry ends the row
-  const RowList<SPARSE> list = make_list<SPARSE>(a, t);
-  auto next_j = [&](int p) -> int {
-    if (p >= list.n) return -1;
-    const int j = list.at(p);
-    return list.ok(j) ? j : -1;
-  };
-  int j = next_j(0);
-  int jn = (j >= 0) ? next_j(1) : -1;
+  // Per-lane LDS element offsets of the operand reads.  K: row 32mt + col, chunk
+  // 2ks + hf (the swizzle depends on col only; mt adds 32 rows).  V (transposed
+  // read): rows 32(kt/2) + 16(kt%2) + {0, 8} + 4hf + r4, features 32dt + d0; the
+  // swizzle depends on the lane only, the rest are immediate offsets.
+  int koff[D / 16];
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) koff[ks] = col * D + 8 * ((2 * ks + hf) ^ Lay::fk(col));
+  const int r16 = lane % 16;
+  const int r4 = r16 / 4;
+  const int d0 = 4 * (r16 % 4) + 16 * ((lane / 16) % 2);
+  const int vrow = 4 * hf + r4;
+  const int fvl = Lay::fv(vrow);
+  int voff[D / 32];
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt) voff[dt] = vrow * D + 8 * ((4 * dt + d0 / 8) ^ fvl) + d0 % 8;
 
-  StageRegs<D> st;
+  // row list
+  const RowList<SPARSE> list = make_list<SPARSE>(a, t);
+  auto fetch_chunk = [&](int base) {  // entries [base, base + kListChunk) of the row list
+    if (SPARSE) {
+      for (int p = tid; p < kListChunk; p += 128)
+        if (base + p < list.n) sList[p] = list.idx[base + p];
+    }
+  };
+  auto entry = [&](int p) -> int {  // p must lie in the current LDS window
+    if (p >= list.n) return -1;
+    const int jj = SPARSE ? (int)sList[p % kListChunk] : p;
+    return list.ok(jj) ? jj : -1;
+  };
+  fetch_chunk(0);
+  __syncthreads();
+  int j = entry(0);
+  int jn = (j >= 0) ? entry(1) : -1;
+
   if (j >= 0) {
-    load_k<D>(st, kp, a.k.ss, j, tid);
-    store_k<D>(st, sK, tid);
-    load_v<D>(st, vp, a.v.ss, j, tid);
-    store_v<D>(st, sVt, tid);
-    if (jn >= 0) load_k<D>(st, kp, a.k.ss, jn, tid);
+    load_tile_lds<D, false>(sK_a, kp + j * ktile, kss, wave_u, lane);
+    load_tile_lds<D, true>(sV_a, vp + j * vtile, vss, wave_u, lane);
   }
+  wait_loads();  // also retires the Q loads: nothing the loop body waits on is pending
   __syncthreads();
 
   for (int n = 0; j >= 0; ++n) {
-    const int jnn = (jn >= 0) ? next_j(n + 2) : -1;
+    int jnn = -1;
+    if (jn >= 0) {
+      if (SPARSE && (n + 2) % kListChunk == 0 && n + 2 < list.n) {
+        fetch_chunk(n + 2);  // every thread has read entry n + 1 already
+        wait_loads();
+        __syncthreads();
+      }
+      jnn = entry(n + 2);
+    }
 
-    // S^T = K Q^T: two 32-key halves of the tile
+    // S^T = K Q^T: two 32-key halves of the tile, operands read two steps ahead
     f32x16 s[2];
 #pragma unroll
-    for (int mt = 0; mt < 2; ++mt) {
+    for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[mt][e] = 0.f;
+    constexpr int NS = 2 * (D / 16);
+    bf16x8 kf[NS];
 #pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 kf =
-            *reinterpret_cast<const bf16x8*>(sK + (32 * mt + col) * Lay::KSTR + 16 * ks + 8 * hf);
-        s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[ks], s[mt], 0, 0, 0);
-      }
+    for (int st = 0; st < NS; ++st) {
+      const int mt = st / (D / 16), ks = st % (D / 16);
+      kf[st] = *reinterpret_cast<const bf16x8*>(sK + 32 * mt * D + koff[ks]);
     }
-    __syncthreads();  // A: K_n fully consumed
-    if (jn >= 0) {
-      store_k<D>(st, sK, tid);
-      load_v<D>(st, vp, a.v.ss, jn, tid);
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      const int mt = st / (D / 16), ks = st % (D / 16);
+      s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[ks], s[mt], 0, 0, 0);
     }
+    // schedule: K reads run four MFMAs ahead
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int st = 0; st < NS - 4; ++st) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    wait_loads();
+    __syncthreads();  // A: K_n consumed, V_n visible
+    if (jn >= 0) load_tile_lds<D, false>(sK_a, kp + jn * ktile, kss, wave_u, lane);
 
     if (a.causal && j == t.i) {  // diagonal tile: key kl visible to query ql iff kl <= ql
       const int ql = 32 * wave + col;
@@ -317,36 +362,68 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
           if (kl > ql) s[mt][e] = -INFINITY;
         }
     }
-    const float alpha = softmax_tile(s, m_run, l_run, c);
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
 
-    // P^T operand: k-step kt covers keys 32*(kt/2) + 16*(kt%2) + {4hf+0..3, 8+4hf+0..3},
-    // exactly accumulators 8*(kt%2) .. +7 of half kt/2
+    // online softmax (lazy rescale)
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mloc = fmaxf(mloc, s[mt][e]);
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+    if (__ballot((mloc - m_run) * c > 8.0f)) {
+      const float m_new = fmaxf(m_run, mloc);
+      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
+    }
+    const float mc = (m_run == -INFINITY) ? 0.f : m_run * c;
+    // P^T operand of k-step kt: accumulators 8(kt%2)..+7 of half kt/2, i.e. keys
+    // 32(kt/2) + 16(kt%2) + {4hf + 0..3, 8 + 4hf + 0..3}
     bf16x8 pb[4];
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pb[kt][e] = (__bf16)s[kt / 2][8 * (kt % 2) + e];
-
-    // O^T += V^T P^T; the V^T operand row is feature d = 32dt + col with the same keys
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt) {
-        const uint16_t* vr = sVt + (32 * dt + col) * Lay::VSTR + 32 * (kt / 2) + 16 * (kt % 2) + 4 * hf;
-        const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vr);
-        const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vr + 8);
-        const bf16x8 vf = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kt], acc[dt], 0, 0, 0);
+      for (int e = 0; e < 8; ++e) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s[kt / 2][8 * (kt % 2) + e], c, -mc));
+        l_run += p;
+        pb[kt][e] = (__bf16)p;
       }
-    __syncthreads();  // B: V_n fully consumed, K_{n+1} visible
-    if (jn >= 0) {
-      store_v<D>(st, sVt, tid);
-      if (jnn >= 0) load_k<D>(st, kp, a.k.ss, jnn, tid);
+
+    // O^T += V^T P^T; V^T operand: feature 32dt + col, the same keys as pb[kt]
+    auto vread = [&](int st) -> bf16x8 {
+      const int dt = st / 4, kt = st % 4;
+      const int rows = 32 * (kt / 2) + 16 * (kt % 2);
+      const uint16_t* base = sV + rows * D + voff[dt];
+      const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)base);
+      const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+          (__attribute__((address_space(3))) s16x4*)(base + 8 * D));
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    constexpr int NV = 4 * (D / 32);
+    bf16x8 vf0 = vread(0), vf1 = vread(1);
+#pragma unroll
+    for (int st = 0; st < NV; ++st) {
+      bf16x8 vf2;
+      if (st + 2 < NV) vf2 = vread(st + 2);
+      acc[st / 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf0, pb[st % 4], acc[st / 4], 0, 0, 0);
+      vf0 = vf1;
+      vf1 = vf2;
     }
+    // schedule: transposed V reads run two MFMAs ahead
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int st = 0; st < NV - 2; ++st) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    wait_loads();
+    __syncthreads();  // B: V_n consumed, K_{n+1} visible
+    if (jn >= 0) load_tile_lds<D, true>(sV_a, vp + jn * vtile, vss, wave_u, lane);
     j = jn;
     jn = jnn;
   }
@@ -354,8 +431,9 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   // epilogue: normalise, stage through LDS, store rows with 16-byte writes
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = (l_tot > 0.f) ? 1.0f / l_tot : 0.f;
+  wait_loads();
   __syncthreads();
-  uint16_t* sO = smem;
+  uint16_t* sO = sK;  // sK and sV are adjacent: 2 tiles of staging room
   const int ql = 32 * wave + col;
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt)
@@ -368,11 +446,10 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     }
   __syncthreads();
   uint16_t* op = static_cast<uint16_t*>(a.o) + t.b * a.osb + t.h * a.osh;
-  constexpr int CPR = D / 8;
 #pragma unroll
-  for (int e = 0; e < 64 * CPR / 128; ++e) {
+  for (int e = 0; e < 64 * Lay::CPR / 128; ++e) {
     const int q = tid + 128 * e;
-    const int r = q / CPR, cc = q % CPR;
+    const int r = q / Lay::CPR, cc = q % Lay::CPR;
     *reinterpret_cast<u32x4*>(op + (int64_t)(64 * t.i + r) * a.oss + 8 * cc) =
         *reinterpret_cast<const u32x4*>(sO + r * Lay::OSTR + 8 * cc);
   }
@@ -506,32 +583,35 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
   }
 }
 
-static int gcd_int(int x, int y) {
-  while (y) {
-    const int r = x % y;
-    x = y;
-    y = r;
-  }
-  return x;
-}
-
+// Groups per phase: the largest power of two whose K + V stay within 64 MiB
+// (a quarter of the 256 MB Infinity Cache); each group is then spread over
+// R = 8 / gpp XCDs.  Measured at 131072 tokens (64 MiB of K + V per group):
+// one group at a time over all 8 XCDs beat one group per XCD by 11% (sparse)
+// and 7% (dense).
+#ifndef SEER_KV_PHASE_BUDGET_MB
+#define SEER_KV_PHASE_BUDGET_MB 64
+#endif
 static TaskMap make_map(const AttnArgs& a) {
   TaskMap m;
   m.batch = a.batch;
   m.heads_q = a.heads_q;
   m.heads_kv = a.heads_kv;
   m.nb = a.n_blocks;
+  m.R = 0;
+  m.gpp = 0;
+  m.tpp = 0;
   const int slices = a.batch * a.heads_kv;
-  const int R = 8 / gcd_int(slices, 8);
-  const int64_t total = (int64_t)a.batch * a.heads_q * a.n_blocks;
-  if (a.n_blocks % R == 0 && total % 8 == 0) {
+  const int G = a.heads_q / a.heads_kv;
+  const double kv_bytes = 2.0 * a.n_blocks * 64.0 * a.head_dim * (a.bf16 ? 2 : 4);
+  const double budget = SEER_KV_PHASE_BUDGET_MB * 1024.0 * 1024.0;
+  for (int gpp = 8; gpp >= 1; gpp /= 2) {
+    const int R = 8 / gpp;
+    if (slices % gpp != 0 || a.n_blocks % R != 0) continue;
+    if (gpp > 1 && gpp * kv_bytes > budget) continue;
     m.R = R;
-    m.lanes_x = slices * R / 8;
-    m.per_xcd = (int)(total / 8);
-  } else {
-    m.R = 0;
-    m.lanes_x = 0;
-    m.per_xcd = 0;
+    m.gpp = gpp;
+    m.tpp = (a.n_blocks / R) * G;
+    break;
   }
   return m;
 }
