@@ -176,12 +176,12 @@ struct Bf16Layout {
 };
 
 // One 16-byte direct global->LDS load per lane (global_load_lds_dwordx4): lane
-// l writes LDS bytes [lds_base + 16 l, +16).  Issued through inline assembly so
-// that the compiler does not add conservative vmcnt waits in front of every LDS
-// read; the kernel waits for its own loads explicitly (wait_loads) before the
-// barrier that publishes them.
-__device__ __forceinline__ void dma16(uint32_t lds_base, const void* gptr) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_base), "v"(gptr)
+// l writes LDS bytes [lds_base + 16 l, +16) from global address base + voff.
+// Issued through inline assembly so that the compiler does not add
+// conservative vmcnt waits in front of every LDS read; the kernel waits for
+// its own loads explicitly (wait_loads) before the barrier that publishes them.
+__device__ __forceinline__ void dma16(uint32_t lds_base, const void* base, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds_base), "v"(voff), "s"(base)
                : "memory", "m0");
 }
 
@@ -193,21 +193,29 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
 }
 
-// Direct load of one 64-row tile: wavefront w, load e covers LDS chunks
-// q = 64 (2e + w) + lane, i.e. row q / CPR, physical chunk q % CPR, which holds
-// global chunk (q % CPR) ^ f(row).
+// Direct load of one 64-row tile.  Wavefront w, load e covers LDS chunks
+// q = 64 (2e + w) + lane: row q / CPR, physical chunk q % CPR, which holds
+// global chunk (q % CPR) ^ f(row).  Since 128 e is a multiple of CPR, the row
+// is 128e / CPR + (64w + lane) / CPR: the first term is uniform (folded into
+// the scalar base) and the swizzle f depends on e only through e & 1, so each
+// lane needs two byte offsets per tensor, computed once (dma_offsets).
 template <int D, bool IS_V>
+__device__ __forceinline__ uint32_t dma_offset(int ss, int wave, int lane, int e_parity) {
+  using Lay = Bf16Layout<D>;
+  const int ql = 64 * wave + lane;
+  const int r = 128 * e_parity / Lay::CPR + ql / Lay::CPR;
+  const int pc = ql % Lay::CPR;
+  const int gc = pc ^ (IS_V ? Lay::fv(r) : Lay::fk(r));
+  return (uint32_t)(((ql / Lay::CPR) * ss + 8 * gc) * 2);
+}
+
+template <int D>
 __device__ __forceinline__ void load_tile_lds(uint32_t lds, const uint16_t* __restrict__ tile,
-                                              int ss, int wave_u, int lane) {
+                                              int ss, int wave_u, const uint32_t (&off)[2]) {
   using Lay = Bf16Layout<D>;
 #pragma unroll
-  for (int e = 0; e < Lay::LOADS; ++e) {
-    const int q = 64 * (2 * e + wave_u) + lane;
-    const int r = q / Lay::CPR;
-    const int pc = q % Lay::CPR;
-    const int gc = pc ^ (IS_V ? Lay::fv(r) : Lay::fk(r));
-    dma16(lds + 1024u * (2 * e + wave_u), tile + r * ss + 8 * gc);
-  }
+  for (int e = 0; e < Lay::LOADS; ++e)
+    dma16(lds + 1024u * (2 * e + wave_u), tile + (int64_t)(128 * e / Lay::CPR) * ss, off[e & 1]);
 }
 
 // Sparse rows read their key-block list through a 256-entry LDS window, so the
@@ -249,6 +257,8 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   const int g = t.h / G;
   const int kss = (int)a.k.ss, vss = (int)a.v.ss;
   const uint32_t sK_a = lds_addr(sK), sV_a = lds_addr(sV);
+  const uint32_t koffd[2] = {dma_offset<D, false>(kss, wave, lane, 0), dma_offset<D, false>(kss, wave, lane, 1)};
+  const uint32_t voffd[2] = {dma_offset<D, true>(vss, wave, lane, 0), dma_offset<D, true>(vss, wave, lane, 1)};
 
   const uint16_t* qp = static_cast<const uint16_t*>(a.q.ptr) + t.b * a.q.sb + t.h * a.q.sh;
   const uint16_t* kp = static_cast<const uint16_t*>(a.k.ptr) + t.b * a.k.sb + g * a.k.sh;
@@ -305,8 +315,8 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   int jn = (j >= 0) ? entry(1) : -1;
 
   if (j >= 0) {
-    load_tile_lds<D, false>(sK_a, kp + j * ktile, kss, wave_u, lane);
-    load_tile_lds<D, true>(sV_a, vp + j * vtile, vss, wave_u, lane);
+    load_tile_lds<D>(sK_a, kp + j * ktile, kss, wave_u, koffd);
+    load_tile_lds<D>(sV_a, vp + j * vtile, vss, wave_u, voffd);
   }
   wait_loads();  // also retires the Q loads: nothing the loop body waits on is pending
   __syncthreads();
@@ -350,7 +360,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
     wait_loads();
     __syncthreads();  // A: K_n consumed, V_n visible
-    if (jn >= 0) load_tile_lds<D, false>(sK_a, kp + jn * ktile, kss, wave_u, lane);
+    if (jn >= 0) load_tile_lds<D>(sK_a, kp + jn * ktile, kss, wave_u, koffd);
 
     if (a.causal && j == t.i) {  // diagonal tile: key kl visible to query ql iff kl <= ql
       const int ql = 32 * wave + col;
@@ -423,7 +433,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     wait_loads();
     __syncthreads();  // B: V_n consumed, K_{n+1} visible
-    if (jn >= 0) load_tile_lds<D, true>(sV_a, vp + jn * vtile, vss, wave_u, lane);
+    if (jn >= 0) load_tile_lds<D>(sV_a, vp + jn * vtile, vss, wave_u, voffd);
     j = jn;
     jn = jnn;
   }
