@@ -313,15 +313,48 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   __syncthreads();
   int j = entry(0);
   int jn = (j >= 0) ? entry(1) : -1;
+  int n = 0;
 
+  // S^T = K Q^T for the tile in sK (two 32-key halves).  With `interleave`,
+  // the reads and MFMAs are issued in the same scheduling region as the
+  // softmax VALU work of the previous tile (see below).
+  constexpr int NS = 2 * (D / 16);
+  auto s_product = [&](f32x16 (&sn)[2]) {
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sn[mt][e] = 0.f;
+    bf16x8 kf[NS];
+#pragma unroll
+    for (int st = 0; st < NS; ++st)
+      kf[st] = *reinterpret_cast<const bf16x8*>(sK + 32 * (st / (D / 16)) * D + koff[st % (D / 16)]);
+#pragma unroll
+    for (int st = 0; st < NS; ++st) {
+      const int mt = st / (D / 16), ks = st % (D / 16);
+      sn[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[ks], sn[mt], 0, 0, 0);
+    }
+  };
+
+  f32x16 sA[2], sB[2];
   if (j >= 0) {
     load_tile_lds<D>(sK_a, kp + j * ktile, kss, wave_u, koffd);
     load_tile_lds<D>(sV_a, vp + j * vtile, vss, wave_u, voffd);
   }
   wait_loads();  // also retires the Q loads: nothing the loop body waits on is pending
   __syncthreads();
+  if (j >= 0) s_product(sA);
+  __syncthreads();  // K_j consumed
+  if (jn >= 0) load_tile_lds<D>(sK_a, kp + jn * ktile, kss, wave_u, koffd);
+  wait_loads();
+  __syncthreads();  // K_jn (and V_j) visible
 
-  for (int n = 0; j >= 0; ++n) {
+  // One tile j.  On entry: sc holds S for tile j, sK holds K_jn, sV holds V_j
+  // (its load may still be in flight), a load of nothing else is pending.
+  //   softmax(S_j) on VALU || S_jn = K_jn Q^T on MFMA      (one scheduling region)
+  //   wait + barrier M -> issue K_jnn                       (V_j visible; K_jn consumed)
+  //   O += V_j^T P_j^T
+  //   wait + barrier E -> issue V_jn                        (K_jnn visible; V_j consumed)
+  auto tile = [&](f32x16 (&sc)[2], f32x16 (&sn)[2]) {
     int jnn = -1;
     if (jn >= 0) {
       if (SPARSE && (n + 2) % kListChunk == 0 && n + 2 < list.n) {
@@ -331,37 +364,6 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
       }
       jnn = entry(n + 2);
     }
-
-    // S^T = K Q^T: two 32-key halves of the tile, operands read two steps ahead
-    f32x16 s[2];
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) s[mt][e] = 0.f;
-    constexpr int NS = 2 * (D / 16);
-    bf16x8 kf[NS];
-#pragma unroll
-    for (int st = 0; st < NS; ++st) {
-      const int mt = st / (D / 16), ks = st % (D / 16);
-      kf[st] = *reinterpret_cast<const bf16x8*>(sK + 32 * mt * D + koff[ks]);
-    }
-#pragma unroll
-    for (int st = 0; st < NS; ++st) {
-      const int mt = st / (D / 16), ks = st % (D / 16);
-      s[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[ks], s[mt], 0, 0, 0);
-    }
-    // schedule: K reads run four MFMAs ahead
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-    for (int st = 0; st < NS - 4; ++st) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    wait_loads();
-    __syncthreads();  // A: K_n consumed, V_n visible
-    if (jn >= 0) load_tile_lds<D>(sK_a, kp + jn * ktile, kss, wave_u, koffd);
-
     if (a.causal && j == t.i) {  // diagonal tile: key kl visible to query ql iff kl <= ql
       const int ql = 32 * wave + col;
 #pragma unroll
@@ -369,16 +371,15 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kl = 32 * mt + 8 * (e / 4) + 4 * hf + (e % 4);
-          if (kl > ql) s[mt][e] = -INFINITY;
+          if (kl > ql) sc[mt][e] = -INFINITY;
         }
     }
-
     // online softmax (lazy rescale)
     float mloc = -INFINITY;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mloc = fmaxf(mloc, s[mt][e]);
+      for (int e = 0; e < 16; ++e) mloc = fmaxf(mloc, sc[mt][e]);
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
     if (__ballot((mloc - m_run) * c > 8.0f)) {
       const float m_new = fmaxf(m_run, mloc);
@@ -391,6 +392,9 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
         for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
     }
     const float mc = (m_run == -INFINITY) ? 0.f : m_run * c;
+
+    // S for the next tile (harmless junk when there is none)
+    s_product(sn);
     // P^T operand of k-step kt: accumulators 8(kt%2)..+7 of half kt/2, i.e. keys
     // 32(kt/2) + 16(kt%2) + {4hf + 0..3, 8 + 4hf + 0..3}
     bf16x8 pb[4];
@@ -398,10 +402,30 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[kt / 2][8 * (kt % 2) + e], c, -mc));
+        const float p = __builtin_amdgcn_exp2f(fmaf(sc[kt / 2][8 * (kt % 2) + e], c, -mc));
         l_run += p;
         pb[kt][e] = (__bf16)p;
       }
+    // schedule: four K reads ahead, then each MFMA of the next tile's S with
+    // seven VALU instructions of this tile's softmax
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int st = 0; st < NS - 4; ++st) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
+    }
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 7, 0);
+    }
+    // keep the softmax and the next S in this region: arithmetic is otherwise
+    // free to sink past the barrier into the P.V region
+    asm volatile("" ::"v"(pb[0]), "v"(pb[1]), "v"(pb[2]), "v"(pb[3]), "v"(l_run), "v"(sn[0]), "v"(sn[1]));
+    wait_loads();
+    __syncthreads();  // M: V_j visible, K_jn consumed
+    if (jnn >= 0) load_tile_lds<D>(sK_a, kp + jnn * ktile, kss, wave_u, koffd);
 
     // O^T += V^T P^T; V^T operand: feature 32dt + col, the same keys as pb[kt]
     auto vread = [&](int st) -> bf16x8 {
@@ -432,10 +456,18 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     wait_loads();
-    __syncthreads();  // B: V_n consumed, K_{n+1} visible
+    __syncthreads();  // E: V_j consumed, K_jnn visible
     if (jn >= 0) load_tile_lds<D>(sV_a, vp + jn * vtile, vss, wave_u, voffd);
     j = jn;
     jn = jnn;
+    ++n;
+  };
+
+  // unrolled twice so that the two S buffers swap roles without copies
+  while (j >= 0) {
+    tile(sA, sB);
+    if (j < 0) break;
+    tile(sB, sA);
   }
 
   // epilogue: normalise, stage through LDS, store rows with 16-byte writes
