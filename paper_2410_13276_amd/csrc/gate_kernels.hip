@@ -282,28 +282,34 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   const int i = (int)(row % nb);
   const int h = (int)((row / nb) % a.heads_q);
   const float* L = a.logits + row * nb;
+  const int M = i / 64 + 1;  // words holding the causal blocks j <= i (wave-uniform)
 
   // per-lane bit m describes block j = 64m + lane
   float v[MAXM];
   uint64_t valid = 0, forced = 0;
 #pragma unroll
   for (int m = 0; m < MAXM; ++m) {
-    const int j = 64 * m + lane;
-    const bool ok = j <= i;
-    v[m] = ok ? L[j] : -INFINITY;
-    valid |= (uint64_t)ok << m;
-    forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
+    v[m] = -INFINITY;
+    if (m < M) {
+      const int j = 64 * m + lane;
+      const bool ok = j <= i;
+      if (ok) v[m] = L[j];
+      valid |= (uint64_t)ok << m;
+      forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
+    }
   }
   uint64_t sel = forced;
 
   if (a.mode == 2) {  // threshold on the softmax probability (Eq. 4, strict)
     float mx = -INFINITY;
 #pragma unroll
-    for (int m = 0; m < MAXM; ++m) mx = fmaxf(mx, v[m]);
+    for (int m = 0; m < MAXM; ++m)
+      if (m < M) mx = fmaxf(mx, v[m]);
     mx = wave_max(mx);
     float s = 0.f;
 #pragma unroll
-    for (int m = 0; m < MAXM; ++m) s += ((valid >> m) & 1) ? __expf(v[m] - mx) : 0.f;
+    for (int m = 0; m < MAXM; ++m)
+      if (m < M) s += ((valid >> m) & 1) ? __expf(v[m] - mx) : 0.f;
     s = wave_sum(s);
     const float lse = mx + __logf(s);
     const float t = a.head_thresholds ? a.head_thresholds[h] : a.threshold;
@@ -312,7 +318,8 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
     } else {
       const float lt = __logf(t);
 #pragma unroll
-      for (int m = 0; m < MAXM; ++m) sel |= (uint64_t)(((valid >> m) & 1) && (v[m] - lse) > lt) << m;
+      for (int m = 0; m < MAXM; ++m)
+        if (m < M) sel |= (uint64_t)(((valid >> m) & 1) && (v[m] - lse) > lt) << m;
     }
   } else {  // TopK (Eq. 3) over the non-forced causal blocks
     const int nf = (a.keep_first ? 1 : 0) + ((a.keep_diag && !(a.keep_first && i == 0)) ? 1 : 0);
@@ -324,31 +331,48 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
     if (take >= ncand) {
       sel = valid;
     } else if (take > 0) {
-      // largest T with #{candidates : key >= T} >= take, built one bit at a time
+      uint32_t key[MAXM];
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m) key[m] = ((cand >> m) & 1) ? ordered_key(v[m]) : 0u;
+      // Largest T with #{candidates : key >= T} >= take, one bit at a time.  Once
+      // exactly `take` candidates lie at or above the current prefix, the
+      // selected set is fixed and the remaining bits cannot change it.
       uint32_t T = 0;
-      for (int bit = 31; bit >= 0; --bit) {
+      int cntT = ncand;
+      for (int bit = 31; bit >= 0 && cntT != take; --bit) {
         const uint32_t trial = T | (1u << bit);
         int cnt = 0;
 #pragma unroll
         for (int m = 0; m < MAXM; ++m)
-          cnt += __popcll(__ballot(((cand >> m) & 1) && ordered_key(v[m]) >= trial));
-        if (cnt >= take) T = trial;
+          if (m < M) cnt += __popcll(__ballot(((cand >> m) & 1) && key[m] >= trial));
+        if (cnt >= take) {
+          T = trial;
+          cntT = cnt;
+        }
       }
       int gt = 0;
+      if (cntT != take) {
 #pragma unroll
-      for (int m = 0; m < MAXM; ++m) gt += __popcll(__ballot(((cand >> m) & 1) && ordered_key(v[m]) > T));
-      const int need = take - gt;  // blocks taken among those tied at T, smallest j first
+        for (int m = 0; m < MAXM; ++m)
+          if (m < M) gt += __popcll(__ballot(((cand >> m) & 1) && key[m] > T));
+      }
+      // everything >= T when the set closed early; otherwise everything > T
+      // plus the (take - gt) smallest-index candidates tied at T
+      const int need = (cntT == take) ? 0 : take - gt;
+      const uint32_t strict_from = (cntT == take) ? T : T + 1;  // key >= strict_from is taken
       const uint64_t lt = lanemask_lt();
       int before = 0;
 #pragma unroll
       for (int m = 0; m < MAXM; ++m) {
-        const bool c = (cand >> m) & 1;
-        const uint32_t key = ordered_key(v[m]);
-        const bool eq = c && key == T;
-        const uint64_t bal = __ballot(eq);
-        const int rank = before + __popcll(bal & lt);
-        sel |= (uint64_t)(c && (key > T || (eq && rank < need))) << m;
-        before += __popcll(bal);
+        if (m < M) {
+          const bool c = (cand >> m) & 1;
+          const bool above = c && key[m] >= strict_from && (cntT == take || key[m] != T);
+          const bool eq = c && cntT != take && key[m] == T;
+          const uint64_t bal = __ballot(eq);
+          const int rank = before + __popcll(bal & lt);
+          sel |= (uint64_t)(above || (eq && rank < need)) << m;
+          before += __popcll(bal);
+        }
       }
     }
   }
