@@ -54,6 +54,8 @@ def lib():
         L.orc_pool.restype = i
         L.orc_linear.argtypes = [p, i, i, i, i, p, i, i, p]
         L.orc_linear.restype = None
+        L.orc_block_rope.argtypes = [p, C.c_int64, i, i, C.c_double, i]
+        L.orc_block_rope.restype = None
         L.orc_gate_logits.argtypes = [p, p, i, i, i, i, i, p]
         L.orc_gate_logits.restype = None
         L.orc_gate_logscore.argtypes = [p, C.c_int64, i, p]
@@ -118,6 +120,14 @@ def linear(pooled: np.ndarray, W: np.ndarray, w_per_head: bool = True) -> np.nda
     return out
 
 
+def block_rope(x: np.ndarray, theta: float, block: int = 64) -> np.ndarray:
+    """Block-level RoPE of gate rows [B, H, nb, Dg] (a rotated copy)."""
+    x = np.array(x, dtype=np.float64, order="C", copy=True)
+    B, H, nb, Dg = x.shape
+    lib().orc_block_rope(_ptr(x), B * H, nb, Dg, float(theta), int(block))
+    return x
+
+
 def gate_logits(Qg: np.ndarray, Kg: np.ndarray) -> np.ndarray:
     Qg = np.ascontiguousarray(Qg, dtype=np.float64)
     Kg = np.ascontiguousarray(Kg, dtype=np.float64)
@@ -166,12 +176,16 @@ def select(ell: np.ndarray, mode: int, rho: float = 0.0, k: int = 0,
 
 
 def gate(q: np.ndarray, k: np.ndarray, wq: np.ndarray, wk: np.ndarray, block: int = 64,
-         w_per_head: bool = True):
-    """Pool, linear and logits of the gate.  Returns (L, ell) [B, Hq, nb, nb]."""
+         w_per_head: bool = True, rope_theta: float = 0.0):
+    """Pool, linear, optional block-level RoPE (rope_theta > 0) and logits of the
+    gate.  Returns (L, ell) [B, Hq, nb, nb]."""
     qp = pool(q, block, POOL_AVG)
     kp = pool(k, block, POOL_MAX_MIN_AVG)
     qg = linear(qp, wq, w_per_head)
     kg = linear(kp, wk, w_per_head)
+    if rope_theta > 0:
+        qg = block_rope(qg, rope_theta, block)
+        kg = block_rope(kg, rope_theta, block)
     L = gate_logits(qg, kg)
     return L, gate_logscore(L)
 

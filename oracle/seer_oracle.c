@@ -18,6 +18,10 @@
  *                        (order: max | min | avg).
  *   orc_linear        -- Eq. 1: the learnable linear layers W_q, W_k applied to
  *                        the pooled tensors (no bias term appears in Eq. 1).
+ *   orc_block_rope    -- section 3.1 "Block-level RoPE in AttnGate": the gate is
+ *                        fed pre-RoPE Q and K and rotates the projected rows at
+ *                        their block positions with the reduced base theta / B
+ *                        (rotate-half pairing (d, d + Dg/2) as in Llama).
  *   orc_gate_logits   -- Eq. 1: (W_q P_q(Q)) . (W_k P_k(K))^T / sqrt(d), with d
  *                        the contracted (gate) dimension, block-causal.
  *   orc_gate_logscore -- Eq. 1: the row softmax, returned in log form
@@ -132,6 +136,29 @@ void orc_linear(const double *in, int B, int H, int nb, int din,
           for (int c = 0; c < din; ++c) acc += p[c] * (double)w[(int64_t)c * dout + j];
           o[j] = acc;
         }
+      }
+    }
+}
+
+/*
+ * Block-level RoPE (section 3.1): row i of x [rows][nb][Dg] (in place) is the
+ * gate feature vector of block i; it is rotated by angle i * w_d in each plane
+ * (d, d + Dg/2), d < Dg/2, with w_d = (theta / block)^(-2d/Dg).  theta is the
+ * model's RoPE base; block is the pooling block size B.
+ */
+void orc_block_rope(double *x, int64_t rows, int nb, int Dg, double theta, int block) {
+  const int half = Dg / 2;
+  const double base = theta / block;
+  for (int64_t r = 0; r < rows; ++r)
+    for (int i = 0; i < nb; ++i) {
+      double *v = x + (r * nb + i) * Dg;
+      for (int d = 0; d < half; ++d) {
+        const double w = pow(base, -2.0 * d / Dg);
+        const double ang = (double)i * w;
+        const double c = cos(ang), s = sin(ang);
+        const double a = v[d], b = v[d + half];
+        v[d] = a * c - b * s;
+        v[d + half] = a * s + b * c;
       }
     }
 }

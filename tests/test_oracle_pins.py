@@ -434,3 +434,53 @@ def test_maxpool_gt_matches_torch():
     p = torch.softmax(sc, -1)
     ref = F.max_pool2d(p, blk, blk).numpy()
     np.testing.assert_allclose(gt, ref, rtol=1e-12, atol=0)
+
+
+# --------------------------------------------------------------------------
+# block-level RoPE in the gate (section 3.1)
+# --------------------------------------------------------------------------
+
+def test_block_rope_matches_complex_rotation():
+    # independent formulation: plane (d, d + Dg/2) as the complex number
+    # x_d + i x_{d+Dg/2}, multiplied by exp(i * pos * (theta/B)^(-2d/Dg))
+    B, H, nb, Dg, theta, blk = 1, 2, 37, 16, 500000.0, 64
+    x = np.random.default_rng(90).standard_normal((B, H, nb, Dg))
+    y = oracle.block_rope(x, theta, blk)
+    half = Dg // 2
+    z = x[..., :half] + 1j * x[..., half:]
+    w = (theta / blk) ** (-2.0 * np.arange(half) / Dg)
+    rot = np.exp(1j * np.arange(nb)[:, None] * w[None, :])
+    zr = z * rot
+    np.testing.assert_allclose(y[..., :half], zr.real, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(y[..., half:], zr.imag, rtol=1e-12, atol=1e-12)
+
+
+def test_block_rope_invariants():
+    B, H, nb, Dg = 1, 3, 50, 32
+    x = np.random.default_rng(91).standard_normal((B, H, nb, Dg))
+    y = oracle.block_rope(x, 10000.0, 64)
+    np.testing.assert_allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-13)
+    np.testing.assert_array_equal(y[..., 0, :], x[..., 0, :])  # position 0 is not rotated
+
+
+def test_block_rope_logits_depend_on_relative_position_only():
+    # identical rows for every block: the rotated logits depend on i - j only
+    B, Hq, Hkv, nb, Dg = 1, 2, 1, 40, 16
+    rng = np.random.default_rng(92)
+    qg = np.broadcast_to(rng.standard_normal(Dg), (B, Hq, nb, Dg)).copy()
+    kg = np.broadcast_to(rng.standard_normal(Dg), (B, Hkv, nb, Dg)).copy()
+    L = oracle.gate_logits(oracle.block_rope(qg, 500000.0), oracle.block_rope(kg, 500000.0))
+    for d in range(nb):
+        diag = np.diagonal(L[0, 0], offset=-d)
+        np.testing.assert_allclose(diag, diag[0], rtol=1e-11, atol=1e-12)
+    assert np.ptp(L[0, 0][np.tril_indices(nb)]) > 1e-3  # and does vary with i - j
+
+
+def test_gate_with_rope_equals_manual_composition():
+    B, Hq, Hkv, S, D, Dg = 1, 2, 1, 512, 16, 8
+    q, k = _rand((B, Hq, S, D), 93), _rand((B, Hkv, S, D), 94)
+    wq, wk = _rand((Hq, D, Dg), 95), _rand((Hkv, 3 * D, Dg), 96)
+    L, _ = oracle.gate(q, k, wq, wk, rope_theta=500000.0)
+    qg = oracle.block_rope(oracle.linear(oracle.pool(q, 64, oracle.POOL_AVG), wq), 500000.0)
+    kg = oracle.block_rope(oracle.linear(oracle.pool(k, 64, oracle.POOL_MAX_MIN_AVG), wk), 500000.0)
+    np.testing.assert_array_equal(L, oracle.gate_logits(qg, kg))
