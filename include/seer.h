@@ -88,6 +88,11 @@ typedef struct {
   const float* head_thresholds; /* SEER_THRESHOLD: device [heads_q] per-head thresholds, or NULL */
   int32_t keep_first;  /* 1: block 0 is always kept */
   int32_t keep_diag;   /* 1: the diagonal block i is always kept (no empty row) */
+  double rope_theta;   /* > 0: block-level RoPE in the gate (section 3.1): q and k are
+                          taken before the model's RoPE, and the projected rows Qg, Kg
+                          are rotated at their block positions with base rope_theta /
+                          block (rope_theta is the model's RoPE base; rotate-half
+                          pairing (d, d + Dg/2)).  0 disables it. */
 } seer_gate_desc;
 
 /* Block mask in compacted form: for row r = (b, h, i), idx[r][0 .. count[r]-1]
@@ -119,6 +124,7 @@ size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block);
  *   Qp = average of each 64-token block of Q            [B][Hq][nb][D]
  *   Kp = max | min | average of each block of K         [B][Hkv][nb][3D]
  *   Qg = Qp Wq, Kg = Kp Wk (no bias)                    fp32
+ *   optional block-level RoPE of Qg[i], Kg[j] at block positions i, j
  *   L[i][j] = Qg[i] . Kg[g][j] / sqrt(Dg) for j <= i    (block-causal)
  *   P = softmax over j of L[i][.]
  *   TopK: the forced blocks ({0} if keep_first, {i} if keep_diag) plus the best

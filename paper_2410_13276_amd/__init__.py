@@ -37,7 +37,7 @@ class GateDesc(C.Structure):
     _fields_ = [("block", C.c_int32), ("gate_dim", C.c_int32), ("w_per_head", C.c_int32),
                 ("mode", C.c_int32), ("topk_ratio", C.c_double), ("topk_k", C.c_int32),
                 ("threshold", C.c_float), ("head_thresholds", C.c_void_p),
-                ("keep_first", C.c_int32), ("keep_diag", C.c_int32)]
+                ("keep_first", C.c_int32), ("keep_diag", C.c_int32), ("rope_theta", C.c_double)]
 
 
 class BlockMaskStruct(C.Structure):
@@ -180,7 +180,7 @@ def alloc_mask(batch: int, heads_q: int, seq_len: int, device="cuda", dense: boo
 
 def gate_desc(gate_dim: int, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
               threshold: float = 0.0, head_thresholds=None, keep_first: bool = True,
-              keep_diag: bool = True, w_per_head: bool = True) -> GateDesc:
+              keep_diag: bool = True, w_per_head: bool = True, rope_theta: float = 0.0) -> GateDesc:
     g = GateDesc()
     g.block = BLOCK
     g.gate_dim = gate_dim
@@ -192,6 +192,7 @@ def gate_desc(gate_dim: int, mode: int, topk_ratio: float = 0.0, topk_k: int = 0
     g.head_thresholds = _ptr(head_thresholds)
     g.keep_first = int(bool(keep_first))
     g.keep_diag = int(bool(keep_diag))
+    g.rope_theta = float(rope_theta)
     return g
 
 
@@ -204,13 +205,16 @@ def gate_workspace_bytes(q, k, gate_dim: int, mode: int = TOPK_RATIO, topk_ratio
 
 def gate(q, k, wq, wk, *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
          threshold: float = 0.0, head_thresholds=None, keep_first: bool = True,
-         keep_diag: bool = True, w_per_head: bool = True, mask: Optional[BlockMask] = None,
-         dense_out: bool = False, logits_out=None, workspace=None, stream=None) -> BlockMask:
-    """AttnGate + block selection (seer_gate).  Returns the block mask."""
+         keep_diag: bool = True, w_per_head: bool = True, rope_theta: float = 0.0,
+         mask: Optional[BlockMask] = None, dense_out: bool = False, logits_out=None,
+         workspace=None, stream=None) -> BlockMask:
+    """AttnGate + block selection (seer_gate).  Returns the block mask.  With
+    rope_theta > 0 (the model's RoPE base) q and k are pre-RoPE and the gate
+    applies its block-level RoPE."""
     torch = _torch()
     d = make_desc(q, k)
     gd = gate_desc(wq.shape[-1], mode, topk_ratio, topk_k, threshold, head_thresholds,
-                   keep_first, keep_diag, w_per_head)
+                   keep_first, keep_diag, w_per_head, rope_theta)
     if mask is None:
         mask = alloc_mask(q.shape[0], q.shape[1], q.shape[2], q.device, dense=dense_out)
     need = lib().seer_gate_workspace_bytes(C.byref(d), C.byref(gd), int(logits_out is None))

@@ -1,7 +1,8 @@
 // gate_kernels.hip -- AttnGate kernels for gfx950 (SeerAttention, arXiv 2410.13276).
 //
 //   pool_proj_kernel    section 3.1 + Eq. 1: average-pool Q and max|min|avg-pool K
-//                       over each 64-token block, then the gate linear layers.
+//                       over each 64-token block, then the gate linear layers and,
+//                       optionally, the block-level RoPE of section 3.1.
 //                       HBM-bound: streams Q and K once with 16-byte loads; the
 //                       GEMV reuses each weight element for every block of the
 //                       workgroup.
@@ -52,7 +53,8 @@ struct Load16<uint16_t> {
 template <typename T, int D, int DG, bool IS_K>
 __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t ss, int nb,
                                                const float* __restrict__ W,
-                                               float* __restrict__ out, float* smem) {
+                                               float* __restrict__ out, float* smem,
+                                               float* srot, double rope_base) {
   constexpr int EPL = Load16<T>::N;  // elements per 16-byte load
   constexpr int TPR = D / EPL;       // threads per block row
   constexpr int R = 256 / TPR;       // blocks per workgroup
@@ -123,10 +125,31 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
       acc[q] = fmaf(p[3], w[3], acc[q]);
     }
   }
+  if (rope_base <= 0.0) {
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) {
+      const int bb = blockIdx.x * R + r0 + q * RSTEP;
+      if (bb < nb) out[(int64_t)bb * DG + j] = acc[q];
+    }
+    return;
+  }
+  // Block-level RoPE (section 3.1): rotate plane (d, d + DG/2) of the row of
+  // block bb by angle bb * base^(-2d/DG); the angle is formed in double.
+#pragma unroll
+  for (int q = 0; q < RPT; ++q) srot[(r0 + q * RSTEP) * DG + j] = acc[q];
+  __syncthreads();
+  constexpr int HALF = DG / 2;
+  const int d = j % HALF;
+  const double w = pow(rope_base, -2.0 * d / DG);
 #pragma unroll
   for (int q = 0; q < RPT; ++q) {
-    const int bb = blockIdx.x * R + r0 + q * RSTEP;
-    if (bb < nb) out[(int64_t)bb * DG + j] = acc[q];
+    const int rr = r0 + q * RSTEP;
+    const int bb = blockIdx.x * R + rr;
+    const double ang = (double)bb * w;
+    const float cs = (float)cos(ang), sn = (float)sin(ang);
+    const float a = srot[rr * DG + d], b = srot[rr * DG + d + HALF];
+    const float y = (j < HALF) ? (a * cs - b * sn) : (a * sn + b * cs);
+    if (bb < nb) out[(int64_t)bb * DG + j] = y;
   }
 }
 
@@ -135,18 +158,21 @@ __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
   constexpr int EPL = Load16<T>::N;
   constexpr int R = 256 / (D / EPL);
   __shared__ __attribute__((aligned(16))) float smem[R * 3 * D];
+  __shared__ float srot[R * DG];
   const int b = blockIdx.z;
   const int slot = blockIdx.y;
   if (slot < a.heads_q) {
     const int h = slot;
     const T* x = static_cast<const T*>(a.q.ptr) + b * a.q.sb + h * a.q.sh;
     float* out = a.qg + ((int64_t)b * a.heads_q + h) * a.n_blocks * DG;
-    pool_proj_head<T, D, DG, false>(x, a.q.ss, a.n_blocks, a.wq + h * a.wq_head_stride, out, smem);
+    pool_proj_head<T, D, DG, false>(x, a.q.ss, a.n_blocks, a.wq + h * a.wq_head_stride, out, smem, srot,
+                                    a.rope_base);
   } else {
     const int g = slot - a.heads_q;
     const T* x = static_cast<const T*>(a.k.ptr) + b * a.k.sb + g * a.k.sh;
     float* out = a.kg + ((int64_t)b * a.heads_kv + g) * a.n_blocks * DG;
-    pool_proj_head<T, D, DG, true>(x, a.k.ss, a.n_blocks, a.wk + g * a.wk_head_stride, out, smem);
+    pool_proj_head<T, D, DG, true>(x, a.k.ss, a.n_blocks, a.wk + g * a.wk_head_stride, out, smem, srot,
+                                   a.rope_base);
   }
 }
 

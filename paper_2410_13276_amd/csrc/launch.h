@@ -21,6 +21,7 @@ struct PoolProjArgs {
   int64_t wq_head_stride, wk_head_stride;  // 0 when one matrix is shared by all heads
   float* qg;  // [B][Hq][nb][Dg]
   float* kg;  // [B][Hkv][nb][Dg]
+  double rope_base;  // > 0: block-level RoPE with this base (model base / block)
 };
 
 struct GateLogitsArgs {

@@ -53,6 +53,7 @@ seer_status check_gate(const seer_attn_desc* d, const seer_gate_desc* g) {
   if (g->block != SEER_BLOCK) return SEER_ERR_UNSUPPORTED;
   if (g->gate_dim != 32 && g->gate_dim != 64 && g->gate_dim != 128) return SEER_ERR_UNSUPPORTED;
   if (d->seq_len / SEER_BLOCK > 4096) return SEER_ERR_UNSUPPORTED;
+  if (!(g->rope_theta >= 0.0) || std::isinf(g->rope_theta)) return SEER_ERR_INVALID_ARG;
   switch (g->mode) {
     case SEER_TOPK_RATIO:
       if (!(g->topk_ratio > 0.0 && g->topk_ratio <= 1.0)) return SEER_ERR_INVALID_ARG;
@@ -153,6 +154,7 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   pa.wk_head_stride = gate->w_per_head ? (int64_t)3 * D * Dg : 0;
   pa.qg = qg;
   pa.kg = kg;
+  pa.rope_base = gate->rope_theta > 0.0 ? gate->rope_theta / gate->block : 0.0;
   if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
 
   seer::GateLogitsArgs la;

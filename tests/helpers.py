@@ -69,8 +69,8 @@ def small_inputs(B, Hq, Hkv, S, D, dtype, seed, Dg=None, spikes=False, w_sigma2=
 
 
 def oracle_gate(q, k, wq, wk, mode, rho=0.0, kfix=0, thresholds=None, keep_first=1, keep_diag=1,
-                w_per_head=True):
-    L, ell = oracle.gate(q, k, wq, wk, 64, w_per_head)
+                w_per_head=True, rope_theta=0.0):
+    L, ell = oracle.gate(q, k, wq, wk, 64, w_per_head, rope_theta=rope_theta)
     sel = oracle.select(ell, mode, rho=rho, k=kfix, thresholds=thresholds,
                         keep_first=keep_first, keep_diag=keep_diag)
     sel["L"] = L

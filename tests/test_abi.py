@@ -96,6 +96,9 @@ def test_gate_rejects_bad_desc(field, value, status):
     ("mode", 9, seer.ERR_INVALID_ARG),
     ("topk_ratio", 0.0, seer.ERR_INVALID_ARG),
     ("topk_ratio", 1.5, seer.ERR_INVALID_ARG),
+    ("rope_theta", -1.0, seer.ERR_INVALID_ARG),
+    ("rope_theta", float("nan"), seer.ERR_INVALID_ARG),
+    ("rope_theta", float("inf"), seer.ERR_INVALID_ARG),
 ])
 def test_gate_rejects_bad_gate(field, value, status):
     assert _call_gate(_desc(), _gate(**{field: value})) == status

@@ -89,6 +89,42 @@ def test_gate_mask_parity(case, sel):
     check_mask(dense, count, orc, topk=mode != oracle.THRESHOLD)
 
 
+ROPE_CASES = [CASES[0], CASES[1], CASES[3], CASES[5]]
+
+
+@pytest.mark.parametrize("case", ROPE_CASES, ids=lambda c: "x".join(map(str, c)))
+@pytest.mark.parametrize("theta,sel", [(10000.0, "ratio"), (500000.0, "thr"), (1e6, "fixed")])
+def test_gate_block_rope_parity(case, theta, sel):
+    """Block-level RoPE in the gate (section 3.1): logits and masks against the
+    oracle with the same rope base."""
+    B, Hq, Hkv, S, D, dt, Dg = case
+    w, q, k, v, wq, wk = small_inputs(B, Hq, Hkv, S, D, dt, seed=stable_seed(case, theta), Dg=Dg,
+                                      spikes=True)
+    qd, kd, _, wqd, wkd = _gpu(q, k, v, wq, wk)
+    if sel == "ratio":
+        mode, args, gargs = oracle.TOPK_RATIO, dict(rho=0.3), dict(mode=seer.TOPK_RATIO, topk_ratio=0.3)
+    elif sel == "thr":
+        mode, args = oracle.THRESHOLD, dict(thresholds=np.float32(0.02))
+        gargs = dict(mode=seer.THRESHOLD, threshold=0.02)
+    else:
+        mode, args, gargs = oracle.TOPK_FIXED, dict(kfix=4), dict(mode=seer.TOPK_FIXED, topk_k=4)
+    orc = oracle_gate(q, k, wq, wk, mode, **args, rope_theta=theta)
+    nb = S // 64
+    logits = torch.empty((B, Hq, nb, nb), dtype=torch.float32, device="cuda")
+    mask = seer.gate(qd, kd, wqd, wkd, **gargs, rope_theta=theta, dense_out=True, logits_out=logits)
+    torch.cuda.synchronize()
+    count, idx, dense = gpu_mask_numpy(mask)
+    tri = np.tril(np.ones((nb, nb), bool))
+    gl = logits.cpu().numpy().astype(np.float64)
+    err = np.abs(gl - orc["L"])[..., tri].max()
+    assert err <= 1e-5 * max(1.0, np.abs(orc["L"][..., tri]).max()), err
+    check_mask(dense, count, orc, topk=mode != oracle.THRESHOLD)
+    if nb > 1:
+        # the rotation changes the scores: the rope-free logits differ
+        L0, _ = oracle.gate(q, k, wq, wk, 64, True)
+        assert np.abs(L0[..., tri] - orc["L"][..., tri]).max() > 10 * err
+
+
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
 @pytest.mark.parametrize("pattern", ["gate", "a_shape", "vertical", "slash", "random", "empty_rows"])
 def test_bsattn_parity(case, pattern):
