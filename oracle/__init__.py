@@ -67,7 +67,8 @@ def lib():
         L.orc_attn.argtypes = [p, p, p, i, i, i, i, i, i, p, p, p, i, i, C.c_double,
                                p, p, i, p, p]
         L.orc_attn.restype = i
-        L.orc_maxpool_gt.argtypes = [p, p, i, i, i, i, i, i, p, p, i, C.c_double, p]
+        L.orc_maxpool_gt.argtypes = [p, p, i, i, i, i, i, i, p, p, i, i, C.c_double, p,
+                                     C.c_int64, p]
         L.orc_maxpool_gt.restype = i
         _lib = L
     return _lib
@@ -222,16 +223,23 @@ def attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, block: int = 64, causal: b
     return O, lse
 
 
-def maxpool_gt(q: np.ndarray, k: np.ndarray, block: int = 64, scale: Optional[float] = None):
-    """Eq. 2 target: block-wise max of the causal attention probabilities [B,Hq,nb,nb]."""
+def maxpool_gt(q: np.ndarray, k: np.ndarray, block: int = 64, scale: Optional[float] = None,
+               causal: bool = True, rows: Optional[np.ndarray] = None):
+    """Eq. 2 target: block-wise max of the attention probabilities.
+    Returns [B,Hq,nb,nb], or [n, nb] for rows int32 [n,3] of (b,h,i)."""
     B, Hq, S, D = q.shape
     Hkv = k.shape[1]
     nb = S // block
     if scale is None:
         scale = 1.0 / np.sqrt(D)
-    gt = np.empty((B, Hq, nb, nb), dtype=np.float64)
+    n = B * Hq * nb
+    if rows is not None:
+        rows = np.ascontiguousarray(rows, dtype=np.int32).reshape(-1, 3)
+        n = rows.shape[0]
+    gt = np.empty((n, nb), dtype=np.float64)
     rc = lib().orc_maxpool_gt(_ptr(q), _ptr(k), _dtype_code(q), B, Hq, Hkv, S, D,
-                              _ptr(_strides(q)), _ptr(_strides(k)), block, float(scale), _ptr(gt))
+                              _ptr(_strides(q)), _ptr(_strides(k)), block, int(bool(causal)),
+                              float(scale), _ptr(rows), n if rows is not None else 0, _ptr(gt))
     if rc != 0:
         raise ValueError(f"orc_maxpool_gt failed ({rc})")
-    return gt
+    return gt if rows is not None else gt.reshape(B, Hq, nb, nb)

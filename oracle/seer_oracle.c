@@ -33,8 +33,9 @@
  *                        64-token block is active in the block mask (section 3.3
  *                        "Block Sparse Flash-Attn Kernel"); an all-ones mask is
  *                        plain causal attention (the dense comparison path).
- *   orc_maxpool_gt    -- Eq. 2: MaxPool2D over blocks of the full causal
- *                        attention probability map (distillation ground truth).
+ *   orc_maxpool_gt    -- Eq. 2: MaxPool2D over blocks of the full (causal or
+ *                        not) attention probability map, the distillation
+ *                        ground truth; all rows or a subset of query blocks.
  *
  * Inputs arrive in the element type the GPU receives (fp32, or bf16 given as
  * raw 16-bit patterns) and are widened to double exactly before any arithmetic.
@@ -395,48 +396,64 @@ int orc_attn(const void *q, const void *k, const void *v, int dtype, int B,
 }
 
 /*
- * Distillation ground truth (Eq. 2): gt[b][h][i][j] = max over the block-sized
- * tile (i, j) of the causal attention probabilities softmax(scale * Q K^T).
- * Tiles above the diagonal hold 0 (every probability there is 0).
- * gt is [B][Hq][nb][nb].
+ * Distillation ground truth (Eq. 2): gt[i][j] = max over the block-sized tile
+ * (i, j) of the attention probabilities softmax(scale * Q K^T), keys s <= t
+ * when causal.  Tiles with no visible key (j > i, causal) hold 0.
+ * rows: int32 [n_rows][3] of (b, h, i) query-block rows, or NULL for all rows
+ * in (b, h, i) order; gt is [n][nb] with n = n_rows or B * Hq * nb.
  */
 int orc_maxpool_gt(const void *q, const void *k, int dtype, int B, int Hq,
                    int Hkv, int S, int D, const int64_t *qs, const int64_t *ks,
-                   int block, double scale, double *gt) {
+                   int block, int causal, double scale, const int32_t *rows,
+                   int64_t n_rows, double *gt) {
   if (block <= 0 || S % block != 0 || Hkv <= 0 || Hq % Hkv != 0) return -1;
   const int nb = S / block;
   const int G = Hq / Hkv;
+  const int64_t n = rows ? n_rows : (int64_t)B * Hq * nb;
   int bad = 0;
-#pragma omp parallel for collapse(2) schedule(dynamic) reduction(| : bad)
-  for (int b = 0; b < B; ++b)
-    for (int h = 0; h < Hq; ++h) {
-      const int g = h / G;
-      double *score = (double *)malloc(sizeof(double) * (size_t)S);
-      if (!score) {
+#pragma omp parallel for schedule(dynamic) reduction(| : bad)
+  for (int64_t r = 0; r < n; ++r) {
+    int b, h, i;
+    if (rows) {
+      b = rows[3 * r];
+      h = rows[3 * r + 1];
+      i = rows[3 * r + 2];
+      if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= nb) {
         bad = 1;
         continue;
       }
-      double *out = gt + ((int64_t)b * Hq + h) * nb * nb;
-      for (int64_t e = 0; e < (int64_t)nb * nb; ++e) out[e] = 0.0;
-      for (int t = 0; t < S; ++t) {
-        double m = -INFINITY;
-        for (int s = 0; s <= t; ++s) {
-          double acc = 0.0;
-          for (int d = 0; d < D; ++d)
-            acc += elem(q, dtype, b * qs[0] + h * qs[1] + (int64_t)t * qs[2] + d) *
-                   elem(k, dtype, b * ks[0] + g * ks[1] + (int64_t)s * ks[2] + d);
-          score[s] = scale * acc;
-          if (score[s] > m) m = score[s];
-        }
-        double l = 0.0;
-        for (int s = 0; s <= t; ++s) l += exp(score[s] - m);
-        for (int s = 0; s <= t; ++s) {
-          const double p = exp(score[s] - m) / l;
-          double *cell = out + (int64_t)(t / block) * nb + s / block;
-          if (p > *cell) *cell = p;
-        }
-      }
-      free(score);
+    } else {
+      b = (int)(r / ((int64_t)Hq * nb));
+      h = (int)((r / nb) % Hq);
+      i = (int)(r % nb);
     }
+    const int g = h / G;
+    double *score = (double *)malloc(sizeof(double) * (size_t)S);
+    if (!score) {
+      bad = 1;
+      continue;
+    }
+    double *out = gt + r * nb;
+    for (int j = 0; j < nb; ++j) out[j] = 0.0;
+    for (int t = i * block; t < (i + 1) * block; ++t) {
+      const int last = causal ? t : S - 1; /* keys 0..last are visible */
+      double m = -INFINITY;
+      for (int s = 0; s <= last; ++s) {
+        double acc = 0.0;
+        for (int d = 0; d < D; ++d)
+          acc += elem(q, dtype, b * qs[0] + h * qs[1] + (int64_t)t * qs[2] + d) *
+                 elem(k, dtype, b * ks[0] + g * ks[1] + (int64_t)s * ks[2] + d);
+        score[s] = scale * acc;
+        if (score[s] > m) m = score[s];
+      }
+      double l = 0.0;
+      for (int s = 0; s <= last; ++s) l += exp(score[s] - m);
+      for (int s = 0; s <= last; ++s) {
+        const double p = exp(score[s] - m) / l;
+        if (p > out[s / block]) out[s / block] = p;
+      }
+    }
+    free(score);
+  }
   return bad ? -2 : 0;
 }

@@ -436,6 +436,33 @@ def test_maxpool_gt_matches_torch():
     np.testing.assert_allclose(gt, ref, rtol=1e-12, atol=0)
 
 
+def test_maxpool_gt_noncausal_matches_torch_and_rows_subset():
+    B, Hq, Hkv, S, D, blk = 2, 3, 1, 192, 8, 64
+    q, k = _rand((B, Hq, S, D), 27), _rand((B, Hkv, S, D), 28)
+    gt = oracle.maxpool_gt(q, k, causal=False)
+    tq = torch.from_numpy(q.astype(np.float64))
+    tk = torch.from_numpy(k.astype(np.float64)).repeat_interleave(Hq, dim=1)
+    p = torch.softmax((tq @ tk.transpose(-1, -2)) / math.sqrt(D), -1)
+    ref = F.max_pool2d(p, blk, blk).numpy()
+    np.testing.assert_allclose(gt, ref, rtol=1e-12, atol=0)
+    # a row subset in any order returns those rows of the full map
+    rows = np.array([[1, 2, 0], [0, 0, 2], [1, 0, 1]], np.int32)
+    sub = oracle.maxpool_gt(q, k, causal=False, rows=rows)
+    np.testing.assert_array_equal(sub, gt[rows[:, 0], rows[:, 1], rows[:, 2]])
+
+
+def test_maxpool_gt_uniform_attention_closed_form():
+    # K = 0 makes every visible score equal: query t spreads 1/(t+1) uniformly,
+    # so tile (i, j <= i) pools to its first query's 1/(64 i + 1); j > i is 0
+    B, Hq, S, D, blk = 1, 1, 320, 16, 64
+    q = _rand((B, Hq, S, D), 29)
+    k = np.zeros((B, Hq, S, D), np.float32)
+    gt = oracle.maxpool_gt(q, k)[0, 0]
+    nb = S // blk
+    want = np.tril(np.ones((nb, nb))) / (blk * np.arange(nb) + 1.0)[:, None]
+    np.testing.assert_allclose(gt, want, rtol=1e-14, atol=0)
+
+
 # --------------------------------------------------------------------------
 # block-level RoPE in the gate (section 3.1)
 # --------------------------------------------------------------------------
