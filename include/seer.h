@@ -13,6 +13,9 @@
  *                    the paper compares against in section 4.2)
  *   seer_mask_from_dense  compaction of a caller-made 0/1 block mask into the
  *                    index-list form seer_bsattn reads
+ *   seer_attn_gt     dense attention that also returns the 2D max-pooled
+ *                    attention map, the gate's distillation target (Eq. 2,
+ *                    appendix A.1)
  *
  * Conventions shared by every entry point:
  *  - Pointers to tensors are DEVICE pointers (HIP device memory of the current
@@ -176,6 +179,35 @@ seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm
  */
 seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, const uint8_t* dense,
                                  seer_block_mask* out, void* stream);
+
+/*
+ * Workspace bytes of seer_attn_gt when it processes `kv_groups` KV groups per
+ * launch (a KV group is one KV head and its heads_q / heads_kv query heads of
+ * one batch entry); kv_groups <= 0 or >= batch * heads_kv means all of them
+ * (one launch).  The workspace holds, per query head, the raw-score maximum of
+ * every query over every key tile: fp32 [heads][nb][nb][64], 16 nb^2 KiB per
+ * query head (1 GiB per head at seq_len 131072).  0 on invalid arguments.
+ */
+size_t seer_attn_gt_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t kv_groups);
+
+/*
+ * Dense attention with the 2D max-pooled attention map (Eq. 2; computed as in
+ * appendix A.1, Eq. 5-6).  Computes o and lse exactly as seer_dense_attn, and
+ *   gt[b][h][i][j] = max over queries t of block i and keys s of block j of
+ *                    softmax_s(sm_scale q_t . k_s)  (s <= t when causal),
+ * 0 where block j holds no key visible to block i (j > i when causal).
+ * gt: device float [batch][heads_q][nb][nb], caller-owned.  lse may be NULL.
+ * workspace: device memory, 256-byte aligned, of at least
+ * seer_attn_gt_workspace_bytes(desc, block, 1) bytes; the call runs as many KV
+ * groups per launch as it holds (all at once with
+ * seer_attn_gt_workspace_bytes(desc, block, 0)), several launches on `stream`
+ * otherwise.  Its contents on return are unspecified.
+ * Errors: as seer_dense_attn; SEER_ERR_WORKSPACE if the workspace is missing
+ * or smaller than one KV group needs.
+ */
+seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t causal, float sm_scale,
+                         const void* q, const void* k, const void* v, void* o, float* lse,
+                         float* gt, void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -9,6 +9,7 @@ no CPU fallback.
     mask = seer.gate(q, k, wq, wk, mode=seer.TOPK_RATIO, topk_ratio=0.1)
     o, lse = seer.bsattn(q, k, v, mask)
     o_dense, _ = seer.dense_attn(q, k, v)
+    o_dense, lse, gt = seer.attn_gt(q, k, v, want_lse=True)   # distillation target
 """
 from __future__ import annotations
 
@@ -56,6 +57,9 @@ _SIGS = {
     "seer_bsattn": ([_P, C.c_int32, _P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P], C.c_int),
     "seer_dense_attn": ([_P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P], C.c_int),
     "seer_mask_from_dense": ([_P, C.c_int32, _P, _P, _P], C.c_int),
+    "seer_attn_gt_workspace_bytes": ([_P, C.c_int32, C.c_int32], C.c_size_t),
+    "seer_attn_gt": ([_P, C.c_int32, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P],
+                     C.c_int),
 }
 
 _lib = None
@@ -257,6 +261,38 @@ def dense_attn(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
                                _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
     _check(st, "seer_dense_attn")
     return out, lse
+
+
+def attn_gt_workspace_bytes(q, k, v=None, kv_groups: int = 0) -> int:
+    """Workspace of attn_gt running `kv_groups` KV groups per launch (0: all)."""
+    d = make_desc(q, k, v)
+    return lib().seer_attn_gt_workspace_bytes(C.byref(d), BLOCK, int(kv_groups))
+
+
+def attn_gt(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
+            lse: Optional[object] = None, want_lse: bool = False, gt=None, workspace=None,
+            kv_groups: int = 0, stream=None):
+    """Dense attention plus the 2D max-pooled attention map (seer_attn_gt).
+    Returns (O, LSE or None, gt [B, Hq, nb, nb] fp32).  Without a workspace,
+    one sized for `kv_groups` KV groups per launch (0: all) is allocated."""
+    torch = _torch()
+    B, Hq, S, _ = q.shape
+    nb = S // BLOCK
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
+    if gt is None:
+        gt = torch.empty((B, Hq, nb, nb), dtype=torch.float32, device=q.device)
+    d = make_desc(q, k, v, out)
+    if workspace is None:
+        n = lib().seer_attn_gt_workspace_bytes(C.byref(d), BLOCK, int(kv_groups))
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=q.device)
+    st = lib().seer_attn_gt(C.byref(d), BLOCK, int(bool(causal)), float(sm_scale), _ptr(q), _ptr(k),
+                            _ptr(v), _ptr(out), _ptr(lse), _ptr(gt), _ptr(workspace),
+                            workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "seer_attn_gt")
+    return out, lse, gt
 
 
 def mask_from_dense(dense, heads_kv: int = 1, mask: Optional[BlockMask] = None,

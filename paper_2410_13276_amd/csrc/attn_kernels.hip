@@ -12,6 +12,13 @@
 // K tile (row-major) and the V tile (transposed, key-contiguous) in LDS, while
 // the next tile's global loads are already in flight in registers.
 //
+// Ground-truth mode (appendix A.1, Eq. 5-6; the distillation target of Eq. 2):
+// the dense kernel also stores, per query and key tile, the tile row maximum of
+// the raw scores r, which online softmax forms anyway; once the row's final
+// max and denominator are known, the workgroup rescales its stored maxima into
+// probabilities and takes the column max over its 64 queries, giving the 2D
+// max-pooled attention map without ever holding a probability matrix.
+//
 // Transposed formulation.  Each wavefront computes S^T = K Q^T and O^T = V^T P^T
 // with v_mfma_f32_32x32x16_bf16, so that the MFMA output column -- one lane
 // (and its partner lane + 32) -- is one query.  The softmax row statistics
@@ -115,8 +122,8 @@ __device__ __forceinline__ RowList<SPARSE> make_list(const AttnArgs& a, const Ta
 // converts s in place to unnormalised probabilities and returns the factor by
 // which the running output must be rescaled.
 __device__ __forceinline__ float softmax_tile(f32x16 (&s)[2], float& m_run, float& l_run,
-                                              float c) {
-  float mloc = -INFINITY;
+                                              float c, float& mloc) {
+  mloc = -INFINITY;
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
@@ -138,6 +145,31 @@ __device__ __forceinline__ float softmax_tile(f32x16 (&s)[2], float& m_run, floa
   l_run = l_run * alpha + psum;
   m_run = m_new;
   return alpha;
+}
+
+// Ground-truth epilogue of one query block (appendix A.1, Eq. 6 and the column
+// max after it).  rrow[j][t] holds the raw-score maximum of query t over key
+// tile j; sL2[t] = m_t c + log2(l_t) is the final softmax normaliser of query t
+// in the exp2 domain (c = scale log2 e), so exp2(r c - sL2) is the largest
+// probability query t gives a key of tile j.  Tiles j >= n_vis hold no visible
+// key and pool to 0.  Thread `tid` of `nthr` handles tiles tid, tid + nthr, ...
+__device__ __forceinline__ void pool_epilogue(const float* __restrict__ rrow, const float* sL2,
+                                              float c, int n_vis, int nb,
+                                              float* __restrict__ gtrow, int tid, int nthr) {
+  for (int j = tid; j < nb; j += nthr) {
+    float x = -INFINITY;
+    if (j < n_vis) {
+      const f32x4* rp = reinterpret_cast<const f32x4*>(rrow + (int64_t)j * 64);
+#pragma unroll 4
+      for (int u = 0; u < 16; ++u) {
+        const f32x4 r = rp[u];
+        const f32x4 l = *reinterpret_cast<const f32x4*>(sL2 + 4 * u);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x = fmaxf(x, fmaf(r[e], c, -l[e]));
+      }
+    }
+    gtrow[j] = __builtin_amdgcn_exp2f(x);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -237,13 +269,15 @@ constexpr int kListChunk = 256;
 // are only rescaled) when some lane's tile max exceeds it by more than 2^8 in
 // the exp2 domain; otherwise probabilities up to 2^8 are accumulated against
 // the stale max, which leaves O / l unchanged.
-template <int D, bool SPARSE>
+template <int D, bool SPARSE, bool POOL>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_bf16_kernel(KernelArgs ka) {
+  static_assert(!(SPARSE && POOL), "the ground truth comes from dense attention");
   using Lay = Bf16Layout<D>;
   __shared__ __attribute__((aligned(16))) uint16_t sK[Lay::TILE];
   __shared__ __attribute__((aligned(16))) uint16_t sV[Lay::TILE];
   __shared__ uint16_t sList[SPARSE ? kListChunk : 1];
+  __shared__ __attribute__((aligned(16))) float sL2[POOL ? 64 : 1];
 
   const AttnArgs& a = ka.a;
   const Task t = decode_task(ka.map, blockIdx.x);
@@ -298,6 +332,8 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
 
   // row list
   const RowList<SPARSE> list = make_list<SPARSE>(a, t);
+  const int64_t trow = ((int64_t)t.b * a.heads_q + t.h) * a.n_blocks + t.i;
+  float* const rrow = POOL ? a.pool_r + trow * a.n_blocks * 64 : nullptr;
   auto fetch_chunk = [&](int base) {  // entries [base, base + kListChunk) of the row list
     if (SPARSE) {
       for (int p = tid; p < kListChunk; p += 128)
@@ -426,6 +462,8 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     wait_loads();
     __syncthreads();  // M: V_j visible, K_jn consumed
     if (jnn >= 0) load_tile_lds<D>(sK_a, kp + jnn * ktile, kss, wave_u, koffd);
+    // ground truth: this tile's row max (Eq. 5), completed with the K load by barrier E
+    if (POOL && hf == 0) rrow[(int64_t)j * 64 + 32 * wave + col] = mloc;
 
     // O^T += V^T P^T; V^T operand: feature 32dt + col, the same keys as pb[kt]
     auto vread = [&](int st) -> bf16x8 {
@@ -499,6 +537,12 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     const float lse = (l_tot > 0.f) ? m_run * a.scale + __logf(l_tot) : -INFINITY;
     a.lse[((int64_t)t.b * a.heads_q + t.h) * (int64_t)a.n_blocks * 64 + qrow] = lse;
   }
+  if (POOL) {
+    if (hf == 0) sL2[ql] = (l_tot > 0.f) ? m_run * c + __log2f(l_tot) : INFINITY;
+    wait_loads();  // the row-max stores of this workgroup have completed
+    __syncthreads();
+    pool_epilogue(rrow, sL2, c, list.n, a.n_blocks, a.gt + trow * a.n_blocks, tid, 128);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -511,6 +555,7 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
   constexpr int VS = D;      // LDS row stride of V (floats)
   __shared__ __attribute__((aligned(16))) float sK[64 * KS];
   __shared__ __attribute__((aligned(16))) float sV[64 * VS];
+  __shared__ __attribute__((aligned(16))) float sL2[64];
 
   const AttnArgs& a = ka.a;
   const Task t = decode_task(ka.map, blockIdx.x);
@@ -549,6 +594,9 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
     dl = make_list<false>(a, t);
     n_tiles = dl.n;
   }
+  const bool pool = a.gt != nullptr;  // the launcher enables it for dense rows only
+  const int64_t trow = ((int64_t)t.b * a.heads_q + t.h) * a.n_blocks + t.i;
+  float* const rrow = pool ? a.pool_r + trow * a.n_blocks * 64 : nullptr;
   for (int n = 0; n < n_tiles; ++n) {
     const int j = sparse ? sl.at(n) : dl.at(n);
     if (!(sparse ? sl.ok(j) : dl.ok(j))) break;
@@ -588,7 +636,9 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
           if (kl > ql) s[mt][e] = -INFINITY;
         }
     }
-    const float alpha = softmax_tile(s, m_run, l_run, c);
+    float rmax;
+    const float alpha = softmax_tile(s, m_run, l_run, c, rmax);
+    if (pool && hf == 0) rrow[(int64_t)j * 64 + 32 * wave + col] = rmax;  // Eq. 5
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
@@ -622,6 +672,12 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
   if (a.lse && hf == 0) {
     const float lse = (l_tot > 0.f) ? m_run * a.scale + __logf(l_tot) : -INFINITY;
     a.lse[((int64_t)t.b * a.heads_q + t.h) * (int64_t)a.n_blocks * 64 + qrow] = lse;
+  }
+  if (pool) {
+    if (hf == 0) sL2[32 * wave + col] = (l_tot > 0.f) ? m_run * c + __log2f(l_tot) : INFINITY;
+    __threadfence_block();
+    __syncthreads();
+    pool_epilogue(rrow, sL2, c, n_tiles, a.n_blocks, a.gt + trow * a.n_blocks, tid, 128);
   }
 }
 
@@ -669,13 +725,17 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   if (total == 0) return hipSuccess;
   dim3 grid((unsigned)total), block(128);
   const bool sparse = a.count != nullptr;
+  const bool pool = a.gt != nullptr;
+  if ((sparse && pool) || (pool && !a.pool_r)) return hipErrorInvalidValue;
   if (a.bf16) {
     if (a.head_dim == 128) {
-      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true>), grid, block, 0, s, ka);
-      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false>), grid, block, 0, s, ka);
+      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true, false>), grid, block, 0, s, ka);
+      else if (pool) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false, true>), grid, block, 0, s, ka);
+      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false, false>), grid, block, 0, s, ka);
     } else if (a.head_dim == 64) {
-      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true>), grid, block, 0, s, ka);
-      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false>), grid, block, 0, s, ka);
+      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true, false>), grid, block, 0, s, ka);
+      else if (pool) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false, true>), grid, block, 0, s, ka);
+      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false, false>), grid, block, 0, s, ka);
     } else {
       return hipErrorInvalidValue;
     }

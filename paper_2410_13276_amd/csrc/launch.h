@@ -65,6 +65,10 @@ struct AttnArgs {
   float scale;
   const int32_t* count;  // nullptr: dense (every causal block)
   const uint16_t* idx;
+  // ground-truth mode (dense only): per-tile row maxima [rows][nb][64] and the
+  // 2D max-pooled probability map [B][Hq][nb][nb]; both nullptr otherwise
+  float* pool_r;
+  float* gt;
 };
 
 hipError_t launch_pool_proj(const PoolProjArgs& a, hipStream_t s);

@@ -5,6 +5,7 @@
 // synchronising.  The library owns no memory and keeps no state.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 
@@ -85,6 +86,48 @@ GateLayout gate_layout(const seer_attn_desc* d, const seer_gate_desc* g, bool lo
 }
 
 seer_status from_hip(hipError_t e) { return e == hipSuccess ? SEER_OK : SEER_ERR_HIP; }
+
+seer_status check_attn(const seer_attn_desc* desc, float sm_scale, const void* q,
+                              const void* k, const void* v, const void* o) {
+  seer_status s = check_desc(desc, 0xF);
+  if (s != SEER_OK) return s;
+  if (!q || !k || !v || !o) return SEER_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return SEER_ERR_INVALID_ARG;
+  if (std::isnan(sm_scale) || std::isinf(sm_scale)) return SEER_ERR_INVALID_ARG;
+  return SEER_OK;
+}
+
+seer::AttnArgs attn_args(const seer_attn_desc* desc, int32_t causal, float sm_scale,
+                                const void* q, const void* k, const void* v, void* o, float* lse) {
+  seer::AttnArgs a;
+  a.q = view(q, desc->q_stride);
+  a.k = view(k, desc->k_stride);
+  a.v = view(v, desc->v_stride);
+  a.o = o;
+  a.osb = desc->o_stride[0];
+  a.osh = desc->o_stride[1];
+  a.oss = desc->o_stride[2];
+  a.lse = lse;
+  a.batch = desc->batch;
+  a.heads_q = desc->heads_q;
+  a.heads_kv = desc->heads_kv;
+  a.n_blocks = desc->seq_len / SEER_BLOCK;
+  a.head_dim = desc->head_dim;
+  a.bf16 = desc->dtype == SEER_BF16;
+  a.causal = causal != 0;
+  a.scale = sm_scale > 0.f ? sm_scale : (float)(1.0 / std::sqrt((double)desc->head_dim));
+  a.count = nullptr;
+  a.idx = nullptr;
+  a.pool_r = nullptr;
+  a.gt = nullptr;
+  return a;
+}
+
+// Bytes of row-max workspace per query head: nb key tiles x 64 queries per query block.
+size_t gt_head_bytes(const seer_attn_desc* d) {
+  const size_t nb = (size_t)(d->seq_len / SEER_BLOCK);
+  return nb * nb * 64 * sizeof(float);
+}
 
 }  // namespace
 
@@ -190,33 +233,14 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
 static seer_status attn_common(const seer_attn_desc* desc, const seer_block_mask* mask,
                                int32_t causal, float sm_scale, const void* q, const void* k,
                                const void* v, void* o, float* lse, void* stream) {
-  seer_status s = check_desc(desc, 0xF);
+  seer_status s = check_attn(desc, sm_scale, q, k, v, o);
   if (s != SEER_OK) return s;
-  if (!q || !k || !v || !o) return SEER_ERR_INVALID_ARG;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return SEER_ERR_INVALID_ARG;
-  if (std::isnan(sm_scale) || std::isinf(sm_scale)) return SEER_ERR_INVALID_ARG;
   const int nb = desc->seq_len / SEER_BLOCK;
   if (mask) {
     if (!mask->count || !mask->idx || mask->n_blocks != nb) return SEER_ERR_INVALID_ARG;
     if (nb > 65536) return SEER_ERR_UNSUPPORTED;
   }
-  seer::AttnArgs a;
-  a.q = view(q, desc->q_stride);
-  a.k = view(k, desc->k_stride);
-  a.v = view(v, desc->v_stride);
-  a.o = o;
-  a.osb = desc->o_stride[0];
-  a.osh = desc->o_stride[1];
-  a.oss = desc->o_stride[2];
-  a.lse = lse;
-  a.batch = desc->batch;
-  a.heads_q = desc->heads_q;
-  a.heads_kv = desc->heads_kv;
-  a.n_blocks = nb;
-  a.head_dim = desc->head_dim;
-  a.bf16 = desc->dtype == SEER_BF16;
-  a.causal = causal != 0;
-  a.scale = sm_scale > 0.f ? sm_scale : (float)(1.0 / std::sqrt((double)desc->head_dim));
+  seer::AttnArgs a = attn_args(desc, causal, sm_scale, q, k, v, o, lse);
   a.count = mask ? mask->count : nullptr;
   a.idx = mask ? mask->idx : nullptr;
   return from_hip(seer::launch_attn(a, static_cast<hipStream_t>(stream)));
@@ -251,6 +275,57 @@ seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, cons
   a.count = out->count;
   a.idx = out->idx;
   return from_hip(seer::launch_mask_from_dense(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t seer_attn_gt_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t kv_groups) {
+  if (block != SEER_BLOCK || check_desc(desc, 0xF) != SEER_OK) return 0;
+  const int64_t groups = (int64_t)desc->batch * desc->heads_kv;
+  const int64_t use = (kv_groups <= 0 || kv_groups >= groups) ? groups : kv_groups;
+  const int G = desc->heads_q / desc->heads_kv;
+  return (size_t)use * G * gt_head_bytes(desc);
+}
+
+seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t causal, float sm_scale,
+                         const void* q, const void* k, const void* v, void* o, float* lse,
+                         float* gt, void* workspace, size_t workspace_bytes, void* stream) {
+  if (block != SEER_BLOCK) return desc ? SEER_ERR_UNSUPPORTED : SEER_ERR_INVALID_ARG;
+  seer_status s = check_attn(desc, sm_scale, q, k, v, o);
+  if (s != SEER_OK) return s;
+  if (!gt) return SEER_ERR_INVALID_ARG;
+  const int G = desc->heads_q / desc->heads_kv;
+  const size_t group_bytes = (size_t)G * gt_head_bytes(desc);
+  if (!workspace || workspace_bytes < group_bytes) return SEER_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t nb = desc->seq_len / SEER_BLOCK;
+  const int64_t all = (int64_t)desc->batch * desc->heads_kv;
+  seer::AttnArgs a = attn_args(desc, causal, sm_scale, q, k, v, o, lse);
+  a.pool_r = static_cast<float*>(workspace);
+  if (workspace_bytes / group_bytes >= (size_t)all) {  // every head in one launch
+    a.gt = gt;
+    return from_hip(seer::launch_attn(a, st));
+  }
+  // otherwise: runs of KV groups of one batch entry per launch
+  const int per = (int)(workspace_bytes / group_bytes);
+  const size_t qe = desc->dtype == SEER_F32 ? 4 : 2;
+  for (int b = 0; b < desc->batch; ++b)
+    for (int g0 = 0; g0 < desc->heads_kv; g0 += per) {
+      const int ng = std::min(per, desc->heads_kv - g0);
+      const int h0 = g0 * G;
+      seer::AttnArgs c = a;
+      c.batch = 1;
+      c.heads_kv = ng;
+      c.heads_q = ng * G;
+      c.q.ptr = static_cast<const char*>(q) + qe * (b * desc->q_stride[0] + h0 * desc->q_stride[1]);
+      c.k.ptr = static_cast<const char*>(k) + qe * (b * desc->k_stride[0] + g0 * desc->k_stride[1]);
+      c.v.ptr = static_cast<const char*>(v) + qe * (b * desc->v_stride[0] + g0 * desc->v_stride[1]);
+      c.o = static_cast<char*>(o) + qe * (b * desc->o_stride[0] + h0 * desc->o_stride[1]);
+      const int64_t hrow = (int64_t)b * desc->heads_q + h0;  // first query head of the run
+      c.lse = lse ? lse + hrow * nb * 64 : nullptr;
+      c.gt = gt + hrow * nb * nb;
+      if ((s = from_hip(seer::launch_attn(c, st))) != SEER_OK) return s;
+    }
+  return SEER_OK;
 }
 
 }  // extern "C"

@@ -24,7 +24,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 8, names
+    assert len(names) == 10, names
     L = C.CDLL(seer.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -147,3 +147,23 @@ def test_mask_from_dense_rejects_bad_args():
     assert L.seer_mask_from_dense(C.byref(d), 32, FAKE, C.byref(m), None) == seer.ERR_UNSUPPORTED
     m.n_blocks = 3
     assert L.seer_mask_from_dense(C.byref(d), 64, FAKE, C.byref(m), None) == seer.ERR_INVALID_ARG
+
+
+def test_attn_gt_workspace_and_rejects_bad_args():
+    L = seer.lib()
+    d = _desc(B=2, Hq=4, Hkv=2, S=1024, D=128)
+    per_head = 16 * 16 * 64 * 4
+    assert L.seer_attn_gt_workspace_bytes(C.byref(d), 64, 0) == 2 * 4 * per_head
+    assert L.seer_attn_gt_workspace_bytes(C.byref(d), 64, 1) == 2 * per_head   # G = 2
+    assert L.seer_attn_gt_workspace_bytes(C.byref(d), 64, 9) == 2 * 4 * per_head
+    assert L.seer_attn_gt_workspace_bytes(C.byref(d), 128, 0) == 0
+    args = (FAKE, FAKE, FAKE, FAKE, None)
+    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, None, FAKE * 16, 1 << 40, None) == \
+        seer.ERR_INVALID_ARG                                                  # no gt
+    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, FAKE, FAKE * 16, 2 * per_head - 1, None) == \
+        seer.ERR_WORKSPACE
+    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, FAKE, None, 1 << 40, None) == seer.ERR_WORKSPACE
+    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, FAKE, FAKE * 16 + 16, 1 << 40, None) == \
+        seer.ERR_INVALID_ARG                                                  # misaligned workspace
+    assert L.seer_attn_gt(C.byref(d), 128, 1, 0.0, *args, FAKE, FAKE * 16, 1 << 40, None) == \
+        seer.ERR_UNSUPPORTED
