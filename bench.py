@@ -108,6 +108,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
     ap.add_argument("--dense-runs", type=int, default=3)
+    ap.add_argument("--gt-runs", type=int, default=2, help="timed runs of the ground-truth kernel (0: skip)")
     ap.add_argument("--cpu-rows", type=int, default=1024, help="oracle sample size (q-block rows)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -207,6 +208,26 @@ def main() -> int:
     dense_ms = float(np.median(dts))
     dense_flops = flops_tile * causal_tiles
 
+    # distillation ground truth (2D max-pooled attention map) at the same shape,
+    # with a workspace of one KV group per launch
+    gt_ms, gt_ws_bytes = None, 0
+    if args.gt_runs > 0:
+        gt_ws_bytes = seer.attn_gt_workspace_bytes(qd, kd, vd, 1)
+        gt_ws = torch.empty(gt_ws_bytes, dtype=torch.uint8, device="cuda")
+        gt_map = torch.empty((w.batch, w.heads_q, nb, nb), dtype=torch.float32, device="cuda")
+        seer.attn_gt(qd, kd, vd, out=od, gt=gt_map, workspace=gt_ws)
+        torch.cuda.synchronize()
+        gts = []
+        for _ in range(args.gt_runs):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            seer.attn_gt(qd, kd, vd, out=od, gt=gt_map, workspace=gt_ws)
+            b.record(stream)
+            torch.cuda.synchronize()
+            gts.append(a.elapsed_time(b))
+        gt_ms = float(np.median(gts))
+        del gt_ws, gt_map
+
     active_flops = flops_tile * active
     attn_tflops = active_flops / (attn_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
@@ -243,7 +264,12 @@ def main() -> int:
         "speedup_vs_dense_incl_gate": round(dense_ms / ms_step, 3),
         "ideal_speedup": round(1.0 / (1.0 - sparsity), 3),
         "speedup_tracking": round(speedup * (1.0 - sparsity), 3),
-        "roofline": {"bound": "mfma", "kernel": "attn_fwd_bf16_kernel<128,true>",
+        "ground_truth": None if gt_ms is None else {
+            "what": "dense attention + 2D max-pooled attention map (seer_attn_gt), one KV group per launch",
+            "ms": round(gt_ms, 3), "dense_ms": round(dense_ms, 3),
+            "overhead_vs_dense": round(gt_ms / dense_ms - 1.0, 4),
+            "workspace_bytes": gt_ws_bytes, "map_bytes": 4 * w.batch * w.heads_q * nb * nb},
+        "roofline": {"bound": "mfma", "kernel": "attn_fwd_bf16_kernel<128, true>",
                      "achieved": round(attn_tflops, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(attn_tflops / peak, 4), "traffic": _traffic(w.name),
                      "flops_per_launch": active_flops},

@@ -269,15 +269,17 @@ constexpr int kListChunk = 256;
 // are only rescaled) when some lane's tile max exceeds it by more than 2^8 in
 // the exp2 domain; otherwise probabilities up to 2^8 are accumulated against
 // the stale max, which leaves O / l unchanged.
-template <int D, bool SPARSE, bool POOL>
+//
+// The dense instantiation also serves the ground-truth mode (a.gt set): a
+// uniform runtime switch rather than a third instantiation.
+template <int D, bool SPARSE>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_bf16_kernel(KernelArgs ka) {
-  static_assert(!(SPARSE && POOL), "the ground truth comes from dense attention");
   using Lay = Bf16Layout<D>;
   __shared__ __attribute__((aligned(16))) uint16_t sK[Lay::TILE];
   __shared__ __attribute__((aligned(16))) uint16_t sV[Lay::TILE];
   __shared__ uint16_t sList[SPARSE ? kListChunk : 1];
-  __shared__ __attribute__((aligned(16))) float sL2[POOL ? 64 : 1];
+  __shared__ __attribute__((aligned(16))) float sL2[SPARSE ? 1 : 64];
 
   const AttnArgs& a = ka.a;
   const Task t = decode_task(ka.map, blockIdx.x);
@@ -332,8 +334,9 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
 
   // row list
   const RowList<SPARSE> list = make_list<SPARSE>(a, t);
+  const bool pool = !SPARSE && a.gt != nullptr;  // ground-truth mode
   const int64_t trow = ((int64_t)t.b * a.heads_q + t.h) * a.n_blocks + t.i;
-  float* const rrow = POOL ? a.pool_r + trow * a.n_blocks * 64 : nullptr;
+  float* const rrow = pool ? a.pool_r + trow * a.n_blocks * 64 : nullptr;
   auto fetch_chunk = [&](int base) {  // entries [base, base + kListChunk) of the row list
     if (SPARSE) {
       for (int p = tid; p < kListChunk; p += 128)
@@ -463,7 +466,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     __syncthreads();  // M: V_j visible, K_jn consumed
     if (jnn >= 0) load_tile_lds<D>(sK_a, kp + jnn * ktile, kss, wave_u, koffd);
     // ground truth: this tile's row max (Eq. 5), completed with the K load by barrier E
-    if (POOL && hf == 0) rrow[(int64_t)j * 64 + 32 * wave + col] = mloc;
+    if (pool && hf == 0) rrow[(int64_t)j * 64 + 32 * wave + col] = mloc;
 
     // O^T += V^T P^T; V^T operand: feature 32dt + col, the same keys as pb[kt]
     auto vread = [&](int st) -> bf16x8 {
@@ -537,7 +540,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     const float lse = (l_tot > 0.f) ? m_run * a.scale + __logf(l_tot) : -INFINITY;
     a.lse[((int64_t)t.b * a.heads_q + t.h) * (int64_t)a.n_blocks * 64 + qrow] = lse;
   }
-  if (POOL) {
+  if (pool) {
     if (hf == 0) sL2[ql] = (l_tot > 0.f) ? m_run * c + __log2f(l_tot) : INFINITY;
     wait_loads();  // the row-max stores of this workgroup have completed
     __syncthreads();
@@ -729,13 +732,11 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   if ((sparse && pool) || (pool && !a.pool_r)) return hipErrorInvalidValue;
   if (a.bf16) {
     if (a.head_dim == 128) {
-      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true, false>), grid, block, 0, s, ka);
-      else if (pool) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false, true>), grid, block, 0, s, ka);
-      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false, false>), grid, block, 0, s, ka);
+      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true>), grid, block, 0, s, ka);
+      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false>), grid, block, 0, s, ka);
     } else if (a.head_dim == 64) {
-      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true, false>), grid, block, 0, s, ka);
-      else if (pool) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false, true>), grid, block, 0, s, ka);
-      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false, false>), grid, block, 0, s, ka);
+      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true>), grid, block, 0, s, ka);
+      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false>), grid, block, 0, s, ka);
     } else {
       return hipErrorInvalidValue;
     }
