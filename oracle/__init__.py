@@ -243,3 +243,93 @@ def maxpool_gt(q: np.ndarray, k: np.ndarray, block: int = 64, scale: Optional[fl
     if rc != 0:
         raise ValueError(f"orc_maxpool_gt failed ({rc})")
     return gt if rows is not None else gt.reshape(B, Hq, nb, nb)
+
+
+# ---------------------------------------------------------------------------
+# gate distillation step (Eq. 2): KL(ground truth || gate score) and its
+# gradients with respect to the gate weights, in fp64 numpy
+# ---------------------------------------------------------------------------
+
+def _rope_angles(nb: int, Dg: int, theta: float, block: int) -> np.ndarray:
+    """[nb, Dg/2] rotation angles of the block-level RoPE: position i, plane d
+    rotates by i * (theta / block)^(-2d/Dg)."""
+    half = Dg // 2
+    w = (theta / block) ** (-2.0 * np.arange(half) / Dg)
+    return np.arange(nb, dtype=np.float64)[:, None] * w[None, :]
+
+
+def _rotate(x: np.ndarray, ang: np.ndarray, inverse: bool) -> np.ndarray:
+    """Rotates plane (d, d + Dg/2) of rows [.., nb, Dg] by +ang (or -ang)."""
+    half = x.shape[-1] // 2
+    c, s = np.cos(ang), np.sin(ang)
+    if inverse:
+        s = -s
+    a, b = x[..., :half], x[..., half:]
+    return np.concatenate([a * c - b * s, a * s + b * c], axis=-1)
+
+
+def distill(q: np.ndarray, k: np.ndarray, wq: np.ndarray, wk: np.ndarray, gt: np.ndarray,
+            block: int = 64, w_per_head: bool = True, rope_theta: float = 0.0,
+            parts: bool = False):
+    """One gate distillation step (section 3.2, Eq. 2) in fp64.
+
+    The gate's block-causal softmax P (Eq. 1, the forward of `gate`) is fitted
+    to the ground truth: each row of gt [B,Hq,nb,nb] (the 2D max-pooled
+    attention map, j <= i) is renormalised to a distribution T, and
+        loss = mean over the B*Hq*nb rows of KL(T || P) = sum_j T log(T / P)
+    with 0 log 0 = 0.  Gradients follow the chain rule backwards through the
+    softmax (dloss/dL = (P sum(T) - T) / rows), the logits, the optional
+    block-level RoPE (its inverse rotation) and the linear layers.
+    Returns (loss, dwq, dwk), dwq/dwk shaped like wq/wk; with parts=True also
+    a dict of the intermediate P, T and logits."""
+    B, Hq, S, D = q.shape
+    Hkv = k.shape[1]
+    G = Hq // Hkv
+    nb = S // block
+    Wq = np.asarray(wq, dtype=np.float64).reshape(-1, D, wq.shape[-1])
+    Wk = np.asarray(wk, dtype=np.float64).reshape(-1, 3 * D, wk.shape[-1])
+    Dg = Wq.shape[-1]
+    qp = pool(q, block, POOL_AVG)                  # [B,Hq,nb,D]
+    kp = pool(k, block, POOL_MAX_MIN_AVG)          # [B,Hkv,nb,3D]
+    wq_h = Wq if w_per_head else np.broadcast_to(Wq[:1], (Hq, D, Dg))
+    wk_g = Wk if w_per_head else np.broadcast_to(Wk[:1], (Hkv, 3 * D, Dg))
+    qg = np.einsum("bhnd,hde->bhne", qp, wq_h)
+    kg = np.einsum("bgnd,gde->bgne", kp, wk_g)
+    if rope_theta > 0:
+        ang = _rope_angles(nb, Dg, rope_theta, block)
+        qg = _rotate(qg, ang, False)
+        kg = _rotate(kg, ang, False)
+    kg_h = np.repeat(kg, G, axis=1)                # KV head of each query head
+    causal = np.tril(np.ones((nb, nb), dtype=bool))
+    L = np.einsum("bhid,bhjd->bhij", qg, kg_h) / np.sqrt(Dg)
+    L = np.where(causal, L, -np.inf)
+    m = L.max(axis=-1, keepdims=True)
+    e = np.where(causal, np.exp(L - m), 0.0)
+    P = e / e.sum(axis=-1, keepdims=True)
+    logP = np.where(causal, L - m - np.log(e.sum(axis=-1, keepdims=True)), 0.0)
+
+    g = np.where(causal, np.asarray(gt, dtype=np.float64), 0.0)
+    gs = g.sum(axis=-1, keepdims=True)
+    T = np.divide(g, gs, out=np.zeros_like(g), where=gs > 0)
+    logT = np.log(np.where(T > 0, T, 1.0))
+    rows = B * Hq * nb
+    loss = float(np.sum(T * (logT - logP)) / rows)
+
+    Tsum = T.sum(axis=-1, keepdims=True)
+    dL = np.where(causal, P * Tsum - T, 0.0) / rows
+    dqg = np.einsum("bhij,bhjd->bhid", dL, kg_h) / np.sqrt(Dg)
+    dkg_h = np.einsum("bhij,bhid->bhjd", dL, qg) / np.sqrt(Dg)
+    dkg = dkg_h.reshape(B, Hkv, G, nb, Dg).sum(axis=2)
+    if rope_theta > 0:
+        dqg = _rotate(dqg, ang, True)
+        dkg = _rotate(dkg, ang, True)
+    dwq = np.einsum("bhnd,bhne->hde", qp, dqg)
+    dwk = np.einsum("bgnd,bgne->gde", kp, dkg)
+    if not w_per_head:
+        dwq = dwq.sum(axis=0, keepdims=True)
+        dwk = dwk.sum(axis=0, keepdims=True)
+    dwq = dwq.reshape(np.shape(wq))
+    dwk = dwk.reshape(np.shape(wk))
+    if parts:
+        return loss, dwq, dwk, dict(P=P, T=T, L=L)
+    return loss, dwq, dwk

@@ -511,3 +511,72 @@ def test_gate_with_rope_equals_manual_composition():
     qg = oracle.block_rope(oracle.linear(oracle.pool(q, 64, oracle.POOL_AVG), wq), 500000.0)
     kg = oracle.block_rope(oracle.linear(oracle.pool(k, 64, oracle.POOL_MAX_MIN_AVG), wk), 500000.0)
     np.testing.assert_array_equal(L, oracle.gate_logits(qg, kg))
+
+
+# --------------------------------------------------------------------------
+# gate distillation step (Eq. 2): KL(gt || score) and weight gradients
+# --------------------------------------------------------------------------
+
+def _distill_case(seed, Hq=2, Hkv=1, S=256, D=16, Dg=8, per_head=True):
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((1, Hq, S, D)).astype(np.float32)
+    k = rng.standard_normal((1, Hkv, S, D)).astype(np.float32)
+    nw_q, nw_k = (Hq, Hkv) if per_head else (1, 1)
+    wq = rng.standard_normal((nw_q, D, Dg)) * 0.4
+    wk = rng.standard_normal((nw_k, 3 * D, Dg)) * 0.4
+    gt = oracle.maxpool_gt(q, k)
+    return q, k, wq, wk, gt
+
+
+@pytest.mark.parametrize("per_head,theta", [(True, 0.0), (True, 10000.0), (False, 0.0), (False, 500000.0)])
+def test_distill_gradients_match_finite_differences(per_head, theta):
+    q, k, wq, wk, gt = _distill_case(31 + int(per_head), per_head=per_head)
+    loss, dwq, dwk = oracle.distill(q, k, wq, wk, gt, w_per_head=per_head, rope_theta=theta)
+    assert loss > 0
+    rng = np.random.default_rng(5)
+    h = 1e-6
+    for W, dW, which in ((wq, dwq, "q"), (wk, dwk, "k")):
+        for _ in range(12):
+            idx = tuple(int(rng.integers(n)) for n in W.shape)
+            Wp, Wm = W.copy(), W.copy()
+            Wp[idx] += h
+            Wm[idx] -= h
+            args = lambda X: (X, wk) if which == "q" else (wq, X)
+            lp = oracle.distill(q, k, *args(Wp), gt, w_per_head=per_head, rope_theta=theta)[0]
+            lm = oracle.distill(q, k, *args(Wm), gt, w_per_head=per_head, rope_theta=theta)[0]
+            fd = (lp - lm) / (2 * h)
+            assert abs(fd - dW[idx]) <= 1e-6 * max(1e-3, abs(fd)) + 1e-9, (which, idx, fd, dW[idx])
+
+
+def test_distill_loss_matches_torch_kl_div_on_the_gate_softmax():
+    # P from the C gate oracle (an independent path), KL from torch's kl_div
+    q, k, wq, wk, gt = _distill_case(41)
+    loss = oracle.distill(q, k, wq, wk, gt)[0]
+    _, ell = oracle.gate(q, k, wq.astype(np.float32), wk.astype(np.float32))
+    nb = ell.shape[-1]
+    tri = np.tril(np.ones((nb, nb), bool))
+    T = np.where(tri, gt, 0.0)
+    T = T / T.sum(-1, keepdims=True)
+    logp = torch.from_numpy(np.where(tri, ell, -1e300))
+    kl = F.kl_div(logp, torch.from_numpy(T), reduction="sum").item() / (ell.size // nb)
+    # weights rounded to fp32 for the C path: compare with the same rounding
+    loss32 = oracle.distill(q, k, wq.astype(np.float32), wk.astype(np.float32), gt)[0]
+    assert abs(kl - loss32) <= 1e-12 * max(1.0, kl)
+    assert abs(loss - loss32) < 1e-3 * loss
+
+
+def test_distill_zero_at_the_optimum_and_descent():
+    q, k, wq, wk, _ = _distill_case(43)
+    _, ell = oracle.gate(q, k, wq.astype(np.float32), wk.astype(np.float32))
+    nb = ell.shape[-1]
+    tri = np.tril(np.ones((nb, nb), bool))
+    target = np.where(tri, np.exp(ell), 0.0) * 0.37  # any positive row scale: rows renormalise
+    w32q, w32k = wq.astype(np.float32).astype(np.float64), wk.astype(np.float32).astype(np.float64)
+    loss, dwq, dwk = oracle.distill(q, k, w32q, w32k, target)
+    assert abs(loss) < 1e-13
+    assert np.abs(dwq).max() < 1e-12 and np.abs(dwk).max() < 1e-12
+    # away from the optimum a small step against the gradient lowers the loss
+    q2, k2, wq2, wk2, gt2 = _distill_case(44)
+    l0, gq, gk = oracle.distill(q2, k2, wq2, wk2, gt2)
+    l1 = oracle.distill(q2, k2, wq2 - 1e-2 * gq / np.abs(gq).max(), wk2 - 1e-2 * gk / np.abs(gk).max(), gt2)[0]
+    assert l1 < l0
