@@ -16,6 +16,8 @@
  *   seer_attn_gt     dense attention that also returns the 2D max-pooled
  *                    attention map, the gate's distillation target (Eq. 2,
  *                    appendix A.1)
+ *   seer_gate_distill  the gate's distillation step (section 3.2, Eq. 2):
+ *                    KL(ground truth || gate score) and its weight gradients
  *
  * Conventions shared by every entry point:
  *  - Pointers to tensors are DEVICE pointers (HIP device memory of the current
@@ -208,6 +210,32 @@ size_t seer_attn_gt_workspace_bytes(const seer_attn_desc* desc, int32_t block, i
 seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t causal, float sm_scale,
                          const void* q, const void* k, const void* v, void* o, float* lse,
                          float* gt, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of device workspace seer_gate_distill needs for this shape (0 on
+ * invalid arguments). */
+size_t seer_gate_distill_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate);
+
+/*
+ * One distillation step of the gate (section 3.2, Eq. 2): the forward of
+ * seer_gate up to the block-causal softmax P (pooling, linear layers, the
+ * optional block-level RoPE, logits), then, with T the ground-truth row
+ * gt[b][h][i][0..i] renormalised to sum 1 (a row summing to 0 gives T = 0),
+ *   *loss = mean over the batch * heads_q * nb rows of KL(T || P)
+ *         = sum_j T_j (log T_j - log P_j) / rows,   0 log 0 = 0,
+ * and its gradients with respect to the gate weights:
+ *   dwq, dwk: device fp32, the layout of wq, wk (per head or shared, as
+ *   gate->w_per_head), overwritten (not accumulated).
+ * gt: device fp32 [batch][heads_q][nb][nb] (seer_attn_gt's output; entries
+ * j > i are not read).  loss: device fp32 scalar.  q, k, wq, wk as seer_gate.
+ * Of gate, only block, gate_dim, w_per_head and rope_theta are used.
+ * workspace: device memory of at least seer_gate_distill_workspace_bytes
+ * bytes, 256-byte aligned.  No atomics: results are identical run to run.
+ * Errors: as seer_gate; SEER_ERR_INVALID_ARG for a NULL gt, loss, dwq or dwk.
+ */
+seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* gate,
+                              const void* q, const void* k, const float* wq, const float* wk,
+                              const float* gt, float* loss, float* dwq, float* dwk,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -293,15 +293,15 @@ def distill(q: np.ndarray, k: np.ndarray, wq: np.ndarray, wk: np.ndarray, gt: np
     kp = pool(k, block, POOL_MAX_MIN_AVG)          # [B,Hkv,nb,3D]
     wq_h = Wq if w_per_head else np.broadcast_to(Wq[:1], (Hq, D, Dg))
     wk_g = Wk if w_per_head else np.broadcast_to(Wk[:1], (Hkv, 3 * D, Dg))
-    qg = np.einsum("bhnd,hde->bhne", qp, wq_h)
-    kg = np.einsum("bgnd,gde->bgne", kp, wk_g)
+    qg = qp @ wq_h
+    kg = kp @ wk_g
     if rope_theta > 0:
         ang = _rope_angles(nb, Dg, rope_theta, block)
         qg = _rotate(qg, ang, False)
         kg = _rotate(kg, ang, False)
     kg_h = np.repeat(kg, G, axis=1)                # KV head of each query head
     causal = np.tril(np.ones((nb, nb), dtype=bool))
-    L = np.einsum("bhid,bhjd->bhij", qg, kg_h) / np.sqrt(Dg)
+    L = (qg @ np.swapaxes(kg_h, -1, -2)) / np.sqrt(Dg)
     L = np.where(causal, L, -np.inf)
     m = L.max(axis=-1, keepdims=True)
     e = np.where(causal, np.exp(L - m), 0.0)
@@ -317,14 +317,14 @@ def distill(q: np.ndarray, k: np.ndarray, wq: np.ndarray, wk: np.ndarray, gt: np
 
     Tsum = T.sum(axis=-1, keepdims=True)
     dL = np.where(causal, P * Tsum - T, 0.0) / rows
-    dqg = np.einsum("bhij,bhjd->bhid", dL, kg_h) / np.sqrt(Dg)
-    dkg_h = np.einsum("bhij,bhid->bhjd", dL, qg) / np.sqrt(Dg)
+    dqg = (dL @ kg_h) / np.sqrt(Dg)
+    dkg_h = (np.swapaxes(dL, -1, -2) @ qg) / np.sqrt(Dg)
     dkg = dkg_h.reshape(B, Hkv, G, nb, Dg).sum(axis=2)
     if rope_theta > 0:
         dqg = _rotate(dqg, ang, True)
         dkg = _rotate(dkg, ang, True)
-    dwq = np.einsum("bhnd,bhne->hde", qp, dqg)
-    dwk = np.einsum("bgnd,bgne->gde", kp, dkg)
+    dwq = (np.swapaxes(qp, -1, -2) @ dqg).sum(axis=0)
+    dwk = (np.swapaxes(kp, -1, -2) @ dkg).sum(axis=0)
     if not w_per_head:
         dwq = dwq.sum(axis=0, keepdims=True)
         dwk = dwk.sum(axis=0, keepdims=True)

@@ -10,6 +10,7 @@ no CPU fallback.
     o, lse = seer.bsattn(q, k, v, mask)
     o_dense, _ = seer.dense_attn(q, k, v)
     o_dense, lse, gt = seer.attn_gt(q, k, v, want_lse=True)   # distillation target
+    loss, dwq, dwk = seer.gate_distill(q, k, wq, wk, gt)      # KL(gt || gate) and gradients
 """
 from __future__ import annotations
 
@@ -58,6 +59,8 @@ _SIGS = {
     "seer_dense_attn": ([_P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P], C.c_int),
     "seer_mask_from_dense": ([_P, C.c_int32, _P, _P, _P], C.c_int),
     "seer_attn_gt_workspace_bytes": ([_P, C.c_int32, C.c_int32], C.c_size_t),
+    "seer_gate_distill_workspace_bytes": ([_P, _P], C.c_size_t),
+    "seer_gate_distill": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P], C.c_int),
     "seer_attn_gt": ([_P, C.c_int32, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P],
                      C.c_int),
 }
@@ -293,6 +296,30 @@ def attn_gt(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
                             workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "seer_attn_gt")
     return out, lse, gt
+
+
+def gate_distill(q, k, wq, wk, gt, *, w_per_head: bool = True, rope_theta: float = 0.0,
+                 dwq=None, dwk=None, loss=None, workspace=None, stream=None):
+    """One gate distillation step (seer_gate_distill): returns (loss [1], dwq, dwk)
+    as device fp32 tensors; loss is the mean KL(renormalised gt || gate softmax)."""
+    torch = _torch()
+    d = make_desc(q, k)
+    gd = gate_desc(wq.shape[-1], TOPK_RATIO, topk_ratio=1.0, w_per_head=w_per_head,
+                   rope_theta=rope_theta)
+    if dwq is None:
+        dwq = torch.empty_like(wq)
+    if dwk is None:
+        dwk = torch.empty_like(wk)
+    if loss is None:
+        loss = torch.empty(1, dtype=torch.float32, device=q.device)
+    if workspace is None:
+        n = lib().seer_gate_distill_workspace_bytes(C.byref(d), C.byref(gd))
+        workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=q.device)
+    st = lib().seer_gate_distill(C.byref(d), C.byref(gd), _ptr(q), _ptr(k), _ptr(wq), _ptr(wk),
+                                 _ptr(gt), _ptr(loss), _ptr(dwq), _ptr(dwk), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "seer_gate_distill")
+    return loss, dwq, dwk
 
 
 def mask_from_dense(dense, heads_kv: int = 1, mask: Optional[BlockMask] = None,

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libseer.so")
-SOURCES = ["gate_kernels.hip", "attn_kernels.hip", "seer_api.cpp"]
+SOURCES = ["gate_kernels.hip", "attn_kernels.hip", "distill_kernels.hip", "seer_api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # packed-FP32 instructions are disabled: plain float code must not be turned

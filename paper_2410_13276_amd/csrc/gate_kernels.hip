@@ -54,7 +54,8 @@ template <typename T, int D, int DG, bool IS_K>
 __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t ss, int nb,
                                                const float* __restrict__ W,
                                                float* __restrict__ out, float* smem,
-                                               float* srot, double rope_base) {
+                                               float* srot, double rope_base,
+                                               float* __restrict__ pooled_out) {
   constexpr int EPL = Load16<T>::N;  // elements per 16-byte load
   constexpr int TPR = D / EPL;       // threads per block row
   constexpr int R = 256 / TPR;       // blocks per workgroup
@@ -99,6 +100,17 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
         prow[2 * D + e] = avg;
       } else {
         prow[e] = avg;
+      }
+    }
+    if (pooled_out) {  // the pooled row itself (kept for the gate's weight gradients)
+      float* po = pooled_out + (int64_t)blk * WIDTH + c * EPL;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) {
+        po[e] = prow[e];
+        if (IS_K) {
+          po[D + e] = prow[D + e];
+          po[2 * D + e] = prow[2 * D + e];
+        }
       }
     }
   }
@@ -165,14 +177,16 @@ __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
     const int h = slot;
     const T* x = static_cast<const T*>(a.q.ptr) + b * a.q.sb + h * a.q.sh;
     float* out = a.qg + ((int64_t)b * a.heads_q + h) * a.n_blocks * DG;
+    float* po = a.qp ? a.qp + ((int64_t)b * a.heads_q + h) * a.n_blocks * D : nullptr;
     pool_proj_head<T, D, DG, false>(x, a.q.ss, a.n_blocks, a.wq + h * a.wq_head_stride, out, smem, srot,
-                                    a.rope_base);
+                                    a.rope_base, po);
   } else {
     const int g = slot - a.heads_q;
     const T* x = static_cast<const T*>(a.k.ptr) + b * a.k.sb + g * a.k.sh;
     float* out = a.kg + ((int64_t)b * a.heads_kv + g) * a.n_blocks * DG;
+    float* po = a.kp ? a.kp + ((int64_t)b * a.heads_kv + g) * a.n_blocks * 3 * D : nullptr;
     pool_proj_head<T, D, DG, true>(x, a.k.ss, a.n_blocks, a.wk + g * a.wk_head_stride, out, smem, srot,
-                                   a.rope_base);
+                                   a.rope_base, po);
   }
 }
 

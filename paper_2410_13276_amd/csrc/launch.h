@@ -22,6 +22,8 @@ struct PoolProjArgs {
   float* qg;  // [B][Hq][nb][Dg]
   float* kg;  // [B][Hkv][nb][Dg]
   double rope_base;  // > 0: block-level RoPE with this base (model base / block)
+  float* qp;  // optional pooled Q [B][Hq][nb][D] (nullptr: not stored)
+  float* kp;  // optional pooled K [B][Hkv][nb][3D]
 };
 
 struct GateLogitsArgs {
@@ -71,7 +73,42 @@ struct AttnArgs {
   float* gt;
 };
 
+// Gate distillation (Eq. 2): row-wise KL between the renormalised ground truth
+// and the gate softmax, and the logit gradient written over the logits.
+struct KlArgs {
+  float* logits;       // [rows][nb] in: logits (j <= i), out: dloss/dlogit (0 for j > i)
+  const float* gt;     // [rows][nb] ground truth (j <= i read)
+  int64_t rows;
+  int n_blocks;
+  float inv_rows;      // 1 / rows: the loss is the mean over rows
+  double* row_loss;    // [rows]
+  float* loss;         // device scalar: mean of row_loss
+};
+
+// C[z][m][n] = alpha * sum_{k1 < K1, k2 < K2} A(z, m, k1, k2) * B(z / bdiv, k1, k2, n), fp32,
+// with element strides; tri = 1: A vanishes for k2 > m, tri = 2: for k2 < m.
+struct GemmArgs {
+  const float* A;
+  const float* B;
+  float* C;
+  int M, N, K1, K2, Z, bdiv, tri;
+  int64_t sam, sak1, sak2, saz;
+  int64_t sbk1, sbk2, sbn, sbz;
+  int64_t scm, scz;
+  float alpha;
+};
+
+struct RopeArgs {  // inverse block-level RoPE of rows [rows][nb][Dg], in place
+  float* x;
+  int64_t rows;
+  int n_blocks, gate_dim;
+  double base;
+};
+
 hipError_t launch_pool_proj(const PoolProjArgs& a, hipStream_t s);
+hipError_t launch_kl_rows(const KlArgs& a, hipStream_t s);
+hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
+hipError_t launch_rope_inverse(const RopeArgs& a, hipStream_t s);
 hipError_t launch_gate_logits(const GateLogitsArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_mask_from_dense(const MaskFromDenseArgs& a, hipStream_t s);

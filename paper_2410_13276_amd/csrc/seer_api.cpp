@@ -47,7 +47,8 @@ seer_status check_desc(const seer_attn_desc* d, int tensors) {
 
 seer::TensorView view(const void* p, const int64_t* st) { return {p, st[0], st[1], st[2]}; }
 
-seer_status check_gate(const seer_attn_desc* d, const seer_gate_desc* g) {
+// Checks of the gate shape and weights (shared by seer_gate and seer_gate_distill).
+seer_status check_gate_common(const seer_attn_desc* d, const seer_gate_desc* g) {
   seer_status s = check_desc(d, 0x3);
   if (s != SEER_OK) return s;
   if (!g) return SEER_ERR_INVALID_ARG;
@@ -55,6 +56,12 @@ seer_status check_gate(const seer_attn_desc* d, const seer_gate_desc* g) {
   if (g->gate_dim != 32 && g->gate_dim != 64 && g->gate_dim != 128) return SEER_ERR_UNSUPPORTED;
   if (d->seq_len / SEER_BLOCK > 4096) return SEER_ERR_UNSUPPORTED;
   if (!(g->rope_theta >= 0.0) || std::isinf(g->rope_theta)) return SEER_ERR_INVALID_ARG;
+  return SEER_OK;
+}
+
+seer_status check_gate(const seer_attn_desc* d, const seer_gate_desc* g) {
+  seer_status s = check_gate_common(d, g);
+  if (s != SEER_OK) return s;
   switch (g->mode) {
     case SEER_TOPK_RATIO:
       if (!(g->topk_ratio > 0.0 && g->topk_ratio <= 1.0)) return SEER_ERR_INVALID_ARG;
@@ -82,6 +89,34 @@ GateLayout gate_layout(const seer_attn_desc* d, const seer_gate_desc* g, bool lo
   L.kg = round_up((size_t)d->batch * d->heads_q * nb * g->gate_dim * 4);
   L.logits = L.kg + round_up((size_t)d->batch * d->heads_kv * nb * g->gate_dim * 4);
   L.total = L.logits + (logits_in_ws ? round_up((size_t)d->batch * d->heads_q * nb * nb * 4) : 0);
+  return L;
+}
+
+// Workspace of seer_gate_distill: projected rows, pooled rows, logits (then
+// their gradient), projected-row gradients, per-row losses.
+struct DistillLayout {
+  size_t qg, kg, qp, kp, logits, dqg, dkg, row_loss, total;
+};
+
+DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g) {
+  const size_t nb = (size_t)(d->seq_len / SEER_BLOCK);
+  const size_t B = d->batch, Hq = d->heads_q, Hkv = d->heads_kv, D = d->head_dim, Dg = g->gate_dim;
+  DistillLayout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += round_up(bytes);
+    return at;
+  };
+  L.qg = take(B * Hq * nb * Dg * 4);
+  L.kg = take(B * Hkv * nb * Dg * 4);
+  L.qp = take(B * Hq * nb * D * 4);
+  L.kp = take(B * Hkv * nb * 3 * D * 4);
+  L.logits = take(B * Hq * nb * nb * 4);
+  L.dqg = take(B * Hq * nb * Dg * 4);
+  L.dkg = take(B * Hkv * nb * Dg * 4);
+  L.row_loss = take(B * Hq * nb * 8);
+  L.total = off;
   return L;
 }
 
@@ -198,6 +233,8 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   pa.qg = qg;
   pa.kg = kg;
   pa.rope_base = gate->rope_theta > 0.0 ? gate->rope_theta / gate->block : 0.0;
+  pa.qp = nullptr;
+  pa.kp = nullptr;
   if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
 
   seer::GateLogitsArgs la;
@@ -326,6 +363,152 @@ seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t caus
       if ((s = from_hip(seer::launch_attn(c, st))) != SEER_OK) return s;
     }
   return SEER_OK;
+}
+
+size_t seer_gate_distill_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate) {
+  if (check_gate_common(desc, gate) != SEER_OK) return 0;
+  return distill_layout(desc, gate).total;
+}
+
+seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* gate, const void* q,
+                              const void* k, const float* wq, const float* wk, const float* gt,
+                              float* loss, float* dwq, float* dwk, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  seer_status s = check_gate_common(desc, gate);
+  if (s != SEER_OK) return s;
+  if (!q || !k || !wq || !wk || !gt || !loss || !dwq || !dwk) return SEER_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
+  const DistillLayout W = distill_layout(desc, gate);
+  if (!workspace || workspace_bytes < W.total) return SEER_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
+
+  char* ws = static_cast<char*>(workspace);
+  float* qg = reinterpret_cast<float*>(ws + W.qg);
+  float* kg = reinterpret_cast<float*>(ws + W.kg);
+  float* qp = reinterpret_cast<float*>(ws + W.qp);
+  float* kp = reinterpret_cast<float*>(ws + W.kp);
+  float* dl = reinterpret_cast<float*>(ws + W.logits);
+  float* dqg = reinterpret_cast<float*>(ws + W.dqg);
+  float* dkg = reinterpret_cast<float*>(ws + W.dkg);
+  double* row_loss = reinterpret_cast<double*>(ws + W.row_loss);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int B = desc->batch, Hq = desc->heads_q, Hkv = desc->heads_kv, D = desc->head_dim;
+  const int Dg = gate->gate_dim, G = Hq / Hkv;
+  const int nb = desc->seq_len / SEER_BLOCK;
+  const double rope_base = gate->rope_theta > 0.0 ? gate->rope_theta / gate->block : 0.0;
+  const float rsqrt_dg = (float)(1.0 / std::sqrt((double)Dg));
+
+  // forward: pooled rows (kept), projected rows, logits
+  seer::PoolProjArgs pa;
+  pa.q = view(q, desc->q_stride);
+  pa.k = view(k, desc->k_stride);
+  pa.batch = B;
+  pa.heads_q = Hq;
+  pa.heads_kv = Hkv;
+  pa.n_blocks = nb;
+  pa.head_dim = D;
+  pa.gate_dim = Dg;
+  pa.bf16 = desc->dtype == SEER_BF16;
+  pa.wq = wq;
+  pa.wk = wk;
+  pa.wq_head_stride = gate->w_per_head ? (int64_t)D * Dg : 0;
+  pa.wk_head_stride = gate->w_per_head ? (int64_t)3 * D * Dg : 0;
+  pa.qg = qg;
+  pa.kg = kg;
+  pa.rope_base = rope_base;
+  pa.qp = qp;
+  pa.kp = kp;
+  if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
+
+  seer::GateLogitsArgs la;
+  la.qg = qg;
+  la.kg = kg;
+  la.batch = B;
+  la.heads_q = Hq;
+  la.heads_kv = Hkv;
+  la.n_blocks = nb;
+  la.gate_dim = Dg;
+  la.scale = rsqrt_dg;
+  la.logits = dl;
+  if ((s = from_hip(seer::launch_gate_logits(la, st))) != SEER_OK) return s;
+
+  // loss and logit gradient
+  seer::KlArgs ka;
+  ka.logits = dl;
+  ka.gt = gt;
+  ka.rows = (int64_t)B * Hq * nb;
+  ka.n_blocks = nb;
+  ka.inv_rows = (float)(1.0 / (double)ka.rows);
+  ka.row_loss = row_loss;
+  ka.loss = loss;
+  if ((s = from_hip(seer::launch_kl_rows(ka, st))) != SEER_OK) return s;
+
+  const int64_t nn = (int64_t)nb * nb;
+  // dQg[b,h] = dL[b,h] Kg[b,g] / sqrt(Dg)   (dL lower triangular)
+  seer::GemmArgs g{};
+  g.A = dl; g.B = kg; g.C = dqg;
+  g.M = nb; g.N = Dg; g.K1 = 1; g.K2 = nb; g.Z = B * Hq; g.bdiv = G; g.tri = 1;
+  g.sam = nb; g.sak1 = 0; g.sak2 = 1; g.saz = nn;
+  g.sbk1 = 0; g.sbk2 = Dg; g.sbn = 1; g.sbz = (int64_t)nb * Dg;
+  g.scm = Dg; g.scz = (int64_t)nb * Dg;
+  g.alpha = rsqrt_dg;
+  if ((s = from_hip(seer::launch_gemm_f32(g, st))) != SEER_OK) return s;
+
+  // dKg[b,g][j] = sum over the group's heads h and rows i of dL[b,h][i][j] Qg[b,h][i] / sqrt(Dg)
+  g = seer::GemmArgs{};
+  g.A = dl; g.B = qg; g.C = dkg;
+  g.M = nb; g.N = Dg; g.K1 = G; g.K2 = nb; g.Z = B * Hkv; g.bdiv = 1; g.tri = 2;
+  g.sam = 1; g.sak1 = nn; g.sak2 = nb; g.saz = G * nn;
+  g.sbk1 = (int64_t)nb * Dg; g.sbk2 = Dg; g.sbn = 1; g.sbz = (int64_t)G * nb * Dg;
+  g.scm = Dg; g.scz = (int64_t)nb * Dg;
+  g.alpha = rsqrt_dg;
+  if ((s = from_hip(seer::launch_gemm_f32(g, st))) != SEER_OK) return s;
+
+  if (rope_base > 0.0) {  // back through the block-level RoPE
+    seer::RopeArgs ra{dqg, (int64_t)B * Hq, nb, Dg, rope_base};
+    if ((s = from_hip(seer::launch_rope_inverse(ra, st))) != SEER_OK) return s;
+    ra = seer::RopeArgs{dkg, (int64_t)B * Hkv, nb, Dg, rope_base};
+    if ((s = from_hip(seer::launch_rope_inverse(ra, st))) != SEER_OK) return s;
+  }
+
+  // dWq[h] = sum over b, i of Qp[b,h,i]^T dQg[b,h,i] (shared weights: also over h)
+  const bool ph = gate->w_per_head != 0;
+  g = seer::GemmArgs{};
+  g.A = qp; g.B = dqg; g.C = dwq;
+  g.M = D; g.N = Dg; g.K2 = nb; g.bdiv = 1; g.tri = 0;
+  g.sam = 1; g.sak2 = D;
+  g.sbk2 = Dg; g.sbn = 1;
+  g.scm = Dg; g.scz = (int64_t)D * Dg;
+  g.alpha = 1.0f;
+  if (ph) {
+    g.Z = Hq; g.K1 = B;
+    g.saz = (int64_t)nb * D; g.sak1 = (int64_t)Hq * nb * D;
+    g.sbz = (int64_t)nb * Dg; g.sbk1 = (int64_t)Hq * nb * Dg;
+  } else {
+    g.Z = 1; g.K1 = B * Hq;
+    g.saz = 0; g.sak1 = (int64_t)nb * D;
+    g.sbz = 0; g.sbk1 = (int64_t)nb * Dg;
+  }
+  if ((s = from_hip(seer::launch_gemm_f32(g, st))) != SEER_OK) return s;
+
+  // dWk[g] = sum over b, j of Kp[b,g,j]^T dKg[b,g,j]
+  g = seer::GemmArgs{};
+  g.A = kp; g.B = dkg; g.C = dwk;
+  g.M = 3 * D; g.N = Dg; g.K2 = nb; g.bdiv = 1; g.tri = 0;
+  g.sam = 1; g.sak2 = 3 * D;
+  g.sbk2 = Dg; g.sbn = 1;
+  g.scm = Dg; g.scz = (int64_t)3 * D * Dg;
+  g.alpha = 1.0f;
+  if (ph) {
+    g.Z = Hkv; g.K1 = B;
+    g.saz = (int64_t)nb * 3 * D; g.sak1 = (int64_t)Hkv * nb * 3 * D;
+    g.sbz = (int64_t)nb * Dg; g.sbk1 = (int64_t)Hkv * nb * Dg;
+  } else {
+    g.Z = 1; g.K1 = B * Hkv;
+    g.saz = 0; g.sak1 = (int64_t)nb * 3 * D;
+    g.sbz = 0; g.sbk1 = (int64_t)nb * Dg;
+  }
+  return from_hip(seer::launch_gemm_f32(g, st));
 }
 
 }  // extern "C"

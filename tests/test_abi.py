@@ -24,7 +24,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 10, names
+    assert len(names) == 12, names
     L = C.CDLL(seer.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -167,3 +167,23 @@ def test_attn_gt_workspace_and_rejects_bad_args():
         seer.ERR_INVALID_ARG                                                  # misaligned workspace
     assert L.seer_attn_gt(C.byref(d), 128, 1, 0.0, *args, FAKE, FAKE * 16, 1 << 40, None) == \
         seer.ERR_UNSUPPORTED
+
+
+def test_gate_distill_workspace_and_rejects_bad_args():
+    L = seer.lib()
+    d, g = _desc(B=1, Hq=4, Hkv=2, S=1024, D=128), _gate()
+    nb, up = 16, (lambda x: (x + 255) // 256 * 256)
+    want = (up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up(4 * nb * 128 * 4) + up(2 * nb * 384 * 4)
+            + up(4 * nb * nb * 4) + up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up(4 * nb * 8))
+    need = L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g))
+    assert need == want
+    g.mode = 9  # the selection mode is not used by the distillation step
+    assert L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g)) == want
+    call = lambda gt=FAKE, ws=FAKE * 16, n=need, gd=g: L.seer_gate_distill(
+        C.byref(d), C.byref(gd), FAKE, FAKE, FAKE, FAKE, gt, FAKE, FAKE, FAKE, ws, n, None)
+    assert call(gt=None) == seer.ERR_INVALID_ARG
+    assert call(n=need - 1) == seer.ERR_WORKSPACE
+    assert call(ws=None) == seer.ERR_WORKSPACE
+    assert call(ws=FAKE * 16 + 16) == seer.ERR_INVALID_ARG
+    assert call(gd=_gate(gate_dim=48)) == seer.ERR_UNSUPPORTED
+    assert call(gd=_gate(rope_theta=-2.0)) == seer.ERR_INVALID_ARG
