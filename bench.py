@@ -160,11 +160,14 @@ def main() -> int:
     ws = torch.empty(max(1, seer.gate_workspace_bytes(qd, kd, w.gate_dim)), dtype=torch.uint8, device="cuda")
     o = torch.empty_like(qd)
     od = torch.empty_like(qd)
+    # key-range split workspace (sparse and dense get the same treatment)
+    n_aws = seer.attn_workspace_bytes(qd, kd, vd)
+    aws = torch.empty(n_aws, dtype=torch.uint8, device="cuda") if n_aws else None
     stream = torch.cuda.current_stream()
 
     def step():
         seer.gate(qd, kd, wqd, wkd, **gate_kw, mask=mask, workspace=ws)
-        seer.bsattn(qd, kd, vd, mask, out=o)
+        seer.bsattn(qd, kd, vd, mask, out=o, workspace=aws)
 
     for _ in range(args.warmup):
         step()
@@ -184,7 +187,7 @@ def main() -> int:
         ev[s][0].record(stream)
         seer.gate(qd, kd, wqd, wkd, **gate_kw, mask=mask, workspace=ws)
         ev[s][1].record(stream)
-        seer.bsattn(qd, kd, vd, mask, out=o)
+        seer.bsattn(qd, kd, vd, mask, out=o, workspace=aws)
         ev[s][2].record(stream)
     end.record(stream)
     torch.cuda.synchronize()
@@ -195,13 +198,13 @@ def main() -> int:
     attn_min = float(np.min([e[1].elapsed_time(e[2]) for e in ev]))
 
     # dense comparison at the same shape, same cache treatment
-    seer.dense_attn(qd, kd, vd, out=od)
+    seer.dense_attn(qd, kd, vd, out=od, workspace=aws)
     torch.cuda.synchronize()
     dts = []
     for _ in range(args.dense_runs):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        seer.dense_attn(qd, kd, vd, out=od)
+        seer.dense_attn(qd, kd, vd, out=od, workspace=aws)
         b.record(stream)
         torch.cuda.synchronize()
         dts.append(a.elapsed_time(b))
@@ -229,6 +232,9 @@ def main() -> int:
         del gt_ws, gt_map
 
     active_flops = flops_tile * active
+    D = w.head_dim
+    attn_kernels = (f"split_bounds_kernel + attn_fwd_bf16_kernel<{D}, true, true> + split_merge_kernel<{D}> "
+                    "(one seer_bsattn_ws call)" if aws is not None else f"attn_fwd_bf16_kernel<{D}, true, false>")
     attn_tflops = active_flops / (attn_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     speedup = dense_ms / attn_ms
@@ -269,7 +275,7 @@ def main() -> int:
             "ms": round(gt_ms, 3), "dense_ms": round(dense_ms, 3),
             "overhead_vs_dense": round(gt_ms / dense_ms - 1.0, 4),
             "workspace_bytes": gt_ws_bytes, "map_bytes": 4 * w.batch * w.heads_q * nb * nb},
-        "roofline": {"bound": "mfma", "kernel": "attn_fwd_bf16_kernel<128, true>",
+        "roofline": {"bound": "mfma", "kernel": attn_kernels,
                      "achieved": round(attn_tflops, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(attn_tflops / peak, 4), "traffic": _traffic(w.name),
                      "flops_per_launch": active_flops},
@@ -278,7 +284,7 @@ def main() -> int:
         f"attn {attn_tflops:.1f} TF/s; dense {dense_ms:.2f} ms; speedup {speedup:.2f}x "
         f"(ideal {1 / (1 - sparsity):.2f}x)")
     if not args.no_cpu_baseline:
-        del qd, kd, vd, o, od, ws
+        del qd, kd, vd, o, od, ws, aws
         result["cpu_baseline"] = cpu_baseline(w, q, k, v, wq, wk, args.cpu_rows)
     print(json.dumps(result), flush=True)
     return 0

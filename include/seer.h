@@ -11,6 +11,8 @@
  *   seer_bsattn      block-sparse causal attention over the active tiles (section 3.3)
  *   seer_dense_attn  the same kernel over every causal tile (the dense baseline
  *                    the paper compares against in section 4.2)
+ *   seer_bsattn_ws, seer_dense_attn_ws  the same with a workspace that lets
+ *                    long rows be split into key ranges for L2 locality
  *   seer_mask_from_dense  compaction of a caller-made 0/1 block mask into the
  *                    index-list form seer_bsattn reads
  *   seer_attn_gt     dense attention that also returns the 2D max-pooled
@@ -174,6 +176,38 @@ seer_status seer_bsattn(const seer_attn_desc* desc, int32_t block, const seer_bl
 seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm_scale,
                             const void* q, const void* k, const void* v, void* o, float* lse,
                             void* stream);
+
+/*
+ * Workspace bytes that let seer_bsattn_ws / seer_dense_attn_ws run the
+ * key-range split for this shape, or 0 when the shape does not split (then
+ * those calls need no workspace).  The split applies to causal bf16 attention
+ * with nb a multiple of 16 and nb / 16 >= the minimum range width (32 blocks;
+ * the environment variable SEER_SPLIT_MIN_WIDTH, read at each call, overrides
+ * it).  Size: 68 bytes per query block plus (256 + 128 head_dim) bytes per
+ * partial slot; a query head has sum over i of (floor(i / (nb / 16)) + 1),
+ * about 8.5 nb, slots (9.3 GB for 32 heads of 131072 tokens, head_dim 128).
+ */
+size_t seer_attn_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t causal);
+
+/*
+ * seer_bsattn / seer_dense_attn with a workspace for the key-range split: each
+ * causal row is cut into 16 ranges of key blocks computed as separate tasks,
+ * the ranges of one KV group distributed over the XCDs so that each XCD's L2
+ * holds the K/V it reads; the normalised partial outputs (bf16) and their
+ * log-sum-exps go to the workspace and a merge kernel writes O and LSE.  O may
+ * differ from the unsplit call by the rounding of the partials (well inside
+ * the bf16 output tolerance).  With workspace NULL, or smaller than
+ * seer_attn_workspace_bytes, or a shape that does not split, the call is the
+ * unsplit one.  workspace: device memory, 256-byte aligned; contents on
+ * return unspecified.
+ */
+seer_status seer_bsattn_ws(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
+                           int32_t causal, float sm_scale, const void* q, const void* k,
+                           const void* v, void* o, float* lse, void* workspace,
+                           size_t workspace_bytes, void* stream);
+seer_status seer_dense_attn_ws(const seer_attn_desc* desc, int32_t causal, float sm_scale,
+                               const void* q, const void* k, const void* v, void* o, float* lse,
+                               void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * Compacts a 0/1 block mask dense (device uint8 [B][Hq][nb][nb]; any non-zero

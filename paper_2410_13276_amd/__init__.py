@@ -60,6 +60,10 @@ _SIGS = {
     "seer_mask_from_dense": ([_P, C.c_int32, _P, _P, _P], C.c_int),
     "seer_attn_gt_workspace_bytes": ([_P, C.c_int32, C.c_int32], C.c_size_t),
     "seer_gate_distill_workspace_bytes": ([_P, _P], C.c_size_t),
+    "seer_attn_workspace_bytes": ([_P, C.c_int32, C.c_int32], C.c_size_t),
+    "seer_bsattn_ws": ([_P, C.c_int32, _P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, C.c_size_t, _P],
+                       C.c_int),
+    "seer_dense_attn_ws": ([_P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, C.c_size_t, _P], C.c_int),
     "seer_gate_distill": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P], C.c_int),
     "seer_attn_gt": ([_P, C.c_int32, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P],
                      C.c_int),
@@ -235,9 +239,23 @@ def gate(q, k, wq, wk, *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
     return mask
 
 
+def attn_workspace_bytes(q, k, v=None, causal: bool = True) -> int:
+    """Workspace that enables the key-range split of bsattn / dense_attn for
+    this shape (0: the shape does not split)."""
+    d = make_desc(q, k, v)
+    return lib().seer_attn_workspace_bytes(C.byref(d), BLOCK, int(bool(causal)))
+
+
+def _ws_args(workspace):
+    if workspace is None:
+        return None, 0
+    return _ptr(workspace), workspace.numel() * workspace.element_size()
+
+
 def bsattn(q, k, v, mask: BlockMask, *, causal: bool = True, sm_scale: float = 0.0, out=None,
-           lse: Optional[object] = None, want_lse: bool = False, stream=None):
-    """Block-sparse attention (seer_bsattn).  Returns (O, LSE or None)."""
+           lse: Optional[object] = None, want_lse: bool = False, workspace=None, stream=None):
+    """Block-sparse attention (seer_bsattn; seer_bsattn_ws with a workspace,
+    which enables the key-range split).  Returns (O, LSE or None)."""
     torch = _torch()
     if out is None:
         out = torch.empty_like(q)
@@ -245,24 +263,37 @@ def bsattn(q, k, v, mask: BlockMask, *, causal: bool = True, sm_scale: float = 0
         lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
     d = make_desc(q, k, v, out)
     ms = mask.struct()
-    st = lib().seer_bsattn(C.byref(d), BLOCK, C.byref(ms), int(bool(causal)), float(sm_scale),
-                           _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
-    _check(st, "seer_bsattn")
+    if workspace is None:
+        st = lib().seer_bsattn(C.byref(d), BLOCK, C.byref(ms), int(bool(causal)), float(sm_scale),
+                               _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
+        _check(st, "seer_bsattn")
+    else:
+        wp, wn = _ws_args(workspace)
+        st = lib().seer_bsattn_ws(C.byref(d), BLOCK, C.byref(ms), int(bool(causal)), float(sm_scale),
+                                  _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), wp, wn, _stream(stream))
+        _check(st, "seer_bsattn_ws")
     return out, lse
 
 
 def dense_attn(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
-               lse: Optional[object] = None, want_lse: bool = False, stream=None):
-    """Dense attention over every (causal) block (seer_dense_attn).  Returns (O, LSE or None)."""
+               lse: Optional[object] = None, want_lse: bool = False, workspace=None, stream=None):
+    """Dense attention over every (causal) block (seer_dense_attn; seer_dense_attn_ws
+    with a workspace).  Returns (O, LSE or None)."""
     torch = _torch()
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:
         lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
     d = make_desc(q, k, v, out)
-    st = lib().seer_dense_attn(C.byref(d), int(bool(causal)), float(sm_scale), _ptr(q), _ptr(k),
-                               _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
-    _check(st, "seer_dense_attn")
+    if workspace is None:
+        st = lib().seer_dense_attn(C.byref(d), int(bool(causal)), float(sm_scale), _ptr(q), _ptr(k),
+                                   _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
+        _check(st, "seer_dense_attn")
+    else:
+        wp, wn = _ws_args(workspace)
+        st = lib().seer_dense_attn_ws(C.byref(d), int(bool(causal)), float(sm_scale), _ptr(q), _ptr(k),
+                                      _ptr(v), _ptr(out), _ptr(lse), wp, wn, _stream(stream))
+        _check(st, "seer_dense_attn_ws")
     return out, lse
 
 

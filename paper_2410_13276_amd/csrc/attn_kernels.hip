@@ -29,6 +29,8 @@
 // MFMA 32x32 output layout used throughout: accumulator e of lane L holds
 // row 8*(e/4) + 4*(L/32) + e%4, column L%32.  Operand k-slots only need to agree
 // between A and B (lane half + slot), which every product below guarantees.
+#include <cstdlib>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -38,6 +40,7 @@ namespace {
 
 struct Task {
   int b, h, i;
+  int p;  // key range of a split task (0 otherwise)
 };
 
 // Task order.  Workgroups are dispatched round-robin over the 8 XCDs (each
@@ -80,12 +83,57 @@ __device__ __forceinline__ Task decode_task(const TaskMap& m, int wg) {
     t.h = rem % m.heads_q;
     t.i = m.nb - 1 - nu;
   }
+  t.p = 0;
   return t;
+}
+
+// Key-range split.  Each causal row is cut into P ranges of w key blocks
+// (P w = nb); range p of row i exists when p w <= i.  Workgroup w runs on XCD
+// x = w % 8 as that XCD's (w / 8)-th task, and KV groups (batch x KV head) are
+// processed in order.  Every XCD gets the same causal work:
+//  - P = 16: within each group, XCD x takes range x and then range 15 - x;
+//  - P = 8: groups go in pairs, XCD x taking range x of the first and range
+//    7 - x of the second (the XCDs then drift apart by up to a group, whose
+//    K and V the Infinity Cache holds).
+// Within a range: every query head of the group and every query block that
+// reaches the range, heaviest first.  An XCD thus reads w key blocks of K and
+// V at a time, which its L2 holds.
+struct SplitMap {
+  int heads_q, heads_kv, nb, w, parts;
+};
+
+__device__ __forceinline__ Task decode_split(const SplitMap& m, int wg) {
+  const int G = m.heads_q / m.heads_kv;
+  const int x = wg % 8;
+  const int u = wg / 8;
+  const int pa = x, pb = m.parts - 1 - x;
+  const int ta = G * (m.nb - pa * m.w), tb = G * (m.nb - pb * m.w);
+  const int unit = u / (ta + tb);  // a group (P = 16) or a pair of groups (P = 8)
+  const int rem = u % (ta + tb);
+  const bool first = rem < ta;
+  int ph;
+  if (m.parts == 16) ph = unit;
+  else ph = 2 * unit + (first ? 0 : 1);
+  const int idx = first ? rem : rem - ta;
+  Task t;
+  t.p = first ? pa : pb;
+  t.i = m.nb - 1 - idx / G;
+  t.b = ph / m.heads_kv;
+  t.h = (ph % m.heads_kv) * G + idx % G;
+  return t;
+}
+
+// Partial slots of the rows before row i of one (batch, head): row i' owns
+// floor(i' / w) + 1 consecutive slots, one per range it reaches.
+__device__ __forceinline__ int64_t split_offset(int i, int w) {
+  const int64_t q = i / w, r = i % w;
+  return i + w * q * (q - 1) / 2 + r * q;
 }
 
 struct KernelArgs {
   AttnArgs a;
   TaskMap map;
+  SplitMap split;
   float scale_log2;  // scale * log2(e)
 };
 
@@ -96,24 +144,38 @@ template <bool SPARSE>
 struct RowList {
   const uint16_t* idx;
   int n, nb, i;
+  int lo;  // dense: first key block
   bool causal;
-  __device__ __forceinline__ int at(int p) const { return SPARSE ? (int)idx[p] : p; }
+  __device__ __forceinline__ int at(int p) const { return SPARSE ? (int)idx[p] : lo + p; }
   __device__ __forceinline__ bool ok(int j) const { return j < nb && (!causal || j <= i); }
 };
 
-template <bool SPARSE>
+// The row's list; for a split task only the entries of its key range (for
+// sparse rows located by split_bounds_kernel beforehand).
+template <bool SPARSE, bool SPLIT = false>
 __device__ __forceinline__ RowList<SPARSE> make_list(const AttnArgs& a, const Task& t) {
   RowList<SPARSE> L;
   L.nb = a.n_blocks;
   L.i = t.i;
   L.causal = a.causal;
+  L.lo = 0;
   const int64_t row = ((int64_t)t.b * a.heads_q + t.h) * a.n_blocks + t.i;
   if (SPARSE) {
     L.idx = a.idx + row * a.n_blocks;
     L.n = min(max(a.count[row], 0), a.n_blocks);
+    if (SPLIT) {
+      const int32_t* bd = a.split_bounds + row * (a.split_parts + 1) + t.p;
+      const int s0 = bd[0];
+      L.idx += s0;
+      L.n = bd[1] - s0;
+    }
   } else {
     L.idx = nullptr;
     L.n = a.causal ? t.i + 1 : a.n_blocks;
+    if (SPLIT) {
+      L.lo = t.p * a.split_w;
+      L.n = min(L.lo + a.split_w, t.i + 1) - L.lo;
+    }
   }
   return L;
 }
@@ -272,7 +334,11 @@ constexpr int kListChunk = 256;
 //
 // The dense instantiation also serves the ground-truth mode (a.gt set): a
 // uniform runtime switch rather than a third instantiation.
-template <int D, bool SPARSE>
+//
+// With SPLIT the workgroup computes one key range of its row and stores the
+// normalised partial output (bf16) and its log2-domain log-sum-exp in the
+// range's partial slot; split_merge_kernel combines the slots afterwards.
+template <int D, bool SPARSE, bool SPLIT>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_bf16_kernel(KernelArgs ka) {
   using Lay = Bf16Layout<D>;
@@ -282,7 +348,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   __shared__ __attribute__((aligned(16))) float sL2[SPARSE ? 1 : 64];
 
   const AttnArgs& a = ka.a;
-  const Task t = decode_task(ka.map, blockIdx.x);
+  const Task t = SPLIT ? decode_split(ka.split, blockIdx.x) : decode_task(ka.map, blockIdx.x);
   const int tid = threadIdx.x;
   const int wave = tid / 64;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
@@ -333,8 +399,8 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   for (int dt = 0; dt < D / 32; ++dt) voff[dt] = vrow * D + 8 * ((4 * dt + d0 / 8) ^ fvl) + d0 % 8;
 
   // row list
-  const RowList<SPARSE> list = make_list<SPARSE>(a, t);
-  const bool pool = !SPARSE && a.gt != nullptr;  // ground-truth mode
+  const RowList<SPARSE> list = make_list<SPARSE, SPLIT>(a, t);
+  const bool pool = !SPARSE && !SPLIT && a.gt != nullptr;  // ground-truth mode
   const int64_t trow = ((int64_t)t.b * a.heads_q + t.h) * a.n_blocks + t.i;
   float* const rrow = pool ? a.pool_r + trow * a.n_blocks * 64 : nullptr;
   auto fetch_chunk = [&](int base) {  // entries [base, base + kListChunk) of the row list
@@ -345,7 +411,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   };
   auto entry = [&](int p) -> int {  // p must lie in the current LDS window
     if (p >= list.n) return -1;
-    const int jj = SPARSE ? (int)sList[p % kListChunk] : p;
+    const int jj = SPARSE ? (int)sList[p % kListChunk] : list.lo + p;
     return list.ok(jj) ? jj : -1;
   };
   fetch_chunk(0);
@@ -528,15 +594,28 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
       *reinterpret_cast<bf16x4*>(sO + ql * Lay::OSTR + 32 * dt + 8 * jj + 4 * hf) = o4;
     }
   __syncthreads();
-  uint16_t* op = static_cast<uint16_t*>(a.o) + t.b * a.osb + t.h * a.osh;
+  // destination: the output rows of the query block, or the task's partial slot
+  int64_t slot = 0;
+  uint16_t* op;
+  int64_t ors;
+  if (SPLIT) {
+    slot = ((int64_t)t.b * a.heads_q + t.h) * a.split_slots + split_offset(t.i, a.split_w) + t.p;
+    op = a.part_o + slot * 64 * D;
+    ors = D;
+  } else {
+    op = static_cast<uint16_t*>(a.o) + t.b * a.osb + t.h * a.osh + (int64_t)64 * t.i * a.oss;
+    ors = a.oss;
+  }
 #pragma unroll
   for (int e = 0; e < 64 * Lay::CPR / 128; ++e) {
     const int q = tid + 128 * e;
     const int r = q / Lay::CPR, cc = q % Lay::CPR;
-    *reinterpret_cast<u32x4*>(op + (int64_t)(64 * t.i + r) * a.oss + 8 * cc) =
+    *reinterpret_cast<u32x4*>(op + (int64_t)r * ors + 8 * cc) =
         *reinterpret_cast<const u32x4*>(sO + r * Lay::OSTR + 8 * cc);
   }
-  if (a.lse && hf == 0) {
+  if (SPLIT) {
+    if (hf == 0) a.part_lse[slot * 64 + ql] = (l_tot > 0.f) ? m_run * c + __log2f(l_tot) : -INFINITY;
+  } else if (a.lse && hf == 0) {
     const float lse = (l_tot > 0.f) ? m_run * a.scale + __logf(l_tot) : -INFINITY;
     a.lse[((int64_t)t.b * a.heads_q + t.h) * (int64_t)a.n_blocks * 64 + qrow] = lse;
   }
@@ -684,6 +763,103 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
   }
 }
 
+// ---------------------------------------------------------------------------
+// key-range split: list bounds and the merge of partial results
+// ---------------------------------------------------------------------------
+
+// One wavefront per sparse row: bounds[p] = number of valid list entries
+// (j <= i when causal, j < nb) in key blocks below p w, for p = 0..P.
+// Lists are ascending, so range p holds entries [bounds[p], bounds[p + 1]).
+__global__ __launch_bounds__(256) void split_bounds_kernel(AttnArgs a) {
+  const int wave = threadIdx.x / 64;
+  const int lane = threadIdx.x % 64;
+  const int64_t rows = (int64_t)a.batch * a.heads_q * a.n_blocks;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wave;
+  if (row >= rows) return;
+  const int nb = a.n_blocks;
+  const int i = (int)(row % nb);
+  const int w = a.split_w;
+  const int n = min(max(a.count[row], 0), nb);
+  const uint16_t* L = a.idx + row * nb;
+  const int P = a.split_parts;
+  int cnt[kMaxSplitParts];
+#pragma unroll
+  for (int p = 0; p < kMaxSplitParts; ++p) cnt[p] = 0;
+  for (int e = lane; e < n; e += 64) {
+    const int j = L[e];
+    if (j < nb && (!a.causal || j <= i)) {
+      const int pj = j / w;
+#pragma unroll
+      for (int p = 0; p < kMaxSplitParts; ++p) cnt[p] += (pj == p) ? 1 : 0;
+    }
+  }
+  int run = 0;
+  int32_t* out = a.split_bounds + row * (P + 1);
+#pragma unroll
+  for (int p = 0; p < kMaxSplitParts; ++p) {
+    if (p == P) break;
+    int c = cnt[p];
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off);
+    if (lane == p) out[p] = run;
+    run += c;
+  }
+  if (lane == P) out[P] = run;
+}
+
+// One workgroup per (batch, head, query block): combines the row's partial
+// outputs O_p (normalised within range p) with weights 2^(lse_p - lse), where
+// lse = log2 sum_p 2^lse_p, writes O (bf16, round to nearest even) and the
+// natural-log LSE.  Thread t handles query t / 4 and a quarter of its features.
+template <int D>
+__global__ __launch_bounds__(256) void split_merge_kernel(AttnArgs a) {
+  constexpr int F = D / 4;  // features per thread
+  const int64_t row = blockIdx.x;
+  const int nb = a.n_blocks;
+  const int i = (int)(row % nb);
+  const int64_t bh = row / nb;
+  const int b = (int)(bh / a.heads_q), h = (int)(bh % a.heads_q);
+  const int w = a.split_w;
+  const int nparts = min(a.split_parts, i / w + 1);
+  const int64_t slot0 = bh * a.split_slots + split_offset(i, w);
+  const int q = threadIdx.x / 4, f0 = (threadIdx.x % 4) * F;
+  float mx = -INFINITY;
+  for (int p = 0; p < nparts; ++p) mx = fmaxf(mx, a.part_lse[(slot0 + p) * 64 + q]);
+  float acc[F];
+#pragma unroll
+  for (int f = 0; f < F; ++f) acc[f] = 0.f;
+  float sum = 0.f;
+  if (mx > -INFINITY) {
+    for (int p = 0; p < nparts; ++p) {
+      const float lp = a.part_lse[(slot0 + p) * 64 + q];
+      if (lp == -INFINITY) continue;
+      const float wgt = __builtin_amdgcn_exp2f(lp - mx);
+      sum += wgt;
+      const u32x4* src = reinterpret_cast<const u32x4*>(a.part_o + ((slot0 + p) * 64 + q) * D + f0);
+#pragma unroll
+      for (int u = 0; u < F / 8; ++u) {
+        const u32x4 v = src[u];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[8 * u + 2 * e] = fmaf(wgt, __uint_as_float(v[e] << 16), acc[8 * u + 2 * e]);
+          acc[8 * u + 2 * e + 1] = fmaf(wgt, __uint_as_float(v[e] & 0xFFFF0000u), acc[8 * u + 2 * e + 1]);
+        }
+      }
+    }
+  }
+  const float inv = sum > 0.f ? 1.0f / sum : 0.f;
+  uint16_t* dst = static_cast<uint16_t*>(a.o) + b * a.osb + h * a.osh + (int64_t)(64 * i + q) * a.oss + f0;
+#pragma unroll
+  for (int u = 0; u < F / 8; ++u) {
+    bf16x8 o8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o8[e] = (__bf16)(acc[8 * u + e] * inv);
+    *reinterpret_cast<bf16x8*>(dst + 8 * u) = o8;
+  }
+  if (a.lse && threadIdx.x % 4 == 0)
+    a.lse[bh * nb * 64 + 64 * i + q] = sum > 0.f ? (mx + __log2f(sum)) * 0.6931471805599453f : -INFINITY;
+}
+
 // Groups per phase: the largest power of two whose K + V stay within 64 MiB
 // (a quarter of the 256 MB Infinity Cache); each group is then spread over
 // R = 8 / gpp XCDs.  Measured at 131072 tokens (64 MiB of K + V per group):
@@ -719,10 +895,52 @@ static TaskMap make_map(const AttnArgs& a) {
 
 }  // namespace
 
+// Ranges narrower than this many key blocks are not worth a split: per-task
+// set-up and the partial traffic outweigh the L2 gain.  The environment
+// variable SEER_SPLIT_MIN_WIDTH (read on the host at each call) overrides it.
+constexpr int kSplitMinWidth = 32;
+
+// Sparse rows prefer 8 ranges (fewer tasks and partials; measured faster at
+// 131072 tokens), which needs an even number of KV groups; dense rows and odd
+// group counts use 16.
+int split_parts(int n_blocks, int kv_groups, bool causal, bool bf16, bool sparse) {
+  if (!causal || !bf16) return 0;
+  int min_w = kSplitMinWidth;
+  if (const char* e = getenv("SEER_SPLIT_MIN_WIDTH")) {
+    const int v = atoi(e);
+    if (v >= 1) min_w = v;
+  }
+  const int cand[2] = {sparse && kv_groups % 2 == 0 ? 8 : 16, 16};
+  for (int P : cand)
+    if (n_blocks % P == 0 && n_blocks / P >= min_w) return P;
+  return 0;
+}
+
+int64_t split_slots_per_head(int n_blocks, int w) {
+  const int64_t q = n_blocks / w, r = n_blocks % w;
+  return n_blocks + w * q * (q - 1) / 2 + r * q;
+}
+
+template <int D>
+static void launch_split(const KernelArgs& ka, bool sparse, hipStream_t s) {
+  const AttnArgs& a = ka.a;
+  const int64_t rows = (int64_t)a.batch * a.heads_q * a.n_blocks;
+  if (sparse)
+    hipLaunchKernelGGL(split_bounds_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, a);
+  // per XCD and group (P = 16) or pair of groups (P = 8): G (2 nb - (P - 1) w) tasks
+  const int64_t units = a.split_parts == 16 ? (int64_t)a.batch * a.heads_kv : (int64_t)a.batch * a.heads_kv / 2;
+  const int64_t tasks = 8 * units * (a.heads_q / a.heads_kv) * (2 * a.n_blocks - (a.split_parts - 1) * a.split_w);
+  dim3 grid((unsigned)tasks), block(128);
+  if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, true, true>), grid, block, 0, s, ka);
+  else hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, false, true>), grid, block, 0, s, ka);
+  hipLaunchKernelGGL(split_merge_kernel<D>, dim3((unsigned)rows), dim3(256), 0, s, a);
+}
+
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   KernelArgs ka;
   ka.a = a;
   ka.map = make_map(a);
+  ka.split = SplitMap{a.heads_q, a.heads_kv, a.n_blocks, a.split_w, a.split_parts};
   ka.scale_log2 = a.scale * kLog2e;
   const int64_t total = (int64_t)a.batch * a.heads_q * a.n_blocks;
   if (total == 0) return hipSuccess;
@@ -730,13 +948,25 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   const bool sparse = a.count != nullptr;
   const bool pool = a.gt != nullptr;
   if ((sparse && pool) || (pool && !a.pool_r)) return hipErrorInvalidValue;
+  if (a.split_w > 0) {
+    // the shape must be the one split_width accepted, with every buffer present
+    const int P = a.split_parts;
+    if (pool || !a.bf16 || !a.causal || (P != 8 && P != 16) || a.split_w * P != a.n_blocks ||
+        (P == 8 && (a.batch * a.heads_kv) % 2 != 0) || !a.part_lse || !a.part_o ||
+        (sparse && !a.split_bounds) || a.split_slots != split_slots_per_head(a.n_blocks, a.split_w))
+      return hipErrorInvalidValue;
+    if (a.head_dim == 128) launch_split<128>(ka, sparse, s);
+    else if (a.head_dim == 64) launch_split<64>(ka, sparse, s);
+    else return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   if (a.bf16) {
     if (a.head_dim == 128) {
-      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true>), grid, block, 0, s, ka);
-      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false>), grid, block, 0, s, ka);
+      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true, false>), grid, block, 0, s, ka);
+      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false, false>), grid, block, 0, s, ka);
     } else if (a.head_dim == 64) {
-      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true>), grid, block, 0, s, ka);
-      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false>), grid, block, 0, s, ka);
+      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true, false>), grid, block, 0, s, ka);
+      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false, false>), grid, block, 0, s, ka);
     } else {
       return hipErrorInvalidValue;
     }

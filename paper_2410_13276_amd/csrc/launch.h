@@ -71,7 +71,18 @@ struct AttnArgs {
   // 2D max-pooled probability map [B][Hq][nb][nb]; both nullptr otherwise
   float* pool_r;
   float* gt;
+  // key-range split (causal, bf16): each row is cut into split_parts key ranges of
+  // split_w blocks, computed as separate tasks into partial slots and merged
+  // afterwards; split_w == 0 disables it
+  int split_parts;              // 8 or 16
+  int split_w;
+  int64_t split_slots;          // partial slots per (batch, head)
+  int32_t* split_bounds;        // sparse: [rows][split_parts + 1] list offsets of the ranges
+  float* part_lse;              // [slots][64] log2-domain log-sum-exp of each partial
+  uint16_t* part_o;             // [slots][64][D] bf16 partial outputs, normalised
 };
+
+constexpr int kMaxSplitParts = 16;
 
 // Gate distillation (Eq. 2): row-wise KL between the renormalised ground truth
 // and the gate softmax, and the logit gradient written over the logits.
@@ -113,5 +124,9 @@ hipError_t launch_gate_logits(const GateLogitsArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_mask_from_dense(const MaskFromDenseArgs& a, hipStream_t s);
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
+// Split geometry: the number of key ranges for a launch (0 when the shape does
+// not split) and the partial slots per (batch, head) for a range width.
+int split_parts(int n_blocks, int kv_groups, bool causal, bool bf16, bool sparse);
+int64_t split_slots_per_head(int n_blocks, int w);
 
 }  // namespace seer

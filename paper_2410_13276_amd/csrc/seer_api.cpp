@@ -155,7 +155,41 @@ seer::AttnArgs attn_args(const seer_attn_desc* desc, int32_t causal, float sm_sc
   a.idx = nullptr;
   a.pool_r = nullptr;
   a.gt = nullptr;
+  a.split_parts = 0;
+  a.split_w = 0;
+  a.split_slots = 0;
+  a.split_bounds = nullptr;
+  a.part_lse = nullptr;
+  a.part_o = nullptr;
   return a;
+}
+
+// Workspace of the key-range split: list bounds [rows][P + 1] int32, then the
+// partial log-sum-exps [slots][64] fp32 and outputs [slots][64][D] bf16.
+struct SplitLayout {
+  int parts, w;
+  int64_t slots;  // per (batch, head)
+  size_t bounds, lse, o, total;
+};
+
+SplitLayout split_layout(const seer_attn_desc* d, int parts) {
+  SplitLayout L{};
+  const int nb = d->seq_len / SEER_BLOCK;
+  if (parts == 0) return L;
+  L.parts = parts;
+  L.w = nb / parts;
+  L.slots = seer::split_slots_per_head(nb, L.w);
+  const size_t bh = (size_t)d->batch * d->heads_q;
+  L.bounds = 0;
+  L.lse = round_up(bh * nb * (parts + 1) * sizeof(int32_t));
+  L.o = L.lse + round_up(bh * L.slots * 64 * sizeof(float));
+  L.total = L.o + round_up(bh * L.slots * 64 * d->head_dim * sizeof(uint16_t));
+  return L;
+}
+
+int split_parts_for(const seer_attn_desc* d, int32_t causal, bool sparse) {
+  return seer::split_parts(d->seq_len / SEER_BLOCK, d->batch * d->heads_kv, causal != 0,
+                           d->dtype == SEER_BF16, sparse);
 }
 
 // Bytes of row-max workspace per query head: nb key tiles x 64 queries per query block.
@@ -269,7 +303,8 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
 
 static seer_status attn_common(const seer_attn_desc* desc, const seer_block_mask* mask,
                                int32_t causal, float sm_scale, const void* q, const void* k,
-                               const void* v, void* o, float* lse, void* stream) {
+                               const void* v, void* o, float* lse, void* workspace,
+                               size_t workspace_bytes, void* stream) {
   seer_status s = check_attn(desc, sm_scale, q, k, v, o);
   if (s != SEER_OK) return s;
   const int nb = desc->seq_len / SEER_BLOCK;
@@ -280,6 +315,19 @@ static seer_status attn_common(const seer_attn_desc* desc, const seer_block_mask
   seer::AttnArgs a = attn_args(desc, causal, sm_scale, q, k, v, o, lse);
   a.count = mask ? mask->count : nullptr;
   a.idx = mask ? mask->idx : nullptr;
+  if (workspace) {
+    if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
+    const SplitLayout L = split_layout(desc, split_parts_for(desc, causal, mask != nullptr));
+    if (L.w > 0 && workspace_bytes >= L.total) {  // key-range split
+      char* ws = static_cast<char*>(workspace);
+      a.split_parts = L.parts;
+      a.split_w = L.w;
+      a.split_slots = L.slots;
+      a.split_bounds = reinterpret_cast<int32_t*>(ws + L.bounds);
+      a.part_lse = reinterpret_cast<float*>(ws + L.lse);
+      a.part_o = reinterpret_cast<uint16_t*>(ws + L.o);
+    }
+  }
   return from_hip(seer::launch_attn(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -288,13 +336,35 @@ seer_status seer_bsattn(const seer_attn_desc* desc, int32_t block, const seer_bl
                         const void* v, void* o, float* lse, void* stream) {
   if (block != SEER_BLOCK) return desc ? SEER_ERR_UNSUPPORTED : SEER_ERR_INVALID_ARG;
   if (!mask) return SEER_ERR_INVALID_ARG;
-  return attn_common(desc, mask, causal, sm_scale, q, k, v, o, lse, stream);
+  return attn_common(desc, mask, causal, sm_scale, q, k, v, o, lse, nullptr, 0, stream);
 }
 
 seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm_scale,
                             const void* q, const void* k, const void* v, void* o, float* lse,
                             void* stream) {
-  return attn_common(desc, nullptr, causal, sm_scale, q, k, v, o, lse, stream);
+  return attn_common(desc, nullptr, causal, sm_scale, q, k, v, o, lse, nullptr, 0, stream);
+}
+
+size_t seer_attn_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t causal) {
+  if (block != SEER_BLOCK || check_desc(desc, 0xF) != SEER_OK) return 0;
+  // enough for the sparse and the dense choice of ranges
+  return std::max(split_layout(desc, split_parts_for(desc, causal, true)).total,
+                  split_layout(desc, split_parts_for(desc, causal, false)).total);
+}
+
+seer_status seer_bsattn_ws(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
+                           int32_t causal, float sm_scale, const void* q, const void* k, const void* v,
+                           void* o, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  if (block != SEER_BLOCK) return desc ? SEER_ERR_UNSUPPORTED : SEER_ERR_INVALID_ARG;
+  if (!mask) return SEER_ERR_INVALID_ARG;
+  return attn_common(desc, mask, causal, sm_scale, q, k, v, o, lse, workspace, workspace_bytes, stream);
+}
+
+seer_status seer_dense_attn_ws(const seer_attn_desc* desc, int32_t causal, float sm_scale,
+                               const void* q, const void* k, const void* v, void* o, float* lse,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  return attn_common(desc, nullptr, causal, sm_scale, q, k, v, o, lse, workspace, workspace_bytes,
+                     stream);
 }
 
 seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, const uint8_t* dense,

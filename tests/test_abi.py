@@ -24,7 +24,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 12, names
+    assert len(names) == 15, names
     L = C.CDLL(seer.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -187,3 +187,38 @@ def test_gate_distill_workspace_and_rejects_bad_args():
     assert call(ws=FAKE * 16 + 16) == seer.ERR_INVALID_ARG
     assert call(gd=_gate(gate_dim=48)) == seer.ERR_UNSUPPORTED
     assert call(gd=_gate(rope_theta=-2.0)) == seer.ERR_INVALID_ARG
+
+
+def test_attn_workspace_bytes_formula(monkeypatch):
+    L = seer.lib()
+    monkeypatch.delenv("SEER_SPLIT_MIN_WIDTH", raising=False)
+    up = lambda x: (x + 255) // 256 * 256
+    d = _desc(B=1, Hq=32, Hkv=8, S=131072, D=128)
+    nb, w = 2048, 128
+    slots = sum(i // w + 1 for i in range(nb))
+    want = up(32 * nb * 17 * 4) + up(32 * slots * 64 * 4) + up(32 * slots * 64 * 128 * 2)
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == want
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 0) == 0      # non-causal: no split
+    d.dtype = 1
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == 0      # fp32: no split
+    d = _desc(B=1, Hq=4, Hkv=2, S=1024, D=128)                       # nb / 16 = 1 < 32
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == 0
+    monkeypatch.setenv("SEER_SPLIT_MIN_WIDTH", "1")
+    slots = sum(i + 1 for i in range(16))
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == \
+        up(4 * 16 * 17 * 4) + up(4 * slots * 64 * 4) + up(4 * slots * 64 * 128 * 2)
+    d = _desc(B=1, Hq=4, Hkv=2, S=1088, D=128)                       # nb = 17: not a multiple of 16
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == 0
+
+
+def test_attention_ws_rejects_bad_args():
+    L = seer.lib()
+    d = _desc()
+    m = seer.BlockMaskStruct()
+    m.n_blocks, m.count, m.idx, m.dense = 16, FAKE, FAKE, None
+    args = (FAKE, FAKE, FAKE, FAKE, None)
+    assert L.seer_bsattn_ws(C.byref(d), 64, None, 1, 0.0, *args, FAKE * 16, 1 << 30, None) == seer.ERR_INVALID_ARG
+    assert L.seer_bsattn_ws(C.byref(d), 64, C.byref(m), 1, 0.0, *args, FAKE * 16 + 8, 1 << 30, None) == \
+        seer.ERR_INVALID_ARG                                               # misaligned workspace
+    assert L.seer_dense_attn_ws(C.byref(d), 1, float("inf"), *args, FAKE * 16, 1 << 30, None) == \
+        seer.ERR_INVALID_ARG

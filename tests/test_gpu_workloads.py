@@ -1,5 +1,6 @@
 """GPU parity at the full sizes of the five workloads, in the launch
-configuration bench.py times (whole tensors, one gate call, one attention call).
+configuration bench.py times (whole tensors, one gate call, one attention call
+with the key-range split workspace wherever the shape splits).
 
 Masks are compared in full against the oracle's fp64 gate (mismatches allowed
 only within 1e-4 of the selection cut in log-score, TopK rows exactly k).
@@ -48,10 +49,13 @@ def test_workload_full_size(name):
     wq, wk = W.make_weights(w)
     gkw, okw = _gate_kwargs(w)
 
-    # device path, exactly as bench.py runs it
+    # device path, exactly as bench.py runs it (with the key-range split workspace)
     qd, kd, vd = to_device(q), to_device(k), to_device(v)
+    nws = seer.attn_workspace_bytes(qd, kd, vd)
+    aws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda") if nws else None
+    print(f"[workload] {name}: split workspace {nws} bytes", flush=True)
     mask = seer.gate(qd, kd, torch.from_numpy(wq).cuda(), torch.from_numpy(wk).cuda(), **gkw)
-    o_e2e, _ = seer.bsattn(qd, kd, vd, mask)
+    o_e2e, _ = seer.bsattn(qd, kd, vd, mask, workspace=aws)
     torch.cuda.synchronize()
     count, idx, dense = gpu_mask_numpy(mask)
     o_e2e = from_device(o_e2e)
@@ -72,7 +76,7 @@ def test_workload_full_size(name):
     tol = ATOL_F32 if w.dtype == "f32" else ATOL_BF16
 
     # block-sparse kernel on the oracle's mask
-    o_sp, lse = seer.bsattn(qd, kd, vd, upload_mask(sel["count"], sel["idx"]), want_lse=True)
+    o_sp, lse = seer.bsattn(qd, kd, vd, upload_mask(sel["count"], sel["idx"]), want_lse=True, workspace=aws)
     torch.cuda.synchronize()
     O_ref, lse_ref = oracle.attn(q, k, v, mask=sel["mask"], rows=rows)
     err = float(np.abs(as_f64(gather_rows(from_device(o_sp), rows)) - O_ref).max())
@@ -94,7 +98,7 @@ def test_workload_full_size(name):
 
     # the dense comparison kernel at the headline size
     if name == W.HEADLINE:
-        od, _ = seer.dense_attn(qd, kd, vd)
+        od, _ = seer.dense_attn(qd, kd, vd, workspace=aws)
         torch.cuda.synchronize()
         drows = rows[:: max(1, len(rows) // 12)]
         O_ref3, _ = oracle.attn(q, k, v, rows=drows)
