@@ -109,7 +109,7 @@ def main() -> int:
     ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
     ap.add_argument("--dense-runs", type=int, default=3)
     ap.add_argument("--gt-runs", type=int, default=2, help="timed runs of the ground-truth kernel (0: skip)")
-    ap.add_argument("--cpu-rows", type=int, default=1024, help="oracle sample size (q-block rows)")
+    ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample size (q-block rows)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device-to-device copy three times (the known-size "
