@@ -247,8 +247,13 @@ __device__ __forceinline__ void pool_epilogue(const float* __restrict__ rrow, co
 //  - K chunk c of row r sits at chunk c ^ fk(r): the S^T operand read (16
 //    lanes = 16 consecutive rows, one chunk each) hits 16 distinct bank groups.
 //  - V chunk c of row r sits at chunk c ^ fv(r): the V^T operand is read with
-//    ds_read_b64_tr_b16, where 16 lanes read 8 bytes each from 4 consecutive
-//    rows x 32 bytes; fv moves those 4 row segments onto distinct banks.
+//    ds_read_b64_tr_b16, whose 8-byte reads are served 32 lanes per pass: 4
+//    consecutive rows x 64 bytes (four 16-byte chunks, 4k .. 4k + 3, of each
+//    row).  fv XORs the chunk index with a multiple of 4 that differs for the
+//    4 rows (or, at D = 64, for the two 256-byte lines they span), so the pass
+//    covers 16 distinct chunk positions = all 64 banks once.  (A 2-way
+//    conflict remained with an XOR by 2 (r % 4), which only separates rows
+//    within a 16-lane group.)
 //
 // ds_read_b64_tr_b16 semantics (within each group of 16 lanes): view the 16
 // lanes' 8-byte reads as a 16 x 4 matrix C of 16-bit values; lane 4a + b
@@ -266,7 +271,7 @@ struct Bf16Layout {
   static constexpr int OSTR = D + 8;          // output staging row
   static_assert(64 * OSTR <= 2 * TILE, "output staging must fit");
   __device__ static int fk(int r) { return (r / RP) & (CPR - 1); }
-  __device__ static int fv(int r) { return 2 * ((r / RP) & 3); }
+  __device__ static int fv(int r) { return 4 * ((r / RP) & (CPR / 4 - 1)); }
 };
 
 // One 16-byte direct global->LDS load per lane (global_load_lds_dwordx4): lane
