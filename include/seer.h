@@ -183,7 +183,10 @@ seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm
  * those calls need no workspace).  The split applies to causal bf16 attention
  * with nb a multiple of 16 and nb / 16 >= the minimum range width (32 blocks;
  * the environment variable SEER_SPLIT_MIN_WIDTH, read at each call, overrides
- * it).  Size: 68 bytes per query block plus (256 + 128 head_dim) bytes per
+ * it).  Dense calls split whenever the shape allows; sparse calls only when
+ * the environment variable SEER_SPLIT_SPARSE is 1 (at 10% density the
+ * unsplit sparse kernel measured as fast), then with 8 ranges when
+ * batch * heads_kv is even, else 16.  Size: 68 bytes per query block plus (256 + 128 head_dim) bytes per
  * partial slot; a query head has sum over i of (floor(i / (nb / 16)) + 1),
  * about 8.5 nb, slots (9.3 GB for 32 heads of 131072 tokens, head_dim 128).
  */

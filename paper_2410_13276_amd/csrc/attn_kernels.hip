@@ -414,10 +414,14 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
         if (base + p < list.n) sList[p] = list.idx[base + p];
     }
   };
+  // last valid key block: j <= i when causal, j < nb always (i < nb); a dense
+  // list is valid by construction
+  const int jmax = a.causal ? t.i : a.n_blocks - 1;
   auto entry = [&](int p) -> int {  // p must lie in the current LDS window
     if (p >= list.n) return -1;
-    const int jj = SPARSE ? (int)sList[p % kListChunk] : list.lo + p;
-    return list.ok(jj) ? jj : -1;
+    if (!SPARSE) return list.lo + p;
+    const int jj = (int)sList[p % kListChunk];
+    return jj <= jmax ? jj : -1;
   };
   fetch_chunk(0);
   __syncthreads();
@@ -434,13 +438,14 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) sn[mt][e] = 0.f;
+    // the two 32-key halves alternate, so consecutive MFMAs are independent
     bf16x8 kf[NS];
 #pragma unroll
     for (int st = 0; st < NS; ++st)
-      kf[st] = *reinterpret_cast<const bf16x8*>(sK + 32 * (st / (D / 16)) * D + koff[st % (D / 16)]);
+      kf[st] = *reinterpret_cast<const bf16x8*>(sK + 32 * (st % 2) * D + koff[st / 2]);
 #pragma unroll
     for (int st = 0; st < NS; ++st) {
-      const int mt = st / (D / 16), ks = st % (D / 16);
+      const int mt = st % 2, ks = st / 2;
       sn[mt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[st], qf[ks], sn[mt], 0, 0, 0);
     }
   };
@@ -485,11 +490,12 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
         }
     }
     // online softmax (lazy rescale)
-    float mloc = -INFINITY;
+    float mx2[2] = {-INFINITY, -INFINITY};  // two independent max chains
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) mloc = fmaxf(mloc, sc[mt][e]);
+      for (int e = 0; e < 16; ++e) mx2[mt] = fmaxf(mx2[mt], sc[mt][e]);
+    float mloc = fmaxf(mx2[0], mx2[1]);
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
     if (__ballot((mloc - m_run) * c > 8.0f)) {
       const float m_new = fmaxf(m_run, mloc);
@@ -508,14 +514,16 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     // P^T operand of k-step kt: accumulators 8(kt%2)..+7 of half kt/2, i.e. keys
     // 32(kt/2) + 16(kt%2) + {4hf + 0..3, 8 + 4hf + 0..3}
     bf16x8 pb[4];
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};  // four independent partial sums
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float p = __builtin_amdgcn_exp2f(fmaf(sc[kt / 2][8 * (kt % 2) + e], c, -mc));
-        l_run += p;
+        ps[kt] += p;
         pb[kt][e] = (__bf16)p;
       }
+    l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
     // schedule: four K reads ahead, then each MFMA of the next tile's S with
     // seven VALU instructions of this tile's softmax
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
@@ -535,13 +543,18 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     asm volatile("" ::"v"(pb[0]), "v"(pb[1]), "v"(pb[2]), "v"(pb[3]), "v"(l_run), "v"(sn[0]), "v"(sn[1]));
     wait_loads();
     __syncthreads();  // M: V_j visible, K_jn consumed
+    // the P.V product runs at raised wave priority: of the two wavefronts sharing
+    // a SIMD, the one feeding the matrix core issues first (measured: sparse
+    // 128k 19.8 -> 18.3 ms, dense split -1%)
+    __builtin_amdgcn_s_setprio(2);
     if (jnn >= 0) load_tile_lds<D>(sK_a, kp + jnn * ktile, kss, wave_u, koffd);
     // ground truth: this tile's row max (Eq. 5), completed with the K load by barrier E
     if (pool && hf == 0) rrow[(int64_t)j * 64 + 32 * wave + col] = mloc;
 
     // O^T += V^T P^T; V^T operand: feature 32dt + col, the same keys as pb[kt]
+    // feature tiles dt alternate, so consecutive MFMAs are independent
     auto vread = [&](int st) -> bf16x8 {
-      const int dt = st / 4, kt = st % 4;
+      const int dt = st % (D / 32), kt = st / (D / 32);
       const int rows = 32 * (kt / 2) + 16 * (kt % 2);
       const uint16_t* base = sV + rows * D + voff[dt];
       const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)base);
@@ -555,7 +568,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     for (int st = 0; st < NV; ++st) {
       bf16x8 vf2;
       if (st + 2 < NV) vf2 = vread(st + 2);
-      acc[st / 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf0, pb[st % 4], acc[st / 4], 0, 0, 0);
+      acc[st % (D / 32)] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf0, pb[st / (D / 32)], acc[st % (D / 32)], 0, 0, 0);
       vf0 = vf1;
       vf1 = vf2;
     }
@@ -568,6 +581,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     wait_loads();
+    __builtin_amdgcn_s_setprio(0);
     __syncthreads();  // E: V_j consumed, K_jnn visible
     if (jn >= 0) load_tile_lds<D>(sV_a, vp + jn * vtile, vss, wave_u, voffd);
     j = jn;
@@ -905,11 +919,18 @@ static TaskMap make_map(const AttnArgs& a) {
 // variable SEER_SPLIT_MIN_WIDTH (read on the host at each call) overrides it.
 constexpr int kSplitMinWidth = 32;
 
-// Sparse rows prefer 8 ranges (fewer tasks and partials; measured faster at
-// 131072 tokens), which needs an even number of KV groups; dense rows and odd
-// group counts use 16.
+// Dense rows use 16 ranges.  Sparse rows are not split unless the environment
+// variable SEER_SPLIT_SPARSE=1 asks for it: at 131072 tokens and 10% density
+// the unsplit sparse kernel (18.3 ms) matched 8 ranges (18.7 ms incl. the
+// merge) and beat 16 (20.0 ms), the short tasks' set-up and the partial traffic
+// eating the L2 gain.  When enabled, sparse rows take 8 ranges if the number
+// of KV groups is even (fewer tasks and partials), else 16.
 int split_parts(int n_blocks, int kv_groups, bool causal, bool bf16, bool sparse) {
   if (!causal || !bf16) return 0;
+  if (sparse) {
+    const char* e = getenv("SEER_SPLIT_SPARSE");
+    if (!e || atoi(e) != 1) return 0;
+  }
   int min_w = kSplitMinWidth;
   if (const char* e = getenv("SEER_SPLIT_MIN_WIDTH")) {
     const int v = atoi(e);

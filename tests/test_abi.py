@@ -192,6 +192,7 @@ def test_gate_distill_workspace_and_rejects_bad_args():
 def test_attn_workspace_bytes_formula(monkeypatch):
     L = seer.lib()
     monkeypatch.delenv("SEER_SPLIT_MIN_WIDTH", raising=False)
+    monkeypatch.delenv("SEER_SPLIT_SPARSE", raising=False)
     up = lambda x: (x + 255) // 256 * 256
     d = _desc(B=1, Hq=32, Hkv=8, S=131072, D=128)
     nb, w = 2048, 128

@@ -1,9 +1,10 @@
 """GPU parity of the key-range split (seer_bsattn_ws / seer_dense_attn_ws): rows
 cut into 8 or 16 key ranges computed as separate tasks, bf16 partials merged.
 
-The split normally starts at 32 key blocks per range; these tests lower that
-limit through SEER_SPLIT_MIN_WIDTH so that small shapes (1 to 4 blocks per
-range, both range counts, ragged GQA layouts) exercise it.  Bars as for the
+The split normally starts at 32 key blocks per range and applies to sparse
+rows only on request; these tests set SEER_SPLIT_MIN_WIDTH=1 and
+SEER_SPLIT_SPARSE=1 so that small shapes (1 to 4 blocks per range, both range
+counts, ragged GQA layouts) exercise it.  Bars as for the
 unsplit kernel (max-abs 2e-2 against the fp64 oracle, LSE 1e-3, empty rows
 O = 0 and LSE = -inf); the split result also stays within 1e-2 of the unsplit
 one (the partials' bf16 rounding) and is bitwise reproducible."""
@@ -33,6 +34,7 @@ CASES = [
 @pytest.fixture(autouse=True)
 def _small_ranges(monkeypatch):
     monkeypatch.setenv("SEER_SPLIT_MIN_WIDTH", "1")
+    monkeypatch.setenv("SEER_SPLIT_SPARSE", "1")   # sparse rows split only on request
 
 
 def _ws(qd, kd, vd):
@@ -110,3 +112,19 @@ def test_split_small_workspace_and_noncausal_fall_back_to_unsplit():
     torch.cuda.synchronize()
     assert torch.equal(o_small.view(torch.int16), o_plain.view(torch.int16))
     assert torch.equal(o_nc.view(torch.int16), o_nc0.view(torch.int16))
+
+
+def test_sparse_split_is_opt_in(monkeypatch):
+    """Without SEER_SPLIT_SPARSE the sparse call with a workspace is the unsplit one."""
+    monkeypatch.delenv("SEER_SPLIT_SPARSE")
+    B, Hq, Hkv, S, D = 1, 4, 2, 2048, 128
+    w, q, k, v, wq, wk = small_inputs(B, Hq, Hkv, S, D, "bf16", seed=stable_seed("splitoptin"))
+    qd, kd, vd = (to_device(x) for x in (q, k, v))
+    orc = oracle_gate(q, k, wq, wk, oracle.TOPK_RATIO, rho=0.3)
+    m = upload_mask(orc["count"], orc["idx"])
+    n, ws = _ws(qd, kd, vd)
+    assert n > 0  # the dense call still splits at this shape
+    o_ws, _ = seer.bsattn(qd, kd, vd, m, workspace=ws)
+    o_plain, _ = seer.bsattn(qd, kd, vd, m)
+    torch.cuda.synchronize()
+    assert torch.equal(o_ws.view(torch.int16), o_plain.view(torch.int16))
