@@ -50,7 +50,8 @@ extern "C" {
 #endif
 
 #define SEER_ABI_VERSION 1
-#define SEER_BLOCK 64 /* the paper fixes the gate / sparse-kernel block at 64 (section 4) */
+#define SEER_BLOCK 64 /* the attention tile edge and the default gate block (section 4); gate
+                        blocks and masks of 128 tokens are the other size the paper names */
 
 typedef enum {
   SEER_OK = 0,
@@ -84,7 +85,8 @@ typedef struct {
 
 /* AttnGate parameters (section 3.1, Eq. 1; selection per Eq. 3 / Eq. 4). */
 typedef struct {
-  int32_t block;       /* pooling kernel = stride = sparse tile; must be SEER_BLOCK */
+  int32_t block;       /* pooling kernel = stride = mask block: 64 or 128 tokens (the paper's
+                          sparse kernel takes "64 or 128", section 3.3); seq_len % block == 0 */
   int32_t gate_dim;    /* Dg, output width of the gate linear layers: 32, 64 or 128 */
   int32_t w_per_head;  /* 1: wq [heads_q][D][Dg], wk [heads_kv][3D][Dg];
                           0: one wq [D][Dg] and one wk [3D][Dg] shared by all heads */
@@ -105,7 +107,7 @@ typedef struct {
 /* Block mask in compacted form: for row r = (b, h, i), idx[r][0 .. count[r]-1]
  * are the active key blocks j in strictly ascending order.  Caller-owned. */
 typedef struct {
-  int32_t n_blocks;  /* nb = seq_len / SEER_BLOCK */
+  int32_t n_blocks;  /* nb = seq_len / block (64 or 128) */
   int32_t* count;    /* device [batch][heads_q][nb] */
   uint16_t* idx;     /* device [batch][heads_q][nb][nb] */
   uint8_t* dense;    /* optional device [batch][heads_q][nb][nb] 0/1 copy, or NULL */
@@ -144,8 +146,8 @@ size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block);
  * (entries above the diagonal unspecified); when NULL, L lives in the workspace.
  * workspace: device memory of at least seer_gate_workspace_bytes(desc, gate,
  * logits_out == NULL) bytes, 256-byte aligned.
- * Unsupported: gate->block != 64, head_dim not in {64, 128}, gate_dim not in
- * {32, 64, 128}, nb > 4096.
+ * Unsupported: gate->block not in {64, 128} or not dividing seq_len, head_dim
+ * not in {64, 128}, gate_dim not in {32, 64, 128}, nb > 4096.
  */
 seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate,
                       const void* q, const void* k, const float* wq, const float* wk,
@@ -154,7 +156,8 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate,
 
 /*
  * Block-sparse FlashAttention forward (section 3.3): for each query block i of
- * (b, h) and each active key block j of mask row (b, h, i),
+ * (b, h) and each active key block j of mask row (b, h, i) (blocks of `block`
+ * tokens, 64 or 128; a 128-token mask is run as its 64-token tiles),
  *   O_i = softmax(sm_scale * Q_i K^T) V over the keys of the active blocks,
  * with the causal mask applied inside the diagonal block when causal != 0.
  * sm_scale <= 0 selects 1/sqrt(head_dim).  o follows desc (same dtype as q);
@@ -163,7 +166,8 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate,
  * yields O = 0 and LSE = -inf.  When causal, list entries j > i end the row;
  * entries j >= nb always end it, and count is clamped to nb, so a malformed
  * mask cannot make the kernel read out of bounds.
- * Unsupported: block != 64, head_dim not in {64, 128}.
+ * Unsupported: block not in {64, 128} or not dividing seq_len, head_dim not in
+ * {64, 128}.
  */
 seer_status seer_bsattn(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
                         int32_t causal, float sm_scale, const void* q, const void* k,

@@ -176,9 +176,10 @@ class BlockMask:
         return self.idx.to(_torch().int32) & 0xFFFF
 
 
-def alloc_mask(batch: int, heads_q: int, seq_len: int, device="cuda", dense: bool = False) -> BlockMask:
+def alloc_mask(batch: int, heads_q: int, seq_len: int, device="cuda", dense: bool = False,
+               block: int = BLOCK) -> BlockMask:
     torch = _torch()
-    nb = seq_len // BLOCK
+    nb = seq_len // block
     return BlockMask(
         count=torch.empty((batch, heads_q, nb), dtype=torch.int32, device=device),
         idx=torch.empty((batch, heads_q, nb, nb), dtype=torch.int16, device=device),
@@ -191,9 +192,10 @@ def alloc_mask(batch: int, heads_q: int, seq_len: int, device="cuda", dense: boo
 
 def gate_desc(gate_dim: int, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
               threshold: float = 0.0, head_thresholds=None, keep_first: bool = True,
-              keep_diag: bool = True, w_per_head: bool = True, rope_theta: float = 0.0) -> GateDesc:
+              keep_diag: bool = True, w_per_head: bool = True, rope_theta: float = 0.0,
+              block: int = BLOCK) -> GateDesc:
     g = GateDesc()
-    g.block = BLOCK
+    g.block = block
     g.gate_dim = gate_dim
     g.w_per_head = int(bool(w_per_head))
     g.mode = mode
@@ -217,17 +219,17 @@ def gate_workspace_bytes(q, k, gate_dim: int, mode: int = TOPK_RATIO, topk_ratio
 def gate(q, k, wq, wk, *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
          threshold: float = 0.0, head_thresholds=None, keep_first: bool = True,
          keep_diag: bool = True, w_per_head: bool = True, rope_theta: float = 0.0,
-         mask: Optional[BlockMask] = None, dense_out: bool = False, logits_out=None,
-         workspace=None, stream=None) -> BlockMask:
-    """AttnGate + block selection (seer_gate).  Returns the block mask.  With
-    rope_theta > 0 (the model's RoPE base) q and k are pre-RoPE and the gate
-    applies its block-level RoPE."""
+         block: int = BLOCK, mask: Optional[BlockMask] = None, dense_out: bool = False,
+         logits_out=None, workspace=None, stream=None) -> BlockMask:
+    """AttnGate + block selection (seer_gate).  Returns the block mask (of
+    `block`-token blocks, 64 or 128).  With rope_theta > 0 (the model's RoPE
+    base) q and k are pre-RoPE and the gate applies its block-level RoPE."""
     torch = _torch()
     d = make_desc(q, k)
     gd = gate_desc(wq.shape[-1], mode, topk_ratio, topk_k, threshold, head_thresholds,
-                   keep_first, keep_diag, w_per_head, rope_theta)
+                   keep_first, keep_diag, w_per_head, rope_theta, block)
     if mask is None:
-        mask = alloc_mask(q.shape[0], q.shape[1], q.shape[2], q.device, dense=dense_out)
+        mask = alloc_mask(q.shape[0], q.shape[1], q.shape[2], q.device, dense=dense_out, block=block)
     need = lib().seer_gate_workspace_bytes(C.byref(d), C.byref(gd), int(logits_out is None))
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
@@ -263,13 +265,14 @@ def bsattn(q, k, v, mask: BlockMask, *, causal: bool = True, sm_scale: float = 0
         lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
     d = make_desc(q, k, v, out)
     ms = mask.struct()
+    block = q.shape[2] // mask.n_blocks if mask.n_blocks else BLOCK  # 64- or 128-token mask blocks
     if workspace is None:
-        st = lib().seer_bsattn(C.byref(d), BLOCK, C.byref(ms), int(bool(causal)), float(sm_scale),
+        st = lib().seer_bsattn(C.byref(d), block, C.byref(ms), int(bool(causal)), float(sm_scale),
                                _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
         _check(st, "seer_bsattn")
     else:
         wp, wn = _ws_args(workspace)
-        st = lib().seer_bsattn_ws(C.byref(d), BLOCK, C.byref(ms), int(bool(causal)), float(sm_scale),
+        st = lib().seer_bsattn_ws(C.byref(d), block, C.byref(ms), int(bool(causal)), float(sm_scale),
                                   _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), wp, wn, _stream(stream))
         _check(st, "seer_bsattn_ws")
     return out, lse
@@ -354,16 +357,17 @@ def gate_distill(q, k, wq, wk, gt, *, w_per_head: bool = True, rope_theta: float
 
 
 def mask_from_dense(dense, heads_kv: int = 1, mask: Optional[BlockMask] = None,
-                    stream=None) -> BlockMask:
-    """Compacts a uint8 [B, Hq, nb, nb] device mask (seer_mask_from_dense)."""
+                    block: int = BLOCK, stream=None) -> BlockMask:
+    """Compacts a uint8 [B, Hq, nb, nb] device mask of `block`-token blocks
+    (seer_mask_from_dense)."""
     torch = _torch()
     B, Hq, nb, _ = dense.shape
     if mask is None:
-        mask = alloc_mask(B, Hq, nb * BLOCK, dense.device)
+        mask = alloc_mask(B, Hq, nb * block, dense.device, block=block)
     d = AttnDesc()
-    d.batch, d.heads_q, d.heads_kv, d.seq_len, d.head_dim, d.dtype = B, Hq, heads_kv, nb * BLOCK, 128, BF16
+    d.batch, d.heads_q, d.heads_kv, d.seq_len, d.head_dim, d.dtype = B, Hq, heads_kv, nb * block, 128, BF16
     ms = mask.struct()
-    st = lib().seer_mask_from_dense(C.byref(d), BLOCK, _ptr(dense.contiguous()), C.byref(ms),
+    st = lib().seer_mask_from_dense(C.byref(d), block, _ptr(dense.contiguous()), C.byref(ms),
                                     _stream(stream))
     _check(st, "seer_mask_from_dense")
     return mask

@@ -140,13 +140,19 @@ struct KernelArgs {
 // Iterates the active key blocks of a row: the compacted list for the sparse
 // kernel, 0..i (causal) or 0..nb-1 for the dense one.  Entries that are out of
 // range (>= nb, or > i when causal) end the row.
+// A sparse row's list holds mask entries; with 128-token mask blocks (sh = 1)
+// position p of the row is the 64-key tile 2 idx[p / 2] + p % 2, so every
+// entry stands for two tiles and n counts tiles.
 template <bool SPARSE>
 struct RowList {
   const uint16_t* idx;
   int n, nb, i;
   int lo;  // dense: first key block
+  int sh;  // sparse: log2(mask block / 64)
   bool causal;
-  __device__ __forceinline__ int at(int p) const { return SPARSE ? (int)idx[p] : lo + p; }
+  __device__ __forceinline__ int at(int p) const {
+    return SPARSE ? ((int)idx[p >> sh] << sh) + (p & sh) : lo + p;
+  }
   __device__ __forceinline__ bool ok(int j) const { return j < nb && (!causal || j <= i); }
 };
 
@@ -159,11 +165,16 @@ __device__ __forceinline__ RowList<SPARSE> make_list(const AttnArgs& a, const Ta
   L.i = t.i;
   L.causal = a.causal;
   L.lo = 0;
+  L.sh = 0;
   const int64_t row = ((int64_t)t.b * a.heads_q + t.h) * a.n_blocks + t.i;
   if (SPARSE) {
-    L.idx = a.idx + row * a.n_blocks;
-    L.n = min(max(a.count[row], 0), a.n_blocks);
-    if (SPLIT) {
+    const int sh = a.mask_shift;
+    const int nbm = a.n_blocks >> sh;  // blocks of the mask
+    const int64_t mrow = ((int64_t)t.b * a.heads_q + t.h) * nbm + (t.i >> sh);
+    L.sh = sh;
+    L.idx = a.idx + mrow * nbm;
+    L.n = min(max(a.count[mrow], 0), nbm) << sh;
+    if (SPLIT) {  // (the split runs on 64-token masks only)
       const int32_t* bd = a.split_bounds + row * (a.split_parts + 1) + t.p;
       const int s0 = bd[0];
       L.idx += s0;
@@ -408,10 +419,11 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   const bool pool = !SPARSE && !SPLIT && a.gt != nullptr;  // ground-truth mode
   const int64_t trow = ((int64_t)t.b * a.heads_q + t.h) * a.n_blocks + t.i;
   float* const rrow = pool ? a.pool_r + trow * a.n_blocks * 64 : nullptr;
-  auto fetch_chunk = [&](int base) {  // entries [base, base + kListChunk) of the row list
+  auto fetch_chunk = [&](int base) {  // mask entries [base, base + kListChunk) of the row
     if (SPARSE) {
+      const int ne = list.n >> list.sh;
       for (int p = tid; p < kListChunk; p += 128)
-        if (base + p < list.n) sList[p] = list.idx[base + p];
+        if (base + p < ne) sList[p] = list.idx[base + p];
     }
   };
   // last valid key block: j <= i when causal, j < nb always (i < nb); a dense
@@ -420,7 +432,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   auto entry = [&](int p) -> int {  // p must lie in the current LDS window
     if (p >= list.n) return -1;
     if (!SPARSE) return list.lo + p;
-    const int jj = (int)sList[p % kListChunk];
+    const int jj = ((int)sList[(p >> list.sh) % kListChunk] << list.sh) + (p & list.sh);
     return jj <= jmax ? jj : -1;
   };
   fetch_chunk(0);
@@ -472,8 +484,8 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   auto tile = [&](f32x16 (&sc)[2], f32x16 (&sn)[2]) {
     int jnn = -1;
     if (jn >= 0) {
-      if (SPARSE && (n + 2) % kListChunk == 0 && n + 2 < list.n) {
-        fetch_chunk(n + 2);  // every thread has read entry n + 1 already
+      if (SPARSE && ((n + 2) & ((kListChunk << list.sh) - 1)) == 0 && n + 2 < list.n) {
+        fetch_chunk((n + 2) >> list.sh);  // every thread has read entry n + 1 already
         wait_loads();
         __syncthreads();
       }
@@ -977,7 +989,8 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   if (a.split_w > 0) {
     // the shape must be the one split_width accepted, with every buffer present
     const int P = a.split_parts;
-    if (pool || !a.bf16 || !a.causal || (P != 8 && P != 16) || a.split_w * P != a.n_blocks ||
+    if (pool || !a.bf16 || !a.causal || (sparse && a.mask_shift != 0) || (P != 8 && P != 16) ||
+        a.split_w * P != a.n_blocks ||
         (P == 8 && (a.batch * a.heads_kv) % 2 != 0) || !a.part_lse || !a.part_o ||
         (sparse && !a.split_bounds) || a.split_slots != split_slots_per_head(a.n_blocks, a.split_w))
       return hipErrorInvalidValue;

@@ -1,7 +1,7 @@
 // gate_kernels.hip -- AttnGate kernels for gfx950 (SeerAttention, arXiv 2410.13276).
 //
 //   pool_proj_kernel    section 3.1 + Eq. 1: average-pool Q and max|min|avg-pool K
-//                       over each 64-token block, then the gate linear layers and,
+//                       over each 64- or 128-token block, then the gate linear layers and,
 //                       optionally, the block-level RoPE of section 3.1.
 //                       HBM-bound: streams Q and K once with 16-byte loads; the
 //                       GEMV reuses each weight element for every block of the
@@ -50,7 +50,7 @@ struct Load16<uint16_t> {
 // One workgroup of 256 threads pools R consecutive 64-token blocks of one head
 // (each thread owns one 16-byte column chunk of one block and walks its 64 rows)
 // and then projects the R pooled rows through the head's gate weights.
-template <typename T, int D, int DG, bool IS_K>
+template <typename T, int D, int DG, bool IS_K, int BLK>
 __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t ss, int nb,
                                                const float* __restrict__ W,
                                                float* __restrict__ out, float* smem,
@@ -76,9 +76,9 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
       mx[e] = -INFINITY;
       mn[e] = INFINITY;
     }
-    const T* base = x + (int64_t)blk * kBlock * ss + c * EPL;
+    const T* base = x + (int64_t)blk * BLK * ss + c * EPL;
 #pragma unroll 8
-    for (int row = 0; row < kBlock; ++row) {
+    for (int row = 0; row < BLK; ++row) {
       float v[EPL];
       Load16<T>::get(base + row * ss, v);
 #pragma unroll
@@ -93,7 +93,7 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
     float* prow = smem + r * WIDTH + c * EPL;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      const float avg = sum[e] * (1.0f / kBlock);
+      const float avg = sum[e] * (1.0f / BLK);
       if (IS_K) {
         prow[e] = mx[e];
         prow[D + e] = mn[e];
@@ -165,7 +165,7 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
   }
 }
 
-template <typename T, int D, int DG>
+template <typename T, int D, int DG, int BLK>
 __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
   constexpr int EPL = Load16<T>::N;
   constexpr int R = 256 / (D / EPL);
@@ -178,14 +178,14 @@ __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
     const T* x = static_cast<const T*>(a.q.ptr) + b * a.q.sb + h * a.q.sh;
     float* out = a.qg + ((int64_t)b * a.heads_q + h) * a.n_blocks * DG;
     float* po = a.qp ? a.qp + ((int64_t)b * a.heads_q + h) * a.n_blocks * D : nullptr;
-    pool_proj_head<T, D, DG, false>(x, a.q.ss, a.n_blocks, a.wq + h * a.wq_head_stride, out, smem, srot,
+    pool_proj_head<T, D, DG, false, BLK>(x, a.q.ss, a.n_blocks, a.wq + h * a.wq_head_stride, out, smem, srot,
                                     a.rope_base, po);
   } else {
     const int g = slot - a.heads_q;
     const T* x = static_cast<const T*>(a.k.ptr) + b * a.k.sb + g * a.k.sh;
     float* out = a.kg + ((int64_t)b * a.heads_kv + g) * a.n_blocks * DG;
     float* po = a.kp ? a.kp + ((int64_t)b * a.heads_kv + g) * a.n_blocks * 3 * D : nullptr;
-    pool_proj_head<T, D, DG, true>(x, a.k.ss, a.n_blocks, a.wk + g * a.wk_head_stride, out, smem, srot,
+    pool_proj_head<T, D, DG, true, BLK>(x, a.k.ss, a.n_blocks, a.wk + g * a.wk_head_stride, out, smem, srot,
                                    a.rope_base, po);
   }
 }
@@ -194,7 +194,9 @@ template <typename T, int D, int DG>
 static hipError_t pool_proj_launch(const PoolProjArgs& a, hipStream_t s) {
   constexpr int R = 256 / (D / Load16<T>::N);
   dim3 grid((a.n_blocks + R - 1) / R, a.heads_q + a.heads_kv, a.batch);
-  hipLaunchKernelGGL((pool_proj_kernel<T, D, DG>), grid, dim3(256), 0, s, a);
+  if (a.block == 64) hipLaunchKernelGGL((pool_proj_kernel<T, D, DG, 64>), grid, dim3(256), 0, s, a);
+  else if (a.block == 128) hipLaunchKernelGGL((pool_proj_kernel<T, D, DG, 128>), grid, dim3(256), 0, s, a);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

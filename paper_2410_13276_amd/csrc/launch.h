@@ -24,6 +24,7 @@ struct PoolProjArgs {
   double rope_base;  // > 0: block-level RoPE with this base (model base / block)
   float* qp;  // optional pooled Q [B][Hq][nb][D] (nullptr: not stored)
   float* kp;  // optional pooled K [B][Hkv][nb][3D]
+  int block;  // tokens per gate block: 64 or 128
 };
 
 struct GateLogitsArgs {
@@ -67,6 +68,8 @@ struct AttnArgs {
   float scale;
   const int32_t* count;  // nullptr: dense (every causal block)
   const uint16_t* idx;
+  int mask_shift;        // 0: mask of 64-token blocks; 1: of 128-token blocks, each
+                         // entry standing for two 64-key tiles
   // ground-truth mode (dense only): per-tile row maxima [rows][nb][64] and the
   // 2D max-pooled probability map [B][Hq][nb][nb]; both nullptr otherwise
   float* pool_r;

@@ -52,9 +52,10 @@ seer_status check_gate_common(const seer_attn_desc* d, const seer_gate_desc* g) 
   seer_status s = check_desc(d, 0x3);
   if (s != SEER_OK) return s;
   if (!g) return SEER_ERR_INVALID_ARG;
-  if (g->block != SEER_BLOCK) return SEER_ERR_UNSUPPORTED;
+  if (g->block != 64 && g->block != 128) return SEER_ERR_UNSUPPORTED;
+  if (d->seq_len % g->block != 0) return SEER_ERR_UNSUPPORTED;
   if (g->gate_dim != 32 && g->gate_dim != 64 && g->gate_dim != 128) return SEER_ERR_UNSUPPORTED;
-  if (d->seq_len / SEER_BLOCK > 4096) return SEER_ERR_UNSUPPORTED;
+  if (d->seq_len / g->block > 4096) return SEER_ERR_UNSUPPORTED;
   if (!(g->rope_theta >= 0.0) || std::isinf(g->rope_theta)) return SEER_ERR_INVALID_ARG;
   return SEER_OK;
 }
@@ -83,7 +84,7 @@ struct GateLayout {
 };
 
 GateLayout gate_layout(const seer_attn_desc* d, const seer_gate_desc* g, bool logits_in_ws) {
-  const size_t nb = (size_t)(d->seq_len / SEER_BLOCK);
+  const size_t nb = (size_t)(d->seq_len / g->block);
   GateLayout L;
   L.qg = 0;
   L.kg = round_up((size_t)d->batch * d->heads_q * nb * g->gate_dim * 4);
@@ -99,7 +100,7 @@ struct DistillLayout {
 };
 
 DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g) {
-  const size_t nb = (size_t)(d->seq_len / SEER_BLOCK);
+  const size_t nb = (size_t)(d->seq_len / g->block);
   const size_t B = d->batch, Hq = d->heads_q, Hkv = d->heads_kv, D = d->head_dim, Dg = g->gate_dim;
   DistillLayout L;
   size_t off = 0;
@@ -153,6 +154,7 @@ seer::AttnArgs attn_args(const seer_attn_desc* desc, int32_t causal, float sm_sc
   a.scale = sm_scale > 0.f ? sm_scale : (float)(1.0 / std::sqrt((double)desc->head_dim));
   a.count = nullptr;
   a.idx = nullptr;
+  a.mask_shift = 0;
   a.pool_r = nullptr;
   a.gt = nullptr;
   a.split_parts = 0;
@@ -222,10 +224,10 @@ size_t seer_gate_workspace_bytes(const seer_attn_desc* desc, const seer_gate_des
 }
 
 size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block) {
-  if (!desc || block != SEER_BLOCK || desc->batch <= 0 || desc->heads_q <= 0 || desc->seq_len <= 0 ||
-      desc->seq_len % SEER_BLOCK != 0)
+  if (!desc || (block != 64 && block != 128) || desc->batch <= 0 || desc->heads_q <= 0 ||
+      desc->seq_len <= 0 || desc->seq_len % block != 0)
     return 0;
-  const size_t nb = (size_t)(desc->seq_len / SEER_BLOCK);
+  const size_t nb = (size_t)(desc->seq_len / block);
   return (size_t)desc->batch * desc->heads_q * nb * nb;
 }
 
@@ -236,7 +238,7 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   if (s != SEER_OK) return s;
   if (!q || !k || !wq || !wk || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
-  const int nb = desc->seq_len / SEER_BLOCK;
+  const int nb = desc->seq_len / gate->block;
   if (out->n_blocks != nb) return SEER_ERR_INVALID_ARG;
   const bool logits_in_ws = logits_out == nullptr;
   const GateLayout L = gate_layout(desc, gate, logits_in_ws);
@@ -269,6 +271,7 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   pa.rope_base = gate->rope_theta > 0.0 ? gate->rope_theta / gate->block : 0.0;
   pa.qp = nullptr;
   pa.kp = nullptr;
+  pa.block = gate->block;
   if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
 
   seer::GateLogitsArgs la;
@@ -301,21 +304,25 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   return from_hip(seer::launch_select(sa, st));
 }
 
-static seer_status attn_common(const seer_attn_desc* desc, const seer_block_mask* mask,
+// block: tokens per mask block (64 or 128; ignored without a mask).
+static seer_status attn_common(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
                                int32_t causal, float sm_scale, const void* q, const void* k,
                                const void* v, void* o, float* lse, void* workspace,
                                size_t workspace_bytes, void* stream) {
   seer_status s = check_attn(desc, sm_scale, q, k, v, o);
   if (s != SEER_OK) return s;
-  const int nb = desc->seq_len / SEER_BLOCK;
   if (mask) {
-    if (!mask->count || !mask->idx || mask->n_blocks != nb) return SEER_ERR_INVALID_ARG;
-    if (nb > 65536) return SEER_ERR_UNSUPPORTED;
+    if (block != 64 && block != 128) return SEER_ERR_UNSUPPORTED;
+    if (desc->seq_len % block != 0) return SEER_ERR_UNSUPPORTED;
+    const int nbm = desc->seq_len / block;
+    if (!mask->count || !mask->idx || mask->n_blocks != nbm) return SEER_ERR_INVALID_ARG;
+    if (nbm > 65536) return SEER_ERR_UNSUPPORTED;
   }
   seer::AttnArgs a = attn_args(desc, causal, sm_scale, q, k, v, o, lse);
   a.count = mask ? mask->count : nullptr;
   a.idx = mask ? mask->idx : nullptr;
-  if (workspace) {
+  a.mask_shift = (mask && block == 128) ? 1 : 0;
+  if (workspace && a.mask_shift == 0) {  // the split runs on 64-token masks
     if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
     const SplitLayout L = split_layout(desc, split_parts_for(desc, causal, mask != nullptr));
     if (L.w > 0 && workspace_bytes >= L.total) {  // key-range split
@@ -334,15 +341,14 @@ static seer_status attn_common(const seer_attn_desc* desc, const seer_block_mask
 seer_status seer_bsattn(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
                         int32_t causal, float sm_scale, const void* q, const void* k,
                         const void* v, void* o, float* lse, void* stream) {
-  if (block != SEER_BLOCK) return desc ? SEER_ERR_UNSUPPORTED : SEER_ERR_INVALID_ARG;
-  if (!mask) return SEER_ERR_INVALID_ARG;
-  return attn_common(desc, mask, causal, sm_scale, q, k, v, o, lse, nullptr, 0, stream);
+  if (!mask || !desc) return SEER_ERR_INVALID_ARG;
+  return attn_common(desc, block, mask, causal, sm_scale, q, k, v, o, lse, nullptr, 0, stream);
 }
 
 seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm_scale,
                             const void* q, const void* k, const void* v, void* o, float* lse,
                             void* stream) {
-  return attn_common(desc, nullptr, causal, sm_scale, q, k, v, o, lse, nullptr, 0, stream);
+  return attn_common(desc, SEER_BLOCK, nullptr, causal, sm_scale, q, k, v, o, lse, nullptr, 0, stream);
 }
 
 size_t seer_attn_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t causal) {
@@ -355,24 +361,24 @@ size_t seer_attn_workspace_bytes(const seer_attn_desc* desc, int32_t block, int3
 seer_status seer_bsattn_ws(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
                            int32_t causal, float sm_scale, const void* q, const void* k, const void* v,
                            void* o, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
-  if (block != SEER_BLOCK) return desc ? SEER_ERR_UNSUPPORTED : SEER_ERR_INVALID_ARG;
-  if (!mask) return SEER_ERR_INVALID_ARG;
-  return attn_common(desc, mask, causal, sm_scale, q, k, v, o, lse, workspace, workspace_bytes, stream);
+  if (!mask || !desc) return SEER_ERR_INVALID_ARG;
+  return attn_common(desc, block, mask, causal, sm_scale, q, k, v, o, lse, workspace, workspace_bytes,
+                     stream);
 }
 
 seer_status seer_dense_attn_ws(const seer_attn_desc* desc, int32_t causal, float sm_scale,
                                const void* q, const void* k, const void* v, void* o, float* lse,
                                void* workspace, size_t workspace_bytes, void* stream) {
-  return attn_common(desc, nullptr, causal, sm_scale, q, k, v, o, lse, workspace, workspace_bytes,
-                     stream);
+  return attn_common(desc, SEER_BLOCK, nullptr, causal, sm_scale, q, k, v, o, lse, workspace,
+                     workspace_bytes, stream);
 }
 
 seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, const uint8_t* dense,
                                  seer_block_mask* out, void* stream) {
   if (!desc || !dense || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
   if (desc->batch <= 0 || desc->heads_q <= 0 || desc->seq_len <= 0) return SEER_ERR_INVALID_ARG;
-  if (block != SEER_BLOCK || desc->seq_len % SEER_BLOCK != 0) return SEER_ERR_UNSUPPORTED;
-  const int nb = desc->seq_len / SEER_BLOCK;
+  if ((block != 64 && block != 128) || desc->seq_len % block != 0) return SEER_ERR_UNSUPPORTED;
+  const int nb = desc->seq_len / block;
   if (out->n_blocks != nb) return SEER_ERR_INVALID_ARG;
   if (nb > 4096) return SEER_ERR_UNSUPPORTED;
   seer::MaskFromDenseArgs a;
@@ -464,7 +470,7 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int B = desc->batch, Hq = desc->heads_q, Hkv = desc->heads_kv, D = desc->head_dim;
   const int Dg = gate->gate_dim, G = Hq / Hkv;
-  const int nb = desc->seq_len / SEER_BLOCK;
+  const int nb = desc->seq_len / gate->block;
   const double rope_base = gate->rope_theta > 0.0 ? gate->rope_theta / gate->block : 0.0;
   const float rsqrt_dg = (float)(1.0 / std::sqrt((double)Dg));
 
@@ -488,6 +494,7 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   pa.rope_base = rope_base;
   pa.qp = qp;
   pa.kp = kp;
+  pa.block = gate->block;
   if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
 
   seer::GateLogitsArgs la;

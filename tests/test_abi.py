@@ -74,7 +74,8 @@ def test_workspace_size_formula():
     assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 0) == want
     assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 1) == want + up(2 * 4 * nb * nb * 4)
     assert L.seer_mask_idx_elems(C.byref(d), 64) == 2 * 4 * nb * nb
-    assert L.seer_mask_idx_elems(C.byref(d), 128) == 0
+    assert L.seer_mask_idx_elems(C.byref(d), 128) == 2 * 4 * (nb // 2) ** 2   # 128-token blocks
+    assert L.seer_mask_idx_elems(C.byref(d), 96) == 0
 
 
 @pytest.mark.parametrize("field,value,status", [
@@ -91,7 +92,7 @@ def test_gate_rejects_bad_desc(field, value, status):
 
 
 @pytest.mark.parametrize("field,value,status", [
-    ("block", 128, seer.ERR_UNSUPPORTED),
+    ("block", 96, seer.ERR_UNSUPPORTED),
     ("gate_dim", 48, seer.ERR_UNSUPPORTED),
     ("mode", 9, seer.ERR_INVALID_ARG),
     ("topk_ratio", 0.0, seer.ERR_INVALID_ARG),
@@ -125,7 +126,8 @@ def test_attention_rejects_bad_args():
     m = seer.BlockMaskStruct()
     m.n_blocks, m.count, m.idx, m.dense = 16, FAKE, FAKE, None
     args = (FAKE, FAKE, FAKE, FAKE, None, None)
-    assert L.seer_bsattn(C.byref(d), 128, C.byref(m), 1, 0.0, *args) == seer.ERR_UNSUPPORTED
+    assert L.seer_bsattn(C.byref(d), 96, C.byref(m), 1, 0.0, *args) == seer.ERR_UNSUPPORTED
+    assert L.seer_bsattn(C.byref(d), 128, C.byref(m), 1, 0.0, *args) == seer.ERR_INVALID_ARG  # nb 16 != 8
     assert L.seer_bsattn(C.byref(d), 64, None, 1, 0.0, *args) == seer.ERR_INVALID_ARG
     m.n_blocks = 8
     assert L.seer_bsattn(C.byref(d), 64, C.byref(m), 1, 0.0, *args) == seer.ERR_INVALID_ARG
@@ -223,3 +225,18 @@ def test_attention_ws_rejects_bad_args():
         seer.ERR_INVALID_ARG                                               # misaligned workspace
     assert L.seer_dense_attn_ws(C.byref(d), 1, float("inf"), *args, FAKE * 16, 1 << 30, None) == \
         seer.ERR_INVALID_ARG
+
+
+def test_block_128_gate_and_mask_validation():
+    L = seer.lib()
+    d = _desc(B=1, Hq=4, Hkv=2, S=1088, D=128)   # 1088 = 17 x 64: not a multiple of 128
+    assert _call_gate(d, _gate(block=128), mask_nb=8) == seer.ERR_UNSUPPORTED
+    d = _desc(B=1, Hq=4, Hkv=2, S=1024, D=128)
+    assert _call_gate(d, _gate(block=128), mask_nb=16) == seer.ERR_INVALID_ARG  # mask must have 8 blocks
+    g = _gate(block=128)
+    need = L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 1)
+    up = lambda x: (x + 255) // 256 * 256
+    assert need == up(4 * 8 * 128 * 4) + up(2 * 8 * 128 * 4) + up(4 * 8 * 8 * 4)
+    m = seer.BlockMaskStruct()
+    m.n_blocks, m.count, m.idx, m.dense = 16, FAKE, FAKE, None
+    assert L.seer_mask_from_dense(C.byref(d), 128, FAKE, C.byref(m), None) == seer.ERR_INVALID_ARG

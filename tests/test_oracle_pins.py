@@ -79,6 +79,20 @@ def test_pool_matches_torch_pooling(dtype):
     np.testing.assert_allclose(k[..., 2 * D:], avg.numpy(), rtol=1e-14, atol=1e-15)  # then avg
 
 
+def test_pool_128_combines_two_64_halves():
+    # a 128-token block pools to max of maxes, min of mins, mean of means of its halves
+    x = _rand((2, 3, 512, 8), 4)
+    k64 = oracle.pool(x, 64, oracle.POOL_MAX_MIN_AVG)
+    k128 = oracle.pool(x, 128, oracle.POOL_MAX_MIN_AVG)
+    q64, q128 = oracle.pool(x, 64, oracle.POOL_AVG), oracle.pool(x, 128, oracle.POOL_AVG)
+    D = 8
+    a, b = k64[:, :, 0::2], k64[:, :, 1::2]
+    np.testing.assert_array_equal(k128[..., :D], np.maximum(a[..., :D], b[..., :D]))
+    np.testing.assert_array_equal(k128[..., D:2 * D], np.minimum(a[..., D:2 * D], b[..., D:2 * D]))
+    np.testing.assert_allclose(k128[..., 2 * D:], (a[..., 2 * D:] + b[..., 2 * D:]) / 2, rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(q128, (q64[:, :, 0::2] + q64[:, :, 1::2]) / 2, rtol=1e-14, atol=1e-15)
+
+
 def test_pool_strided_input_matches_contiguous():
     x = _rand((1, 4, 128, 16), 2)
     view = x[:, ::2]  # non-contiguous head stride
@@ -345,14 +359,15 @@ def test_dense_noncausal_matches_sdpa():
     np.testing.assert_allclose(_o_full(O, B, H, S, D), _sdpa(q, k, v), rtol=1e-10, atol=1e-12)
 
 
+@pytest.mark.parametrize("blk", [64, 128])
 @pytest.mark.parametrize("kind", ["a_shape", "vertical", "slash", "random"])
-def test_block_masked_matches_sdpa_with_token_mask(kind):
-    B, Hq, Hkv, S, D, blk = 1, 4, 2, 512, 16, 64
+def test_block_masked_matches_sdpa_with_token_mask(kind, blk):
+    B, Hq, Hkv, S, D = 1, 4, 2, 512, 16
     nb = S // blk
     q, k, v = _rand((B, Hq, S, D), 7), _rand((B, Hkv, S, D), 8), _rand((B, Hkv, S, D), 9)
     bm = np.stack([pattern_mask(kind, nb, 100 + h, 0.3) for h in range(Hq)])[None]
     bm[..., np.arange(nb), np.arange(nb)] = 1  # keep the diagonal so no row is empty
-    O, lse = oracle.attn(q, k, v, mask=bm)
+    O, lse = oracle.attn(q, k, v, mask=bm, block=blk)
     tok = np.kron(bm, np.ones((blk, blk), np.uint8)).astype(bool) & np.tril(np.ones((S, S), bool))
     ref = _sdpa(q, k, v, attn_mask=torch.from_numpy(tok))
     np.testing.assert_allclose(_o_full(O, B, Hq, S, D), ref, rtol=1e-10, atol=1e-12)
