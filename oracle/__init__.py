@@ -100,12 +100,12 @@ def _strides(x: np.ndarray) -> np.ndarray:
 def pool(x: np.ndarray, block: int, kind: int) -> np.ndarray:
     """Sequence pooling of [B, H, S, D]: avg -> [B,H,nb,D]; max|min|avg -> [B,H,nb,3D]."""
     B, H, S, D = x.shape
-    nb = S // block
+    nb = -(-S // block)  # the last block may be partial
     out = np.empty((B, H, nb, D if kind == POOL_AVG else 3 * D), dtype=np.float64)
     st = _strides(x)
     rc = lib().orc_pool(_ptr(x), _dtype_code(x), B, H, S, D, _ptr(st), block, kind, _ptr(out))
     if rc != 0:
-        raise ValueError("seq_len must be a multiple of block")
+        raise ValueError("bad pooling arguments")
     return out
 
 
@@ -198,11 +198,12 @@ def attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, block: int = 64, causal: b
 
     q [B,Hq,S,D], k/v [B,Hkv,S,D] (fp32 or bf16 bits, same type); mask uint8
     [B,Hq,nb,nb] or None (dense); rows int32 [n,3] of (b,h,i) or None (all).
-    Returns (O [n, block, D], LSE [n, block]) with n = len(rows) or B*Hq*nb."""
+    Returns (O [n, block, D], LSE [n, block]) with n = len(rows) or B*Hq*nb; rows
+    past the end of a partial last block are NaN."""
     assert q.dtype == k.dtype == v.dtype
     B, Hq, S, D = q.shape
     Hkv = k.shape[1]
-    nb = S // block
+    nb = -(-S // block)  # the last block may be partial
     if scale is None:
         scale = 1.0 / np.sqrt(D)
     if mask is not None:
@@ -229,7 +230,7 @@ def maxpool_gt(q: np.ndarray, k: np.ndarray, block: int = 64, scale: Optional[fl
     Returns [B,Hq,nb,nb], or [n, nb] for rows int32 [n,3] of (b,h,i)."""
     B, Hq, S, D = q.shape
     Hkv = k.shape[1]
-    nb = S // block
+    nb = -(-S // block)  # the last block may be partial
     if scale is None:
         scale = 1.0 / np.sqrt(D)
     n = B * Hq * nb
@@ -285,7 +286,7 @@ def distill(q: np.ndarray, k: np.ndarray, wq: np.ndarray, wk: np.ndarray, gt: np
     B, Hq, S, D = q.shape
     Hkv = k.shape[1]
     G = Hq // Hkv
-    nb = S // block
+    nb = -(-S // block)  # the last block may be partial
     Wq = np.asarray(wq, dtype=np.float64).reshape(-1, D, wq.shape[-1])
     Wk = np.asarray(wk, dtype=np.float64).reshape(-1, 3 * D, wk.shape[-1])
     Dg = Wq.shape[-1]

@@ -37,6 +37,10 @@
  *                        not) attention probability map, the distillation
  *                        ground truth; all rows or a subset of query blocks.
  *
+ * Sequences need not be a multiple of the block: the last block is then
+ * partial (pooled over the tokens it holds; its rows past the end are not
+ * queries and come back as NaN from orc_attn).
+ *
  * Inputs arrive in the element type the GPU receives (fp32, or bf16 given as
  * raw 16-bit patterns) and are widened to double exactly before any arithmetic.
  * Strides are in elements, in the order (batch, head, sequence); the head
@@ -88,8 +92,8 @@ int orc_set_threads(int n) {
  */
 int orc_pool(const void *x, int dtype, int B, int H, int S, int D,
              const int64_t *st, int block, int kind, double *out) {
-  if (block <= 0 || S % block != 0) return -1;
-  const int nb = S / block;
+  if (block <= 0 || S <= 0) return -1;
+  const int nb = (S + block - 1) / block; /* the last block may be partial */
   const int width = (kind == ORC_POOL_AVG) ? D : 3 * D;
 #pragma omp parallel for collapse(2) schedule(static)
   for (int b = 0; b < B; ++b)
@@ -98,13 +102,14 @@ int orc_pool(const void *x, int dtype, int B, int H, int S, int D,
         double *o = out + (((int64_t)b * H + h) * nb + i) * width;
         for (int d = 0; d < D; ++d) {
           double sum = 0.0, mx = -INFINITY, mn = INFINITY;
-          for (int t = i * block; t < (i + 1) * block; ++t) {
+          const int t_end = (i + 1) * block < S ? (i + 1) * block : S;
+          for (int t = i * block; t < t_end; ++t) {
             double v = elem(x, dtype, b * st[0] + h * st[1] + t * st[2] + d);
             sum += v;
             if (v > mx) mx = v;
             if (v < mn) mn = v;
           }
-          double avg = sum / block;
+          double avg = sum / (t_end - i * block);
           if (kind == ORC_POOL_AVG) {
             o[d] = avg;
           } else {
@@ -329,8 +334,8 @@ int orc_attn(const void *q, const void *k, const void *v, int dtype, int B,
              const int64_t *vs, int block, int causal, double scale,
              const uint8_t *mask, const int32_t *rows, int n_rows, double *O,
              double *LSE) {
-  if (block <= 0 || S % block != 0 || Hkv <= 0 || Hq % Hkv != 0) return -1;
-  const int nb = S / block;
+  if (block <= 0 || S <= 0 || Hkv <= 0 || Hq % Hkv != 0) return -1;
+  const int nb = (S + block - 1) / block; /* the last block may be partial */
   const int G = Hq / Hkv;
   const int64_t total = rows ? n_rows : (int64_t)B * Hq * nb;
   int bad = 0;
@@ -359,6 +364,11 @@ int orc_attn(const void *q, const void *k, const void *v, int dtype, int B,
     for (int tt = 0; tt < block; ++tt) {
       const int t = i * block + tt;
       double *o = O + (r * block + tt) * D;
+      if (t >= S) { /* past the end of a partial last block: no query */
+        for (int d = 0; d < D; ++d) o[d] = NAN;
+        if (LSE) LSE[r * block + tt] = NAN;
+        continue;
+      }
       for (int d = 0; d < D; ++d) qv[d] = elem(q, dtype, b * qs[0] + h * qs[1] + (int64_t)t * qs[2] + d);
       double m = -INFINITY;
       for (int s = 0; s < S; ++s) {
@@ -406,8 +416,8 @@ int orc_maxpool_gt(const void *q, const void *k, int dtype, int B, int Hq,
                    int Hkv, int S, int D, const int64_t *qs, const int64_t *ks,
                    int block, int causal, double scale, const int32_t *rows,
                    int64_t n_rows, double *gt) {
-  if (block <= 0 || S % block != 0 || Hkv <= 0 || Hq % Hkv != 0) return -1;
-  const int nb = S / block;
+  if (block <= 0 || S <= 0 || Hkv <= 0 || Hq % Hkv != 0) return -1;
+  const int nb = (S + block - 1) / block; /* the last block may be partial */
   const int G = Hq / Hkv;
   const int64_t n = rows ? n_rows : (int64_t)B * Hq * nb;
   int bad = 0;
@@ -435,7 +445,8 @@ int orc_maxpool_gt(const void *q, const void *k, int dtype, int B, int Hq,
     }
     double *out = gt + r * nb;
     for (int j = 0; j < nb; ++j) out[j] = 0.0;
-    for (int t = i * block; t < (i + 1) * block; ++t) {
+    const int t_end = (i + 1) * block < S ? (i + 1) * block : S;
+    for (int t = i * block; t < t_end; ++t) {
       const int last = causal ? t : S - 1; /* keys 0..last are visible */
       double m = -INFINITY;
       for (int s = 0; s <= last; ++s) {

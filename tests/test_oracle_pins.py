@@ -101,9 +101,67 @@ def test_pool_strided_input_matches_contiguous():
     np.testing.assert_array_equal(a, b)
 
 
-def test_pool_rejects_ragged_sequence():
-    with pytest.raises(ValueError):
-        oracle.pool(_rand((1, 1, 100, 4), 3), 64, oracle.POOL_AVG)
+@pytest.mark.parametrize("blk", [64, 128])
+def test_pool_partial_last_block(blk):
+    # a sequence that is not a multiple of the block: the last block pools over
+    # the tokens it holds (blocks do not overlap, section 3.1)
+    S = 3 * blk + 37
+    x = _rand((1, 2, S, 4), 3)
+    q = oracle.pool(x, blk, oracle.POOL_AVG)
+    k = oracle.pool(x, blk, oracle.POOL_MAX_MIN_AVG)
+    assert q.shape[2] == 4 and k.shape[2] == 4
+    tail = x[:, :, 3 * blk:].astype(np.float64)
+    np.testing.assert_allclose(q[:, :, 3], tail.mean(axis=2), rtol=1e-14, atol=1e-15)
+    np.testing.assert_array_equal(k[:, :, 3, :4], tail.max(axis=2))
+    np.testing.assert_array_equal(k[:, :, 3, 4:8], tail.min(axis=2))
+    np.testing.assert_allclose(k[:, :, 2, 8:], x[:, :, 2 * blk:3 * blk].astype(np.float64).mean(axis=2),
+                               rtol=1e-14, atol=1e-15)
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_partial_last_block_attention_matches_sdpa(causal):
+    B, Hq, Hkv, S, D = 1, 2, 1, 64 * 5 + 23, 16
+    q, k, v = _rand((B, Hq, S, D), 51), _rand((B, Hkv, S, D), 52), _rand((B, Hkv, S, D), 53)
+    nb = 6
+    bm = np.stack([pattern_mask("random", nb, 7 + h, 0.5) for h in range(Hq)])[None]
+    bm[..., np.arange(nb), np.arange(nb)] = 1
+    O, lse = oracle.attn(q, k, v, mask=bm, causal=causal)
+    tok = np.kron(bm, np.ones((64, 64), np.uint8))[..., :S, :S].astype(bool)
+    if causal:
+        tok &= np.tril(np.ones((S, S), bool))
+    ref = _sdpa(q, k, v, attn_mask=torch.from_numpy(tok))
+    Of = O.reshape(B, Hq, nb * 64, D)
+    np.testing.assert_allclose(Of[:, :, :S], ref, rtol=1e-10, atol=1e-12)
+    assert np.isnan(Of[:, :, S:]).all() and np.isnan(lse.reshape(B, Hq, nb * 64)[:, :, S:]).all()
+
+
+def test_partial_last_block_maxpool_matches_torch_ceil_mode():
+    B, Hq, S, D = 1, 2, 64 * 3 + 50, 8
+    q, k = _rand((B, Hq, S, D), 54), _rand((B, 1, S, D), 55)
+    gt = oracle.maxpool_gt(q, k)
+    tq = torch.from_numpy(q.astype(np.float64))
+    tk = torch.from_numpy(k.astype(np.float64)).repeat_interleave(Hq, dim=1)
+    sc = (tq @ tk.transpose(-1, -2)) / math.sqrt(D)
+    sc = sc.masked_fill(~torch.ones(S, S, dtype=torch.bool).tril(), float("-inf"))
+    ref = F.max_pool2d(torch.softmax(sc, -1), 64, 64, ceil_mode=True).numpy()
+    np.testing.assert_allclose(gt, ref, rtol=1e-12, atol=0)
+
+
+def test_partial_last_block_distill_gradients():
+    rng = np.random.default_rng(56)
+    S, D, Dg = 64 * 3 + 29, 16, 8
+    q = rng.standard_normal((1, 2, S, D)).astype(np.float32)
+    k = rng.standard_normal((1, 1, S, D)).astype(np.float32)
+    wq, wk = rng.standard_normal((2, D, Dg)) * 0.4, rng.standard_normal((1, 3 * D, Dg)) * 0.4
+    gt = oracle.maxpool_gt(q, k)
+    loss, dwq, dwk = oracle.distill(q, k, wq, wk, gt)
+    h = 1e-6
+    for idx in [(0, 3, 2), (1, 15, 7)]:
+        Wp, Wm = wq.copy(), wq.copy()
+        Wp[idx] += h
+        Wm[idx] -= h
+        fd = (oracle.distill(q, k, Wp, wk, gt)[0] - oracle.distill(q, k, Wm, wk, gt)[0]) / (2 * h)
+        assert abs(fd - dwq[idx]) <= 1e-6 * max(1e-3, abs(fd)) + 1e-9
 
 
 # --------------------------------------------------------------------------
