@@ -38,6 +38,10 @@
  *    (batch, head, seq) and head_dim contiguous.  Query head h reads KV head
  *    h / (heads_q / heads_kv) (grouped-query attention, contiguous groups).
  *  - "Causal" means aligned prefill: query t sees key s iff s <= t.
+ *  - seq_len need not be a multiple of the block: nb = ceil(seq_len / block),
+ *    and the last block is partial (the gate pools it over the tokens it
+ *    holds; attention neither reads past the end of Q/K/V nor writes past the
+ *    end of O/LSE).
  */
 #ifndef SEER_H
 #define SEER_H
@@ -74,7 +78,7 @@ typedef struct {
   int32_t batch;
   int32_t heads_q;
   int32_t heads_kv;  /* heads_q % heads_kv == 0 */
-  int32_t seq_len;   /* a multiple of SEER_BLOCK */
+  int32_t seq_len;   /* any length >= 1 (the last block may be partial) */
   int32_t head_dim;  /* 64 or 128 */
   int32_t dtype;     /* seer_dtype of Q, K, V and O */
   int64_t q_stride[3]; /* element strides of (batch, head, seq); head_dim stride is 1 */
@@ -107,7 +111,7 @@ typedef struct {
 /* Block mask in compacted form: for row r = (b, h, i), idx[r][0 .. count[r]-1]
  * are the active key blocks j in strictly ascending order.  Caller-owned. */
 typedef struct {
-  int32_t n_blocks;  /* nb = seq_len / block (64 or 128) */
+  int32_t n_blocks;  /* nb = ceil(seq_len / block), block 64 or 128 */
   int32_t* count;    /* device [batch][heads_q][nb] */
   uint16_t* idx;     /* device [batch][heads_q][nb][nb] */
   uint8_t* dense;    /* optional device [batch][heads_q][nb][nb] 0/1 copy, or NULL */
@@ -146,8 +150,8 @@ size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block);
  * (entries above the diagonal unspecified); when NULL, L lives in the workspace.
  * workspace: device memory of at least seer_gate_workspace_bytes(desc, gate,
  * logits_out == NULL) bytes, 256-byte aligned.
- * Unsupported: gate->block not in {64, 128} or not dividing seq_len, head_dim
- * not in {64, 128}, gate_dim not in {32, 64, 128}, nb > 4096.
+ * Unsupported: gate->block not in {64, 128}, head_dim not in {64, 128},
+ * gate_dim not in {32, 64, 128}, nb > 4096.
  */
 seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate,
                       const void* q, const void* k, const float* wq, const float* wk,
@@ -166,8 +170,7 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate,
  * yields O = 0 and LSE = -inf.  When causal, list entries j > i end the row;
  * entries j >= nb always end it, and count is clamped to nb, so a malformed
  * mask cannot make the kernel read out of bounds.
- * Unsupported: block not in {64, 128} or not dividing seq_len, head_dim not in
- * {64, 128}.
+ * Unsupported: block not in {64, 128}, head_dim not in {64, 128}.
  */
 seer_status seer_bsattn(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
                         int32_t causal, float sm_scale, const void* q, const void* k,

@@ -154,10 +154,12 @@ def _check(status: int, where: str):
 
 @dataclass
 class BlockMask:
-    """Compacted block mask: idx[b, h, i, :count[b, h, i]] ascending (device tensors)."""
+    """Compacted block mask: idx[b, h, i, :count[b, h, i]] ascending (device tensors)
+    of `block`-token blocks (64 or 128; the last block may be partial)."""
     count: object  # int32 [B, Hq, nb]
     idx: object    # int16 storage of uint16 [B, Hq, nb, nb]
     dense: Optional[object] = None  # uint8 [B, Hq, nb, nb]
+    block: int = BLOCK
 
     @property
     def n_blocks(self) -> int:
@@ -179,11 +181,12 @@ class BlockMask:
 def alloc_mask(batch: int, heads_q: int, seq_len: int, device="cuda", dense: bool = False,
                block: int = BLOCK) -> BlockMask:
     torch = _torch()
-    nb = seq_len // block
+    nb = -(-seq_len // block)  # the last block may be partial
     return BlockMask(
         count=torch.empty((batch, heads_q, nb), dtype=torch.int32, device=device),
         idx=torch.empty((batch, heads_q, nb, nb), dtype=torch.int16, device=device),
-        dense=torch.empty((batch, heads_q, nb, nb), dtype=torch.uint8, device=device) if dense else None)
+        dense=torch.empty((batch, heads_q, nb, nb), dtype=torch.uint8, device=device) if dense else None,
+        block=block)
 
 
 # ---------------------------------------------------------------------------
@@ -230,6 +233,7 @@ def gate(q, k, wq, wk, *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
                    keep_first, keep_diag, w_per_head, rope_theta, block)
     if mask is None:
         mask = alloc_mask(q.shape[0], q.shape[1], q.shape[2], q.device, dense=dense_out, block=block)
+    mask.block = block
     need = lib().seer_gate_workspace_bytes(C.byref(d), C.byref(gd), int(logits_out is None))
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
@@ -265,7 +269,7 @@ def bsattn(q, k, v, mask: BlockMask, *, causal: bool = True, sm_scale: float = 0
         lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
     d = make_desc(q, k, v, out)
     ms = mask.struct()
-    block = q.shape[2] // mask.n_blocks if mask.n_blocks else BLOCK  # 64- or 128-token mask blocks
+    block = mask.block  # 64- or 128-token mask blocks
     if workspace is None:
         st = lib().seer_bsattn(C.byref(d), block, C.byref(ms), int(bool(causal)), float(sm_scale),
                                _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
@@ -314,7 +318,7 @@ def attn_gt(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
     one sized for `kv_groups` KV groups per launch (0: all) is allocated."""
     torch = _torch()
     B, Hq, S, _ = q.shape
-    nb = S // BLOCK
+    nb = -(-S // BLOCK)  # the last block may be partial
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:
@@ -364,6 +368,7 @@ def mask_from_dense(dense, heads_kv: int = 1, mask: Optional[BlockMask] = None,
     B, Hq, nb, _ = dense.shape
     if mask is None:
         mask = alloc_mask(B, Hq, nb * block, dense.device, block=block)
+    mask.block = block
     d = AttnDesc()
     d.batch, d.heads_q, d.heads_kv, d.seq_len, d.head_dim, d.dtype = B, Hq, heads_kv, nb * block, 128, BF16
     ms = mask.struct()

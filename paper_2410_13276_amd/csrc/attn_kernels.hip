@@ -169,7 +169,7 @@ __device__ __forceinline__ RowList<SPARSE> make_list(const AttnArgs& a, const Ta
   const int64_t row = ((int64_t)t.b * a.heads_q + t.h) * a.n_blocks + t.i;
   if (SPARSE) {
     const int sh = a.mask_shift;
-    const int nbm = a.n_blocks >> sh;  // blocks of the mask
+    const int nbm = a.mask_blocks;  // blocks of the mask
     const int64_t mrow = ((int64_t)t.b * a.heads_q + t.h) * nbm + (t.i >> sh);
     L.sh = sh;
     L.idx = a.idx + mrow * nbm;
@@ -328,6 +328,25 @@ __device__ __forceinline__ void load_tile_lds(uint32_t lds, const uint16_t* __re
     dma16(lds + 1024u * (2 * e + wave_u), tile + (int64_t)(128 * e / Lay::CPR) * ss, off[e & 1]);
 }
 
+// The last tile of a sequence that ends inside it: rows past the end are read
+// from the last row instead (finite data, masked or discarded later), so no
+// load leaves the tensor.  Row offsets are per lane and per load here.
+template <int D, bool IS_V>
+__device__ __forceinline__ void load_tile_lds_clamped(uint32_t lds, const uint16_t* __restrict__ tile,
+                                                      int ss, int wave, int wave_u, int lane,
+                                                      int rows_valid) {
+  using Lay = Bf16Layout<D>;
+  const int ql = 64 * wave + lane;
+  const int pc = ql % Lay::CPR;
+#pragma unroll
+  for (int e = 0; e < Lay::LOADS; ++e) {
+    const int r = 128 * e / Lay::CPR + ql / Lay::CPR;  // the LDS row this lane fills
+    const int gc = pc ^ (IS_V ? Lay::fv(r) : Lay::fk(r));
+    const int rr = min(r, rows_valid - 1);
+    dma16(lds + 1024u * (2 * e + wave_u), tile, (uint32_t)((rr * ss + 8 * gc) * 2));
+  }
+}
+
 // Sparse rows read their key-block list through a 256-entry LDS window, so the
 // loop issues no vector-memory loads of its own (whose waits would also drain
 // the tile loads in flight).
@@ -354,7 +373,10 @@ constexpr int kListChunk = 256;
 // With SPLIT the workgroup computes one key range of its row and stores the
 // normalised partial output (bf16) and its log2-domain log-sum-exp in the
 // range's partial slot; split_merge_kernel combines the slots afterwards.
-template <int D, bool SPARSE, bool SPLIT>
+//
+// RAGGED: the sequence ends inside its last tile (the clamped loads and the
+// key mask past the end exist only in that instantiation).
+template <int D, bool SPARSE, bool SPLIT, bool RAGGED>
 __global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_bf16_kernel(KernelArgs ka) {
   using Lay = Bf16Layout<D>;
@@ -383,12 +405,17 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   const uint16_t* vp = static_cast<const uint16_t*>(a.v.ptr) + t.b * a.v.sb + g * a.v.sh;
   const int64_t ktile = 64 * a.k.ss, vtile = 64 * a.v.ss;
 
-  // Q^T operand: lane holds query q0 + col, features 16ks + 8hf .. +7
+  // Q^T operand: lane holds query q0 + col, features 16ks + 8hf .. +7 (rows past
+  // the end of the sequence read its last row and are never stored)
+  const int S = a.seq_len;
   const int qrow = 64 * t.i + 32 * wave + col;
+  const int qrow_c = min(qrow, S - 1);
+  const int n_last = S - 64 * (a.n_blocks - 1);  // rows of the last tile
+  constexpr bool ragged = RAGGED;
   bf16x8 qf[D / 16];
 #pragma unroll
   for (int ks = 0; ks < D / 16; ++ks)
-    qf[ks] = *reinterpret_cast<const bf16x8*>(qp + (int64_t)qrow * a.q.ss + 16 * ks + 8 * hf);
+    qf[ks] = *reinterpret_cast<const bf16x8*>(qp + (int64_t)qrow_c * a.q.ss + 16 * ks + 8 * hf);
 
   f32x16 acc[D / 32];
 #pragma unroll
@@ -462,16 +489,29 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     }
   };
 
+  auto load_k = [&](int jt) {
+    if (RAGGED && jt == a.n_blocks - 1)
+      load_tile_lds_clamped<D, false>(sK_a, kp + jt * ktile, kss, wave, wave_u, lane, n_last);
+    else
+      load_tile_lds<D>(sK_a, kp + jt * ktile, kss, wave_u, koffd);
+  };
+  auto load_v = [&](int jt) {
+    if (RAGGED && jt == a.n_blocks - 1)
+      load_tile_lds_clamped<D, true>(sV_a, vp + jt * vtile, vss, wave, wave_u, lane, n_last);
+    else
+      load_tile_lds<D>(sV_a, vp + jt * vtile, vss, wave_u, voffd);
+  };
+
   f32x16 sA[2], sB[2];
   if (j >= 0) {
-    load_tile_lds<D>(sK_a, kp + j * ktile, kss, wave_u, koffd);
-    load_tile_lds<D>(sV_a, vp + j * vtile, vss, wave_u, voffd);
+    load_k(j);
+    load_v(j);
   }
   wait_loads();  // also retires the Q loads: nothing the loop body waits on is pending
   __syncthreads();
   if (j >= 0) s_product(sA);
   __syncthreads();  // K_j consumed
-  if (jn >= 0) load_tile_lds<D>(sK_a, kp + jn * ktile, kss, wave_u, koffd);
+  if (jn >= 0) load_k(jn);
   wait_loads();
   __syncthreads();  // K_jn (and V_j) visible
 
@@ -491,14 +531,19 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
       }
       jnn = entry(n + 2);
     }
-    if (a.causal && j == t.i) {  // diagonal tile: key kl visible to query ql iff kl <= ql
+    // diagonal tile: key kl visible to query ql iff kl <= ql.  Without causality
+    // the last tile of a sequence ending inside it hides its keys past the end
+    // (with causality they are already hidden from every real query).
+    const bool diag = a.causal && j == t.i;
+    const bool tail = ragged && !a.causal && j == a.n_blocks - 1;
+    if (diag || tail) {
       const int ql = 32 * wave + col;
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kl = 32 * mt + 8 * (e / 4) + 4 * hf + (e % 4);
-          if (kl > ql) sc[mt][e] = -INFINITY;
+          if ((diag && kl > ql) || (tail && kl >= n_last)) sc[mt][e] = -INFINITY;
         }
     }
     // online softmax (lazy rescale)
@@ -559,7 +604,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     // a SIMD, the one feeding the matrix core issues first (measured: sparse
     // 128k 19.8 -> 18.3 ms, dense split -1%)
     __builtin_amdgcn_s_setprio(2);
-    if (jnn >= 0) load_tile_lds<D>(sK_a, kp + jnn * ktile, kss, wave_u, koffd);
+    if (jnn >= 0) load_k(jnn);
     // ground truth: this tile's row max (Eq. 5), completed with the K load by barrier E
     if (pool && hf == 0) rrow[(int64_t)j * 64 + 32 * wave + col] = mloc;
 
@@ -595,7 +640,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     wait_loads();
     __builtin_amdgcn_s_setprio(0);
     __syncthreads();  // E: V_j consumed, K_jnn visible
-    if (jn >= 0) load_tile_lds<D>(sV_a, vp + jn * vtile, vss, wave_u, voffd);
+    if (jn >= 0) load_v(jn);
     j = jn;
     jn = jnn;
     ++n;
@@ -637,21 +682,24 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     op = static_cast<uint16_t*>(a.o) + t.b * a.osb + t.h * a.osh + (int64_t)64 * t.i * a.oss;
     ors = a.oss;
   }
+  const int rows_out = (SPLIT || !RAGGED) ? 64 : min(64, S - 64 * t.i);  // rows past the end are not stored
 #pragma unroll
   for (int e = 0; e < 64 * Lay::CPR / 128; ++e) {
     const int q = tid + 128 * e;
     const int r = q / Lay::CPR, cc = q % Lay::CPR;
-    *reinterpret_cast<u32x4*>(op + (int64_t)r * ors + 8 * cc) =
-        *reinterpret_cast<const u32x4*>(sO + r * Lay::OSTR + 8 * cc);
+    if (r < rows_out)
+      *reinterpret_cast<u32x4*>(op + (int64_t)r * ors + 8 * cc) =
+          *reinterpret_cast<const u32x4*>(sO + r * Lay::OSTR + 8 * cc);
   }
   if (SPLIT) {
     if (hf == 0) a.part_lse[slot * 64 + ql] = (l_tot > 0.f) ? m_run * c + __log2f(l_tot) : -INFINITY;
-  } else if (a.lse && hf == 0) {
+  } else if (a.lse && hf == 0 && qrow < S) {
     const float lse = (l_tot > 0.f) ? m_run * a.scale + __logf(l_tot) : -INFINITY;
-    a.lse[((int64_t)t.b * a.heads_q + t.h) * (int64_t)a.n_blocks * 64 + qrow] = lse;
+    a.lse[((int64_t)t.b * a.heads_q + t.h) * (int64_t)S + qrow] = lse;
   }
   if (pool) {
-    if (hf == 0) sL2[ql] = (l_tot > 0.f) ? m_run * c + __log2f(l_tot) : INFINITY;
+    // padding rows take no part in the column max
+    if (hf == 0) sL2[ql] = (l_tot > 0.f && qrow < S) ? m_run * c + __log2f(l_tot) : INFINITY;
     wait_loads();  // the row-max stores of this workgroup have completed
     __syncthreads();
     pool_epilogue(rrow, sL2, c, list.n, a.n_blocks, a.gt + trow * a.n_blocks, tid, 128);
@@ -683,11 +731,15 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
   const float* kp = static_cast<const float*>(a.k.ptr) + t.b * a.k.sb + g * a.k.sh;
   const float* vp = static_cast<const float*>(a.v.ptr) + t.b * a.v.sb + g * a.v.sh;
 
+  const int S = a.seq_len;
   const int qrow = 64 * t.i + 32 * wave + col;
+  const int qrow_c = min(qrow, S - 1);  // rows past the end read the last row, never stored
+  const int n_last = S - 64 * (a.n_blocks - 1);
+  const bool ragged = n_last < 64;
   f32x4 qf[D / 8];  // features 8u + 4hf .. +3 of this lane's query
 #pragma unroll
   for (int u = 0; u < D / 8; ++u)
-    qf[u] = *reinterpret_cast<const f32x4*>(qp + (int64_t)qrow * a.q.ss + 8 * u + 4 * hf);
+    qf[u] = *reinterpret_cast<const f32x4*>(qp + (int64_t)qrow_c * a.q.ss + 8 * u + 4 * hf);
 
   f32x16 acc[D / 32];
 #pragma unroll
@@ -719,10 +771,11 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
     for (int e = 0; e < 64 * CPR / 128; ++e) {
       const int q = tid + 128 * e;
       const int key = q / CPR, cc = q % CPR;
+      const int krow = min(64 * j + key, S - 1);  // clamped inside the last tile
       *reinterpret_cast<f32x4*>(sK + key * KS + 4 * cc) =
-          *reinterpret_cast<const f32x4*>(kp + (int64_t)(64 * j + key) * a.k.ss + 4 * cc);
+          *reinterpret_cast<const f32x4*>(kp + (int64_t)krow * a.k.ss + 4 * cc);
       *reinterpret_cast<f32x4*>(sV + key * VS + 4 * cc) =
-          *reinterpret_cast<const f32x4*>(vp + (int64_t)(64 * j + key) * a.v.ss + 4 * cc);
+          *reinterpret_cast<const f32x4*>(vp + (int64_t)krow * a.v.ss + 4 * cc);
     }
     __syncthreads();
 
@@ -739,14 +792,16 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
           s[mt] = __builtin_amdgcn_mfma_f32_32x32x2f32(kf[vv], qf[u][vv], s[mt], 0, 0, 0);
       }
     }
-    if (a.causal && j == t.i) {
+    const bool diag = a.causal && j == t.i;
+    const bool tail = ragged && !a.causal && j == a.n_blocks - 1;
+    if (diag || tail) {
       const int ql = 32 * wave + col;
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int kl = 32 * mt + 8 * (e / 4) + 4 * hf + (e % 4);
-          if (kl > ql) s[mt][e] = -INFINITY;
+          if ((diag && kl > ql) || (tail && kl >= n_last)) s[mt][e] = -INFINITY;
         }
     }
     float rmax;
@@ -773,21 +828,23 @@ __global__ __launch_bounds__(128) void attn_fwd_f32_kernel(KernelArgs ka, int sp
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = (l_tot > 0.f) ? 1.0f / l_tot : 0.f;
   float* op = static_cast<float*>(a.o) + t.b * a.osb + t.h * a.osh + (int64_t)qrow * a.oss;
+  if (qrow < S) {
 #pragma unroll
-  for (int dt = 0; dt < D / 32; ++dt)
+    for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      f32x4 o4;
+      for (int jj = 0; jj < 4; ++jj) {
+        f32x4 o4;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) o4[r] = acc[dt][4 * jj + r] * inv;
-      *reinterpret_cast<f32x4*>(op + 32 * dt + 8 * jj + 4 * hf) = o4;
-    }
-  if (a.lse && hf == 0) {
+        for (int r = 0; r < 4; ++r) o4[r] = acc[dt][4 * jj + r] * inv;
+        *reinterpret_cast<f32x4*>(op + 32 * dt + 8 * jj + 4 * hf) = o4;
+      }
+  }
+  if (a.lse && hf == 0 && qrow < S) {
     const float lse = (l_tot > 0.f) ? m_run * a.scale + __logf(l_tot) : -INFINITY;
-    a.lse[((int64_t)t.b * a.heads_q + t.h) * (int64_t)a.n_blocks * 64 + qrow] = lse;
+    a.lse[((int64_t)t.b * a.heads_q + t.h) * (int64_t)S + qrow] = lse;
   }
   if (pool) {
-    if (hf == 0) sL2[32 * wave + col] = (l_tot > 0.f) ? m_run * c + __log2f(l_tot) : INFINITY;
+    if (hf == 0) sL2[32 * wave + col] = (l_tot > 0.f && qrow < S) ? m_run * c + __log2f(l_tot) : INFINITY;
     __threadfence_block();
     __syncthreads();
     pool_epilogue(rrow, sL2, c, n_tiles, a.n_blocks, a.gt + trow * a.n_blocks, tid, 128);
@@ -879,6 +936,7 @@ __global__ __launch_bounds__(256) void split_merge_kernel(AttnArgs a) {
     }
   }
   const float inv = sum > 0.f ? 1.0f / sum : 0.f;
+  if (64 * i + q >= a.seq_len) return;  // padding row of a partial last tile
   uint16_t* dst = static_cast<uint16_t*>(a.o) + b * a.osb + h * a.osh + (int64_t)(64 * i + q) * a.oss + f0;
 #pragma unroll
   for (int u = 0; u < F / 8; ++u) {
@@ -888,7 +946,7 @@ __global__ __launch_bounds__(256) void split_merge_kernel(AttnArgs a) {
     *reinterpret_cast<bf16x8*>(dst + 8 * u) = o8;
   }
   if (a.lse && threadIdx.x % 4 == 0)
-    a.lse[bh * nb * 64 + 64 * i + q] = sum > 0.f ? (mx + __log2f(sum)) * 0.6931471805599453f : -INFINITY;
+    a.lse[bh * a.seq_len + 64 * i + q] = sum > 0.f ? (mx + __log2f(sum)) * 0.6931471805599453f : -INFINITY;
 }
 
 // Groups per phase: the largest power of two whose K + V stay within 64 MiB
@@ -959,7 +1017,7 @@ int64_t split_slots_per_head(int n_blocks, int w) {
   return n_blocks + w * q * (q - 1) / 2 + r * q;
 }
 
-template <int D>
+template <int D, bool RAGGED>
 static void launch_split(const KernelArgs& ka, bool sparse, hipStream_t s) {
   const AttnArgs& a = ka.a;
   const int64_t rows = (int64_t)a.batch * a.heads_q * a.n_blocks;
@@ -969,8 +1027,8 @@ static void launch_split(const KernelArgs& ka, bool sparse, hipStream_t s) {
   const int64_t units = a.split_parts == 16 ? (int64_t)a.batch * a.heads_kv : (int64_t)a.batch * a.heads_kv / 2;
   const int64_t tasks = 8 * units * (a.heads_q / a.heads_kv) * (2 * a.n_blocks - (a.split_parts - 1) * a.split_w);
   dim3 grid((unsigned)tasks), block(128);
-  if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, true, true>), grid, block, 0, s, ka);
-  else hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, false, true>), grid, block, 0, s, ka);
+  if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, true, true, RAGGED>), grid, block, 0, s, ka);
+  else hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, false, true, RAGGED>), grid, block, 0, s, ka);
   hipLaunchKernelGGL(split_merge_kernel<D>, dim3((unsigned)rows), dim3(256), 0, s, a);
 }
 
@@ -985,7 +1043,10 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   dim3 grid((unsigned)total), block(128);
   const bool sparse = a.count != nullptr;
   const bool pool = a.gt != nullptr;
+  const bool ragged = a.seq_len % 64 != 0;  // the last tile is partial
   if ((sparse && pool) || (pool && !a.pool_r)) return hipErrorInvalidValue;
+  if (a.seq_len <= 0 || (a.n_blocks - 1) * 64 >= a.seq_len || a.n_blocks * 64 < a.seq_len)
+    return hipErrorInvalidValue;  // n_blocks must be ceil(seq_len / 64)
   if (a.split_w > 0) {
     // the shape must be the one split_width accepted, with every buffer present
     const int P = a.split_parts;
@@ -994,18 +1055,34 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
         (P == 8 && (a.batch * a.heads_kv) % 2 != 0) || !a.part_lse || !a.part_o ||
         (sparse && !a.split_bounds) || a.split_slots != split_slots_per_head(a.n_blocks, a.split_w))
       return hipErrorInvalidValue;
-    if (a.head_dim == 128) launch_split<128>(ka, sparse, s);
-    else if (a.head_dim == 64) launch_split<64>(ka, sparse, s);
-    else return hipErrorInvalidValue;
+    if (a.head_dim == 128) {
+      if (ragged) launch_split<128, true>(ka, sparse, s);
+      else launch_split<128, false>(ka, sparse, s);
+    } else if (a.head_dim == 64) {
+      if (ragged) launch_split<64, true>(ka, sparse, s);
+      else launch_split<64, false>(ka, sparse, s);
+    } else {
+      return hipErrorInvalidValue;
+    }
     return hipGetLastError();
   }
   if (a.bf16) {
     if (a.head_dim == 128) {
-      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true, false>), grid, block, 0, s, ka);
-      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false, false>), grid, block, 0, s, ka);
+      if (ragged) {
+        if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true, false, true>), grid, block, 0, s, ka);
+        else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false, false, true>), grid, block, 0, s, ka);
+      } else {
+        if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true, false, false>), grid, block, 0, s, ka);
+        else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, false, false, false>), grid, block, 0, s, ka);
+      }
     } else if (a.head_dim == 64) {
-      if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true, false>), grid, block, 0, s, ka);
-      else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false, false>), grid, block, 0, s, ka);
+      if (ragged) {
+        if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true, false, true>), grid, block, 0, s, ka);
+        else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false, false, true>), grid, block, 0, s, ka);
+      } else {
+        if (sparse) hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, true, false, false>), grid, block, 0, s, ka);
+        else hipLaunchKernelGGL((attn_fwd_bf16_kernel<64, false, false, false>), grid, block, 0, s, ka);
+      }
     } else {
       return hipErrorInvalidValue;
     }

@@ -51,7 +51,7 @@ struct Load16<uint16_t> {
 // (each thread owns one 16-byte column chunk of one block and walks its 64 rows)
 // and then projects the R pooled rows through the head's gate weights.
 template <typename T, int D, int DG, bool IS_K, int BLK>
-__device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t ss, int nb,
+__device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t ss, int nb, int seq_len,
                                                const float* __restrict__ W,
                                                float* __restrict__ out, float* smem,
                                                float* srot, double rope_base,
@@ -77,8 +77,9 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
       mn[e] = INFINITY;
     }
     const T* base = x + (int64_t)blk * BLK * ss + c * EPL;
+    const int nrow = min(BLK, seq_len - blk * BLK);  // the last block may be partial
 #pragma unroll 8
-    for (int row = 0; row < BLK; ++row) {
+    for (int row = 0; row < nrow; ++row) {
       float v[EPL];
       Load16<T>::get(base + row * ss, v);
 #pragma unroll
@@ -93,7 +94,7 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
     float* prow = smem + r * WIDTH + c * EPL;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      const float avg = sum[e] * (1.0f / BLK);
+      const float avg = sum[e] / (float)nrow;
       if (IS_K) {
         prow[e] = mx[e];
         prow[D + e] = mn[e];
@@ -178,14 +179,14 @@ __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
     const T* x = static_cast<const T*>(a.q.ptr) + b * a.q.sb + h * a.q.sh;
     float* out = a.qg + ((int64_t)b * a.heads_q + h) * a.n_blocks * DG;
     float* po = a.qp ? a.qp + ((int64_t)b * a.heads_q + h) * a.n_blocks * D : nullptr;
-    pool_proj_head<T, D, DG, false, BLK>(x, a.q.ss, a.n_blocks, a.wq + h * a.wq_head_stride, out, smem, srot,
+    pool_proj_head<T, D, DG, false, BLK>(x, a.q.ss, a.n_blocks, a.seq_len, a.wq + h * a.wq_head_stride, out, smem, srot,
                                     a.rope_base, po);
   } else {
     const int g = slot - a.heads_q;
     const T* x = static_cast<const T*>(a.k.ptr) + b * a.k.sb + g * a.k.sh;
     float* out = a.kg + ((int64_t)b * a.heads_kv + g) * a.n_blocks * DG;
     float* po = a.kp ? a.kp + ((int64_t)b * a.heads_kv + g) * a.n_blocks * 3 * D : nullptr;
-    pool_proj_head<T, D, DG, true, BLK>(x, a.k.ss, a.n_blocks, a.wk + g * a.wk_head_stride, out, smem, srot,
+    pool_proj_head<T, D, DG, true, BLK>(x, a.k.ss, a.n_blocks, a.seq_len, a.wk + g * a.wk_head_stride, out, smem, srot,
                                    a.rope_base, po);
   }
 }

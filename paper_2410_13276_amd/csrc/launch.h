@@ -25,6 +25,7 @@ struct PoolProjArgs {
   float* qp;  // optional pooled Q [B][Hq][nb][D] (nullptr: not stored)
   float* kp;  // optional pooled K [B][Hkv][nb][3D]
   int block;  // tokens per gate block: 64 or 128
+  int seq_len;  // tokens; the last block holds seq_len - (n_blocks - 1) block of them
 };
 
 struct GateLogitsArgs {
@@ -62,7 +63,9 @@ struct AttnArgs {
   void* o;
   int64_t osb, osh, oss;
   float* lse;  // [B][Hq][S] or nullptr
-  int batch, heads_q, heads_kv, n_blocks, head_dim;
+  int batch, heads_q, heads_kv, n_blocks, head_dim;  // n_blocks: 64-token tiles, ceil(S / 64)
+  int seq_len;       // S; rows past it in the last tile are padding (clamped reads, no writes)
+  int mask_blocks;   // blocks of the mask (ceil(S / 64) or ceil(S / 128)), 0 when dense
   bool bf16;
   bool causal;
   float scale;

@@ -22,6 +22,9 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 size_t elem_size(int32_t dtype) { return dtype == SEER_F32 ? 4 : 2; }
 
+// 64-token attention tiles covering seq_len (the last one may be partial).
+int64_t tiles(int seq_len) { return (seq_len + SEER_BLOCK - 1) / SEER_BLOCK; }
+
 // Checks shared by every call that takes a seer_attn_desc.  `tensors` selects
 // which stride triples are used: bit 0 q, 1 k, 2 v, 3 o.
 seer_status check_desc(const seer_attn_desc* d, int tensors) {
@@ -31,7 +34,6 @@ seer_status check_desc(const seer_attn_desc* d, int tensors) {
   if (d->heads_q % d->heads_kv != 0) return SEER_ERR_INVALID_ARG;
   if (d->dtype != SEER_BF16 && d->dtype != SEER_F32) return SEER_ERR_INVALID_ARG;
   if (d->head_dim != 64 && d->head_dim != 128) return SEER_ERR_UNSUPPORTED;
-  if (d->seq_len % SEER_BLOCK != 0) return SEER_ERR_UNSUPPORTED;
   const int64_t vec = 16 / (int64_t)elem_size(d->dtype);  // elements per 16-byte access
   const int64_t* st[4] = {d->q_stride, d->k_stride, d->v_stride, d->o_stride};
   for (int t = 0; t < 4; ++t) {
@@ -40,12 +42,15 @@ seer_status check_desc(const seer_attn_desc* d, int tensors) {
       if (st[t][e] < 0 || st[t][e] % vec != 0) return SEER_ERR_UNSUPPORTED;
     if (st[t][2] < d->head_dim) return SEER_ERR_INVALID_ARG;  // rows may not overlap
   }
-  const int64_t tasks = (int64_t)d->batch * d->heads_q * (d->seq_len / SEER_BLOCK);
+  const int64_t tasks = (int64_t)d->batch * d->heads_q * tiles(d->seq_len);
   if (tasks > INT32_MAX / 2) return SEER_ERR_UNSUPPORTED;
   return SEER_OK;
 }
 
 seer::TensorView view(const void* p, const int64_t* st) { return {p, st[0], st[1], st[2]}; }
+
+// Blocks of `block` tokens covering seq_len (the last one may be partial).
+int blocks_of(int seq_len, int block) { return (seq_len + block - 1) / block; }
 
 // Checks of the gate shape and weights (shared by seer_gate and seer_gate_distill).
 seer_status check_gate_common(const seer_attn_desc* d, const seer_gate_desc* g) {
@@ -53,9 +58,8 @@ seer_status check_gate_common(const seer_attn_desc* d, const seer_gate_desc* g) 
   if (s != SEER_OK) return s;
   if (!g) return SEER_ERR_INVALID_ARG;
   if (g->block != 64 && g->block != 128) return SEER_ERR_UNSUPPORTED;
-  if (d->seq_len % g->block != 0) return SEER_ERR_UNSUPPORTED;
   if (g->gate_dim != 32 && g->gate_dim != 64 && g->gate_dim != 128) return SEER_ERR_UNSUPPORTED;
-  if (d->seq_len / g->block > 4096) return SEER_ERR_UNSUPPORTED;
+  if (blocks_of(d->seq_len, g->block) > 4096) return SEER_ERR_UNSUPPORTED;
   if (!(g->rope_theta >= 0.0) || std::isinf(g->rope_theta)) return SEER_ERR_INVALID_ARG;
   return SEER_OK;
 }
@@ -84,7 +88,7 @@ struct GateLayout {
 };
 
 GateLayout gate_layout(const seer_attn_desc* d, const seer_gate_desc* g, bool logits_in_ws) {
-  const size_t nb = (size_t)(d->seq_len / g->block);
+  const size_t nb = (size_t)blocks_of(d->seq_len, g->block);
   GateLayout L;
   L.qg = 0;
   L.kg = round_up((size_t)d->batch * d->heads_q * nb * g->gate_dim * 4);
@@ -100,7 +104,7 @@ struct DistillLayout {
 };
 
 DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g) {
-  const size_t nb = (size_t)(d->seq_len / g->block);
+  const size_t nb = (size_t)blocks_of(d->seq_len, g->block);
   const size_t B = d->batch, Hq = d->heads_q, Hkv = d->heads_kv, D = d->head_dim, Dg = g->gate_dim;
   DistillLayout L;
   size_t off = 0;
@@ -147,7 +151,9 @@ seer::AttnArgs attn_args(const seer_attn_desc* desc, int32_t causal, float sm_sc
   a.batch = desc->batch;
   a.heads_q = desc->heads_q;
   a.heads_kv = desc->heads_kv;
-  a.n_blocks = desc->seq_len / SEER_BLOCK;
+  a.n_blocks = blocks_of(desc->seq_len, SEER_BLOCK);
+  a.seq_len = desc->seq_len;
+  a.mask_blocks = 0;
   a.head_dim = desc->head_dim;
   a.bf16 = desc->dtype == SEER_BF16;
   a.causal = causal != 0;
@@ -176,7 +182,7 @@ struct SplitLayout {
 
 SplitLayout split_layout(const seer_attn_desc* d, int parts) {
   SplitLayout L{};
-  const int nb = d->seq_len / SEER_BLOCK;
+  const int nb = blocks_of(d->seq_len, SEER_BLOCK);
   if (parts == 0) return L;
   L.parts = parts;
   L.w = nb / parts;
@@ -190,13 +196,13 @@ SplitLayout split_layout(const seer_attn_desc* d, int parts) {
 }
 
 int split_parts_for(const seer_attn_desc* d, int32_t causal, bool sparse) {
-  return seer::split_parts(d->seq_len / SEER_BLOCK, d->batch * d->heads_kv, causal != 0,
+  return seer::split_parts(blocks_of(d->seq_len, SEER_BLOCK), d->batch * d->heads_kv, causal != 0,
                            d->dtype == SEER_BF16, sparse);
 }
 
 // Bytes of row-max workspace per query head: nb key tiles x 64 queries per query block.
 size_t gt_head_bytes(const seer_attn_desc* d) {
-  const size_t nb = (size_t)(d->seq_len / SEER_BLOCK);
+  const size_t nb = (size_t)blocks_of(d->seq_len, SEER_BLOCK);
   return nb * nb * 64 * sizeof(float);
 }
 
@@ -225,9 +231,9 @@ size_t seer_gate_workspace_bytes(const seer_attn_desc* desc, const seer_gate_des
 
 size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block) {
   if (!desc || (block != 64 && block != 128) || desc->batch <= 0 || desc->heads_q <= 0 ||
-      desc->seq_len <= 0 || desc->seq_len % block != 0)
+      desc->seq_len <= 0)
     return 0;
-  const size_t nb = (size_t)(desc->seq_len / block);
+  const size_t nb = (size_t)blocks_of(desc->seq_len, block);
   return (size_t)desc->batch * desc->heads_q * nb * nb;
 }
 
@@ -238,7 +244,7 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   if (s != SEER_OK) return s;
   if (!q || !k || !wq || !wk || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
-  const int nb = desc->seq_len / gate->block;
+  const int nb = blocks_of(desc->seq_len, gate->block);
   if (out->n_blocks != nb) return SEER_ERR_INVALID_ARG;
   const bool logits_in_ws = logits_out == nullptr;
   const GateLayout L = gate_layout(desc, gate, logits_in_ws);
@@ -272,6 +278,7 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   pa.qp = nullptr;
   pa.kp = nullptr;
   pa.block = gate->block;
+  pa.seq_len = desc->seq_len;
   if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
 
   seer::GateLogitsArgs la;
@@ -313,8 +320,7 @@ static seer_status attn_common(const seer_attn_desc* desc, int32_t block, const 
   if (s != SEER_OK) return s;
   if (mask) {
     if (block != 64 && block != 128) return SEER_ERR_UNSUPPORTED;
-    if (desc->seq_len % block != 0) return SEER_ERR_UNSUPPORTED;
-    const int nbm = desc->seq_len / block;
+    const int nbm = blocks_of(desc->seq_len, block);
     if (!mask->count || !mask->idx || mask->n_blocks != nbm) return SEER_ERR_INVALID_ARG;
     if (nbm > 65536) return SEER_ERR_UNSUPPORTED;
   }
@@ -322,6 +328,7 @@ static seer_status attn_common(const seer_attn_desc* desc, int32_t block, const 
   a.count = mask ? mask->count : nullptr;
   a.idx = mask ? mask->idx : nullptr;
   a.mask_shift = (mask && block == 128) ? 1 : 0;
+  a.mask_blocks = mask ? mask->n_blocks : 0;
   if (workspace && a.mask_shift == 0) {  // the split runs on 64-token masks
     if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
     const SplitLayout L = split_layout(desc, split_parts_for(desc, causal, mask != nullptr));
@@ -377,8 +384,8 @@ seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, cons
                                  seer_block_mask* out, void* stream) {
   if (!desc || !dense || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
   if (desc->batch <= 0 || desc->heads_q <= 0 || desc->seq_len <= 0) return SEER_ERR_INVALID_ARG;
-  if ((block != 64 && block != 128) || desc->seq_len % block != 0) return SEER_ERR_UNSUPPORTED;
-  const int nb = desc->seq_len / block;
+  if (block != 64 && block != 128) return SEER_ERR_UNSUPPORTED;
+  const int nb = blocks_of(desc->seq_len, block);
   if (out->n_blocks != nb) return SEER_ERR_INVALID_ARG;
   if (nb > 4096) return SEER_ERR_UNSUPPORTED;
   seer::MaskFromDenseArgs a;
@@ -410,7 +417,7 @@ seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t caus
   if (!workspace || workspace_bytes < group_bytes) return SEER_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const int64_t nb = desc->seq_len / SEER_BLOCK;
+  const int64_t nb = blocks_of(desc->seq_len, SEER_BLOCK);
   const int64_t all = (int64_t)desc->batch * desc->heads_kv;
   seer::AttnArgs a = attn_args(desc, causal, sm_scale, q, k, v, o, lse);
   a.pool_r = static_cast<float*>(workspace);
@@ -434,7 +441,7 @@ seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t caus
       c.v.ptr = static_cast<const char*>(v) + qe * (b * desc->v_stride[0] + g0 * desc->v_stride[1]);
       c.o = static_cast<char*>(o) + qe * (b * desc->o_stride[0] + h0 * desc->o_stride[1]);
       const int64_t hrow = (int64_t)b * desc->heads_q + h0;  // first query head of the run
-      c.lse = lse ? lse + hrow * nb * 64 : nullptr;
+      c.lse = lse ? lse + hrow * desc->seq_len : nullptr;
       c.gt = gt + hrow * nb * nb;
       if ((s = from_hip(seer::launch_attn(c, st))) != SEER_OK) return s;
     }
@@ -470,7 +477,7 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int B = desc->batch, Hq = desc->heads_q, Hkv = desc->heads_kv, D = desc->head_dim;
   const int Dg = gate->gate_dim, G = Hq / Hkv;
-  const int nb = desc->seq_len / gate->block;
+  const int nb = blocks_of(desc->seq_len, gate->block);
   const double rope_base = gate->rope_theta > 0.0 ? gate->rope_theta / gate->block : 0.0;
   const float rsqrt_dg = (float)(1.0 / std::sqrt((double)Dg));
 
@@ -495,6 +502,7 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   pa.qp = qp;
   pa.kp = kp;
   pa.block = gate->block;
+  pa.seq_len = desc->seq_len;
   if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
 
   seer::GateLogitsArgs la;

@@ -127,11 +127,12 @@ def check_mask(gpu_dense: np.ndarray, gpu_count: np.ndarray, orc: dict, topk: bo
     return stats
 
 
-def upload_mask(count: np.ndarray, idx: np.ndarray, device="cuda"):
+def upload_mask(count: np.ndarray, idx: np.ndarray, device="cuda", block: int = 64):
     import torch
     import paper_2410_13276_amd as seer
     return seer.BlockMask(count=torch.from_numpy(np.ascontiguousarray(count, np.int32)).to(device),
-                          idx=torch.from_numpy(np.ascontiguousarray(idx).view(np.int16)).to(device))
+                          idx=torch.from_numpy(np.ascontiguousarray(idx).view(np.int16)).to(device),
+                          block=block)
 
 
 def sample_rows(B, Hq, nb, n, seed):

@@ -80,7 +80,7 @@ def test_workspace_size_formula():
 
 @pytest.mark.parametrize("field,value,status", [
     ("heads_kv", 3, seer.ERR_INVALID_ARG),     # heads_q % heads_kv != 0
-    ("seq_len", 1000, seer.ERR_UNSUPPORTED),   # not a multiple of 64
+    ("seq_len", 0, seer.ERR_INVALID_ARG),
     ("head_dim", 96, seer.ERR_UNSUPPORTED),
     ("dtype", 7, seer.ERR_INVALID_ARG),
     ("batch", 0, seer.ERR_INVALID_ARG),
@@ -229,8 +229,9 @@ def test_attention_ws_rejects_bad_args():
 
 def test_block_128_gate_and_mask_validation():
     L = seer.lib()
-    d = _desc(B=1, Hq=4, Hkv=2, S=1088, D=128)   # 1088 = 17 x 64: not a multiple of 128
-    assert _call_gate(d, _gate(block=128), mask_nb=8) == seer.ERR_UNSUPPORTED
+    d = _desc(B=1, Hq=4, Hkv=2, S=1088, D=128)   # 1088 = 8.5 x 128: 9 blocks, the last partial
+    assert _call_gate(d, _gate(block=128), mask_nb=8) == seer.ERR_INVALID_ARG
+    assert L.seer_mask_idx_elems(C.byref(d), 128) == 4 * 9 * 9
     d = _desc(B=1, Hq=4, Hkv=2, S=1024, D=128)
     assert _call_gate(d, _gate(block=128), mask_nb=16) == seer.ERR_INVALID_ARG  # mask must have 8 blocks
     g = _gate(block=128)
@@ -240,3 +241,15 @@ def test_block_128_gate_and_mask_validation():
     m = seer.BlockMaskStruct()
     m.n_blocks, m.count, m.idx, m.dense = 16, FAKE, FAKE, None
     assert L.seer_mask_from_dense(C.byref(d), 128, FAKE, C.byref(m), None) == seer.ERR_INVALID_ARG
+
+
+def test_partial_last_block_sizes():
+    """Sequences that are not a multiple of 64: ceil(S / block) blocks everywhere."""
+    L = seer.lib()
+    d, g = _desc(B=1, Hq=4, Hkv=2, S=1000, D=128), _gate()
+    up = lambda x: (x + 255) // 256 * 256
+    nb = 16  # ceil(1000 / 64)
+    assert L.seer_mask_idx_elems(C.byref(d), 64) == 4 * nb * nb
+    assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 0) == up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4)
+    assert L.seer_attn_gt_workspace_bytes(C.byref(d), 64, 0) == 4 * nb * nb * 64 * 4
+    assert _call_gate(d, g, mask_nb=15) == seer.ERR_INVALID_ARG

@@ -82,7 +82,7 @@ def test_bsattn_block128_parity(case, pattern):
     count, idx = lists_from_dense(om)
     O_ref, lse_ref = oracle.attn(q, k, v, block=BLK, mask=om)
     qd, kd, vd = (to_device(x) for x in (q, k, v))
-    m = upload_mask(count, idx)
+    m = upload_mask(count, idx, block=BLK)
     ws = torch.empty(max(1, seer.attn_workspace_bytes(qd, kd, vd)), dtype=torch.uint8, device="cuda")
     o, lse = seer.bsattn(qd, kd, vd, m, want_lse=True)
     o_ws, _ = seer.bsattn(qd, kd, vd, m, workspace=ws)  # a 128-token mask never splits
@@ -110,7 +110,7 @@ def test_block128_equals_expanded_64_mask():
     om[..., np.arange(nb), np.arange(nb)] = 1
     om64 = np.kron(om, np.ones((2, 2), np.uint8)) & np.tril(np.ones((2 * nb, 2 * nb), np.uint8))
     qd, kd, vd = (to_device(x) for x in (q, k, v))
-    o128, l128 = seer.bsattn(qd, kd, vd, upload_mask(*lists_from_dense(om)), want_lse=True)
+    o128, l128 = seer.bsattn(qd, kd, vd, upload_mask(*lists_from_dense(om), block=BLK), want_lse=True)
     o64, l64 = seer.bsattn(qd, kd, vd, upload_mask(*lists_from_dense(om64)), want_lse=True)
     torch.cuda.synchronize()
     assert torch.equal(o128.view(torch.int16), o64.view(torch.int16))
