@@ -234,8 +234,9 @@ def main() -> int:
     active_flops = flops_tile * active
     D = w.head_dim
     sparse_split = aws is not None and os.environ.get("SEER_SPLIT_SPARSE") == "1"
-    attn_kernels = (f"split_bounds_kernel + attn_fwd_bf16_kernel<{D}, true, true> + split_merge_kernel<{D}> "
-                    "(one seer_bsattn_ws call)" if sparse_split else f"attn_fwd_bf16_kernel<{D}, true, false>")
+    rg = "true" if w.seq_len % 64 else "false"  # partial last tile
+    attn_kernels = (f"split_bounds_kernel + attn_fwd_bf16_kernel<{D}, true, true, {rg}> + split_merge_kernel<{D}> "
+                    "(one seer_bsattn_ws call)" if sparse_split else f"attn_fwd_bf16_kernel<{D}, true, false, {rg}>")
     attn_tflops = active_flops / (attn_ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     speedup = dense_ms / attn_ms
