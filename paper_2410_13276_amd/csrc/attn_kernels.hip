@@ -1032,7 +1032,43 @@ static void launch_split(const KernelArgs& ka, bool sparse, hipStream_t s) {
   hipLaunchKernelGGL(split_merge_kernel<D>, dim3((unsigned)rows), dim3(256), 0, s, a);
 }
 
+static hipError_t launch_attn_one(const AttnArgs& a, hipStream_t s);
+
+// One launch per KV group when a phase of the task order holds a single group
+// (its K and V alone fill the phase's cache budget): the launch boundary keeps
+// every XCD on the same group's K and V.  Measured at 131072 tokens (sparse):
+// 8 launches 17.8 ms, one launch 18.1 ms.  Not for the split or pooling modes.
 hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
+  const int groups = a.batch * a.heads_kv;
+  if (a.split_w > 0 || a.gt != nullptr || groups <= 1 || make_map(a).gpp != 1)
+    return launch_attn_one(a, s);
+  const int G = a.heads_q / a.heads_kv;
+  const int64_t es = a.bf16 ? 2 : 4;
+  const int nbm = a.mask_blocks;
+  for (int b = 0; b < a.batch; ++b)
+    for (int g = 0; g < a.heads_kv; ++g) {
+      const int h0 = g * G;
+      AttnArgs c = a;
+      c.batch = 1;
+      c.heads_kv = 1;
+      c.heads_q = G;
+      c.q.ptr = static_cast<const char*>(a.q.ptr) + es * (b * a.q.sb + h0 * a.q.sh);
+      c.k.ptr = static_cast<const char*>(a.k.ptr) + es * (b * a.k.sb + g * a.k.sh);
+      c.v.ptr = static_cast<const char*>(a.v.ptr) + es * (b * a.v.sb + g * a.v.sh);
+      c.o = static_cast<char*>(a.o) + es * (b * a.osb + h0 * a.osh);
+      const int64_t hrow = (int64_t)b * a.heads_q + h0;  // first query head of the group
+      if (a.lse) c.lse = a.lse + hrow * a.seq_len;
+      if (a.count) {
+        c.count = a.count + hrow * nbm;
+        c.idx = a.idx + hrow * nbm * nbm;
+      }
+      const hipError_t e = launch_attn_one(c, s);
+      if (e != hipSuccess) return e;
+    }
+  return hipSuccess;
+}
+
+static hipError_t launch_attn_one(const AttnArgs& a, hipStream_t s) {
   KernelArgs ka;
   ka.a = a;
   ka.map = make_map(a);
