@@ -9,7 +9,8 @@
 //   gate_logits_kernel  Eq. 1: Qg Kg^T / sqrt(Dg) on the block-causal lower
 //                       triangle, fp32 MFMA (v_mfma_f32_32x32x2_f32), 64x64 tiles.
 //   select_kernel       Eq. 3 (TopK by exact radix select on order-preserving
-//                       keys, ties to the smaller block index) or Eq. 4 (strict
+//                       keys, 8-bit digits from a per-wavefront LDS histogram,
+//                       ties to the smaller block index) or Eq. 4 (strict
 //                       threshold on the row softmax), plus the always-kept first
 //                       and diagonal blocks; one wavefront per query-block row,
 //                       writing the ascending index list by ballot compaction.
@@ -317,6 +318,7 @@ __device__ __forceinline__ void emit_row(uint64_t sel, int nb, int64_t row, int3
 
 template <int MAXM>
 __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
+  __shared__ __attribute__((aligned(16))) uint32_t s_hist[4][256];  // per-wavefront digit histogram
   const int lane = threadIdx.x % kWave;
   const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
   const int nb = a.n_blocks;
@@ -377,28 +379,62 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
       uint32_t key[MAXM];
 #pragma unroll
       for (int m = 0; m < MAXM; ++m) key[m] = ((cand >> m) & 1) ? ordered_key(v[m]) : 0u;
-      // Largest T with #{candidates : key >= T} >= take, one bit at a time.  Once
-      // exactly `take` candidates lie at or above the current prefix, the
-      // selected set is fixed and the remaining bits cannot change it.
-      uint32_t T = 0;
-      int cntT = ncand;
-      for (int bit = 31; bit >= 0 && cntT != take; --bit) {
-        const uint32_t trial = T | (1u << bit);
-        int cnt = 0;
+      // T: the largest value with #{candidates : key >= T} >= take, found 8 bits
+      // at a time from a per-wavefront LDS histogram of the candidates that
+      // match the digits fixed so far.  `above` counts candidates whose fixed
+      // digits are already larger.  Once exactly `take` candidates lie at or
+      // above the current prefix the selected set is fixed (cntT == take).
+      // (Starting the digits below the bits all candidates share was measured
+      // slower: the extra reduction raised register use and cost occupancy.)
+      uint32_t* hist = s_hist[threadIdx.x / kWave];
+      uint32_t prefix = 0;
+      int above = 0;
+      int cntT = take + 1;  // != take until the set closes early
+      int shift = 0;
+      for (int d = 3; d >= 0; --d) {
+        const int sh = 8 * d;
+        *reinterpret_cast<u32x4*>(hist + 4 * lane) = u32x4{0u, 0u, 0u, 0u};
+        __builtin_amdgcn_wave_barrier();
 #pragma unroll
         for (int m = 0; m < MAXM; ++m)
-          if (m < M) cnt += __popcll(__ballot(((cand >> m) & 1) && key[m] >= trial));
-        if (cnt >= take) {
-          T = trial;
-          cntT = cnt;
+          if (m < M && ((cand >> m) & 1) && (d == 3 || (key[m] >> (sh + 8)) == prefix))
+            atomicAdd(hist + ((key[m] >> sh) & 255u), 1u);
+        __builtin_amdgcn_wave_barrier();
+        const u32x4 c = *reinterpret_cast<const u32x4*>(hist + 4 * lane);  // bins 4 lane .. +3
+        const int local = (int)(c[0] + c[1] + c[2] + c[3]);
+        int incl = local;  // candidates in the bins of this lane and every higher lane
+#pragma unroll
+        for (int off = 1; off < kWave; off <<= 1) {
+          const int t = __shfl_down(incl, off);
+          if (lane + off < kWave) incl += t;
+        }
+        // the target bin: the highest b with above + #{digit >= b} >= take
+        int run = above + (incl - local);
+        int found = -1, abv = 0, cb = 0;
+#pragma unroll
+        for (int e = 3; e >= 0; --e) {
+          if (found < 0 && run < take && run + (int)c[e] >= take) {
+            found = e;
+            abv = run;
+            cb = (int)c[e];
+          }
+          run += (int)c[e];
+        }
+        const uint64_t hit = __ballot(found >= 0);  // exactly one lane: bins are monotone
+        const int src = __builtin_ctzll(hit);
+        const int b = 4 * src + __shfl(found, src);
+        abv = __shfl(abv, src);
+        cb = __shfl(cb, src);
+        prefix = (d == 3) ? (uint32_t)b : ((prefix << 8) | (uint32_t)b);
+        above = abv;
+        if (abv + cb == take) {
+          cntT = take;
+          shift = sh;
+          break;
         }
       }
-      int gt = 0;
-      if (cntT != take) {
-#pragma unroll
-        for (int m = 0; m < MAXM; ++m)
-          if (m < M) gt += __popcll(__ballot(((cand >> m) & 1) && key[m] > T));
-      }
+      const uint32_t T = (cntT == take) ? (prefix << shift) : prefix;
+      const int gt = above;  // candidates with key > T (when the set did not close early)
       // everything >= T when the set closed early; otherwise everything > T
       // plus the (take - gt) smallest-index candidates tied at T
       const int need = (cntT == take) ? 0 : take - gt;
