@@ -33,6 +33,7 @@ import workload as W  # noqa: E402
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA (published)
 PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 MFMA (published)
 PEAK_HBM_GBS = 8000.0
+ROPE_BASE = 500000.0         # Llama 3.1's RoPE base, for the gate's block-level RoPE
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_traffic.json")
 ATTN_SRC = os.path.join(ROOT, "paper_2410_13276_amd", "csrc", "attn_kernels.hip")
 
@@ -109,6 +110,8 @@ def main() -> int:
     ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
     ap.add_argument("--dense-runs", type=int, default=3)
     ap.add_argument("--gt-runs", type=int, default=2, help="timed runs of the ground-truth kernel (0: skip)")
+    ap.add_argument("--extra-runs", type=int, default=3,
+                    help="timed runs of the gate with block RoPE and of the distillation step (0: skip)")
     ap.add_argument("--cpu-rows", type=int, default=4096, help="oracle sample size (q-block rows)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -229,7 +232,39 @@ def main() -> int:
             torch.cuda.synchronize()
             gts.append(a.elapsed_time(b))
         gt_ms = float(np.median(gts))
-        del gt_ws, gt_map
+        del gt_ws
+
+    def timed(fn, runs):
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(runs):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    # the gate with block-level RoPE (section 3.1: pre-RoPE q/k, rotation at block
+    # positions after the linear layers), Llama 3.1's RoPE base
+    rope_ms, distill_ms = None, None
+    if args.extra_runs > 0:
+        rope_ms = timed(lambda: seer.gate(qd, kd, wqd, wkd, **gate_kw, rope_theta=ROPE_BASE, mask=mask,
+                                          workspace=ws), args.extra_runs)
+    # one gate distillation step (Eq. 2: KL against the pooled ground truth,
+    # gradients of both gate weights) at the same shape
+    if args.extra_runs > 0 and args.gt_runs > 0 and w.dtype == "bf16":
+        dwq, dwk = torch.empty_like(wqd), torch.empty_like(wkd)
+        loss = torch.empty(1, dtype=torch.float32, device="cuda")
+        dws = torch.empty(max(1, seer.gate_distill_workspace_bytes(qd, kd, wqd, wkd)), dtype=torch.uint8,
+                          device="cuda")
+        distill_ms = timed(lambda: seer.gate_distill(qd, kd, wqd, wkd, gt_map, dwq=dwq, dwk=dwk, loss=loss,
+                                                     workspace=dws), args.extra_runs)
+        del dwq, dwk, dws
+    if args.gt_runs > 0:
+        del gt_map
 
     active_flops = flops_tile * active
     D = w.head_dim
@@ -277,6 +312,12 @@ def main() -> int:
             "ms": round(gt_ms, 3), "dense_ms": round(dense_ms, 3),
             "overhead_vs_dense": round(gt_ms / dense_ms - 1.0, 4),
             "workspace_bytes": gt_ws_bytes, "map_bytes": 4 * w.batch * w.heads_q * nb * nb},
+        "gate_block_rope": None if rope_ms is None else {
+            "what": f"seer_gate with block-level RoPE (base {ROPE_BASE:g}) at the same shape",
+            "ms": round(rope_ms, 4), "overhead_vs_gate": round(rope_ms / gate_ms - 1.0, 4)},
+        "distill": None if distill_ms is None else {
+            "what": "seer_gate_distill: gate forward, KL(renormalised ground truth || gate), dWq and dWk",
+            "ms": round(distill_ms, 3)},
         "roofline": {"bound": "mfma", "kernel": attn_kernels,
                      "achieved": round(attn_tflops, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(attn_tflops / peak, 4), "traffic": _traffic(w.name),

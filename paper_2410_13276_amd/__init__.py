@@ -336,6 +336,13 @@ def attn_gt(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
     return out, lse, gt
 
 
+def gate_distill_workspace_bytes(q, k, wq, wk, *, w_per_head: bool = True, rope_theta: float = 0.0) -> int:
+    """Workspace of gate_distill for these shapes."""
+    d = make_desc(q, k)
+    gd = gate_desc(wq.shape[-1], TOPK_RATIO, topk_ratio=1.0, w_per_head=w_per_head, rope_theta=rope_theta)
+    return lib().seer_gate_distill_workspace_bytes(C.byref(d), C.byref(gd))
+
+
 def gate_distill(q, k, wq, wk, gt, *, w_per_head: bool = True, rope_theta: float = 0.0,
                  dwq=None, dwk=None, loss=None, workspace=None, stream=None):
     """One gate distillation step (seer_gate_distill): returns (loss [1], dwq, dwk)
