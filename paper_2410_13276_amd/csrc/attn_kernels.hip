@@ -502,14 +502,51 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
       load_tile_lds<D>(sV_a, vp + jt * vtile, vss, wave_u, voffd);
   };
 
+  // diagonal tile: key kl visible to query ql iff kl <= ql.  Without causality
+  // the last tile of a sequence ending inside it hides its keys past the end
+  // (with causality they are already hidden from every real query).
+  auto mask_tile = [&](f32x16 (&s)[2], int jt) {
+    const bool diag = a.causal && jt == t.i;
+    const bool tail = ragged && !a.causal && jt == a.n_blocks - 1;
+    if (diag || tail) {
+      const int ql = 32 * wave + col;
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int kl = 32 * mt + 8 * (e / 4) + 4 * hf + (e % 4);
+          if ((diag && kl > ql) || (tail && kl >= n_last)) s[mt][e] = -INFINITY;
+        }
+    }
+  };
+  // the row max of a tile per query: the two lane halves hold the two 32-key
+  // halves of a query's tile row, exchanged in registers by v_permlane32_swap
+  auto row_max = [&](const f32x16 (&s)[2]) -> float {
+    float mx2[2] = {-INFINITY, -INFINITY};  // two independent max chains
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx2[mt] = fmaxf(mx2[mt], s[mt][e]);
+    const float m = fmaxf(mx2[0], mx2[1]);
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+    return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+  };
+
   f32x16 sA[2], sB[2];
+  float mloc = -INFINITY;  // row max of the tile in the current S buffer
+  bool resc = false;       // whether that tile moves the running max
   if (j >= 0) {
     load_k(j);
     load_v(j);
   }
   wait_loads();  // also retires the Q loads: nothing the loop body waits on is pending
   __syncthreads();
-  if (j >= 0) s_product(sA);
+  if (j >= 0) {
+    s_product(sA);
+    mask_tile(sA, j);
+    mloc = row_max(sA);
+    resc = __ballot((mloc - m_run) * c > 8.0f) != 0;
+  }
   __syncthreads();  // K_j consumed
   if (jn >= 0) load_k(jn);
   wait_loads();
@@ -531,30 +568,9 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
       }
       jnn = entry(n + 2);
     }
-    // diagonal tile: key kl visible to query ql iff kl <= ql.  Without causality
-    // the last tile of a sequence ending inside it hides its keys past the end
-    // (with causality they are already hidden from every real query).
-    const bool diag = a.causal && j == t.i;
-    const bool tail = ragged && !a.causal && j == a.n_blocks - 1;
-    if (diag || tail) {
-      const int ql = 32 * wave + col;
-#pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int kl = 32 * mt + 8 * (e / 4) + 4 * hf + (e % 4);
-          if ((diag && kl > ql) || (tail && kl >= n_last)) sc[mt][e] = -INFINITY;
-        }
-    }
-    // online softmax (lazy rescale)
-    float mx2[2] = {-INFINITY, -INFINITY};  // two independent max chains
-#pragma unroll
-    for (int mt = 0; mt < 2; ++mt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx2[mt] = fmaxf(mx2[mt], sc[mt][e]);
-    float mloc = fmaxf(mx2[0], mx2[1]);
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-    if (__ballot((mloc - m_run) * c > 8.0f)) {
+    // online softmax (lazy rescale); tile j's masked row max and the rescale
+    // decision were formed under the previous tile's P.V product
+    if (resc) {
       const float m_new = fmaxf(m_run, mloc);
       const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
       m_run = m_new;
@@ -619,6 +635,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
           (__attribute__((address_space(3))) s16x4*)(base + 8 * D));
       return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
     };
+    if (jn >= 0) mask_tile(sn, jn);
     constexpr int NV = 4 * (D / 32);
     bf16x8 vf0 = vread(0), vf1 = vread(1);
 #pragma unroll
@@ -629,18 +646,23 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
       vf0 = vf1;
       vf1 = vf2;
     }
-    // schedule: transposed V reads run two MFMAs ahead
+    const float mloc_n = row_max(sn);
+    // schedule: transposed V reads run two MFMAs ahead, the next tile's row max
+    // fills VALU slots between the MFMAs
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
     for (int st = 0; st < NV - 2; ++st) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    resc = __ballot((mloc_n - m_run) * c > 8.0f) != 0;
     wait_loads();
     __builtin_amdgcn_s_setprio(0);
     __syncthreads();  // E: V_j consumed, K_jnn visible
     if (jn >= 0) load_v(jn);
+    mloc = mloc_n;
     j = jn;
     jn = jnn;
     ++n;
