@@ -266,6 +266,27 @@ def main() -> int:
     if args.gt_runs > 0:
         del gt_map
 
+    # variant: one mask per KV group (the mean of the group's head probabilities
+    # selects; attention loads each K/V tile once for two query heads), same
+    # TopK setting, at the same shape
+    kv = None
+    if args.extra_runs > 0 and w.dtype == "bf16" and w.heads_q > w.heads_kv and w.select != W.SEL_THRESHOLD:
+        mkv = seer.alloc_mask(w.batch, w.heads_kv, w.seq_len, kv_shared=True)
+        kv_gate_ms = timed(lambda: seer.gate(qd, kd, wqd, wkd, **gate_kw, kv_shared=True, mask=mkv, workspace=ws),
+                           args.extra_runs)
+        kv_attn_ms = timed(lambda: seer.bsattn(qd, kd, vd, mkv, out=od, workspace=aws), args.extra_runs)
+        kv_active = int(mkv.count.sum().item()) * (w.heads_q // w.heads_kv)
+        kv_sp = 1.0 - kv_active / causal_tiles
+        kv = {"what": "shared-mask variant (not the paper's per-head gate): one mask per KV group selected "
+                      "from the mean of its query heads' gate probabilities; attention loads each K/V tile "
+                      "once for two query heads of the group",
+              "gate_ms": round(kv_gate_ms, 4), "attn_ms": round(kv_attn_ms, 4),
+              "attn_tflops": round(flops_tile * kv_active / (kv_attn_ms * 1e-3) / 1e12, 2),
+              "sparsity": round(kv_sp, 5), "active_tiles": kv_active,
+              "speedup_vs_dense": round(dense_ms / kv_attn_ms, 3),
+              "speedup_tracking": round(dense_ms / kv_attn_ms * (1.0 - kv_sp), 3)}
+        del mkv
+
     active_flops = flops_tile * active
     D = w.head_dim
     sparse_split = aws is not None and os.environ.get("SEER_SPLIT_SPARSE") == "1"
@@ -315,6 +336,7 @@ def main() -> int:
         "gate_block_rope": None if rope_ms is None else {
             "what": f"seer_gate with block-level RoPE (base {ROPE_BASE:g}) at the same shape",
             "ms": round(rope_ms, 4), "overhead_vs_gate": round(rope_ms / gate_ms - 1.0, 4)},
+        "kv_shared": kv,
         "distill": None if distill_ms is None else {
             "what": "seer_gate_distill: gate forward, KL(renormalised ground truth || gate), dWq and dWk",
             "ms": round(distill_ms, 3)},

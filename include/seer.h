@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define SEER_ABI_VERSION 1
+#define SEER_ABI_VERSION 2
 #define SEER_BLOCK 64 /* the attention tile edge and the default gate block (section 4); gate
                         blocks and masks of 128 tokens are the other size the paper names */
 
@@ -106,15 +106,25 @@ typedef struct {
                           are rotated at their block positions with base rope_theta /
                           block (rope_theta is the model's RoPE base; rotate-half
                           pairing (d, d + Dg/2)).  0 disables it. */
+  int32_t kv_shared;   /* 1: one mask per KV group instead of per query head (a
+                          variant, not the paper's per-head gate): block j of query
+                          block i is scored by the mean over the group's query heads
+                          of their probabilities P[h][i][j], and TopK / threshold
+                          select on that score; head_thresholds then has heads_kv
+                          entries and out->kv_shared must be 1.  0: per head. */
 } seer_gate_desc;
 
 /* Block mask in compacted form: for row r = (b, h, i), idx[r][0 .. count[r]-1]
- * are the active key blocks j in strictly ascending order.  Caller-owned. */
+ * are the active key blocks j in strictly ascending order.  Caller-owned.
+ * With kv_shared = 1 the rows are per KV head (h = KV head; heads = heads_kv
+ * below) and row (b, g, i) applies to every query head of group g: attention
+ * then loads each K/V tile once for several query heads of the group. */
 typedef struct {
   int32_t n_blocks;  /* nb = ceil(seq_len / block), block 64 or 128 */
-  int32_t* count;    /* device [batch][heads_q][nb] */
-  uint16_t* idx;     /* device [batch][heads_q][nb][nb] */
-  uint8_t* dense;    /* optional device [batch][heads_q][nb][nb] 0/1 copy, or NULL */
+  int32_t* count;    /* device [batch][heads][nb], heads = heads_q (or heads_kv) */
+  uint16_t* idx;     /* device [batch][heads][nb][nb] */
+  uint8_t* dense;    /* optional device [batch][heads][nb][nb] 0/1 copy, or NULL */
+  int32_t kv_shared; /* 0: rows per query head; 1: rows per KV head (see above) */
 } seer_block_mask;
 
 /* ABI version (SEER_ABI_VERSION of the built library). */
@@ -129,7 +139,8 @@ const char* seer_status_str(int status);
 size_t seer_gate_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate,
                                  int32_t logits_in_workspace);
 
-/* Elements of the idx array of a seer_block_mask for this shape (B*Hq*nb*nb). */
+/* Elements of the idx array of a per-query-head seer_block_mask for this shape
+ * (B*Hq*nb*nb; a kv_shared mask needs B*Hkv*nb*nb). */
 size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block);
 
 /*
@@ -144,6 +155,8 @@ size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block);
  *         remaining causal blocks by L, ties to the smaller j, k_i blocks in all
  *         with k_i = min(i + 1, max(#forced, k)).
  *   Threshold: the forced blocks plus every causal j with P[i][j] > threshold.
+ *   With gate->kv_shared the rows are per KV group and P above is replaced by
+ *   the mean of P over the group's query heads.
  * Inputs q, k follow desc (bf16 or fp32); wq, wk are fp32 (layout in
  * seer_gate_desc).  Writes out->count, out->idx and, when non-NULL, out->dense.
  * logits_out (device float [B][Hq][nb][nb], or NULL) receives L for j <= i
@@ -160,7 +173,8 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate,
 
 /*
  * Block-sparse FlashAttention forward (section 3.3): for each query block i of
- * (b, h) and each active key block j of mask row (b, h, i) (blocks of `block`
+ * (b, h) and each active key block j of mask row (b, h, i) -- row (b, g, i),
+ * g = h / (heads_q / heads_kv), of a kv_shared mask -- (blocks of `block`
  * tokens, 64 or 128; a 128-token mask is run as its 64-token tiles),
  *   O_i = softmax(sm_scale * Q_i K^T) V over the keys of the active blocks,
  * with the causal mask applied inside the diagonal block when causal != 0.
@@ -220,8 +234,9 @@ seer_status seer_dense_attn_ws(const seer_attn_desc* desc, int32_t causal, float
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * Compacts a 0/1 block mask dense (device uint8 [B][Hq][nb][nb]; any non-zero
- * byte is active) into out->count / out->idx (ascending).  out->dense is ignored.
+ * Compacts a 0/1 block mask dense (device uint8 [B][heads][nb][nb], heads =
+ * heads_kv when out->kv_shared, else heads_q; any non-zero byte is active)
+ * into out->count / out->idx (ascending).  out->dense is ignored.
  */
 seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, const uint8_t* dense,
                                  seer_block_mask* out, void* stream);

@@ -60,6 +60,8 @@ def lib():
         L.orc_gate_logits.restype = None
         L.orc_gate_logscore.argtypes = [p, C.c_int64, i, p]
         L.orc_gate_logscore.restype = None
+        L.orc_group_logscore.argtypes = [p, i, i, i, i, p]
+        L.orc_group_logscore.restype = None
         L.orc_topk_k.argtypes = [i, i, C.c_double, i, i]
         L.orc_topk_k.restype = i
         L.orc_select.argtypes = [p, i, i, i, i, C.c_double, i, p, i, i, i, p, p, p, p]
@@ -145,6 +147,18 @@ def gate_logscore(L: np.ndarray) -> np.ndarray:
     ell = np.empty_like(L)
     lib().orc_gate_logscore(_ptr(L), L.size // nb, nb, _ptr(ell))
     return ell
+
+
+def group_logscore(ell: np.ndarray, heads_kv: int) -> np.ndarray:
+    """Log of the mean gate probability over each KV group's query heads
+    [B, Hkv, nb, nb] (the shared-mask variant's score)."""
+    ell = np.ascontiguousarray(ell, dtype=np.float64)
+    B, Hq, nb, _ = ell.shape
+    if Hq % heads_kv != 0:
+        raise ValueError("heads_q must be a multiple of heads_kv")
+    out = np.empty((B, heads_kv, nb, nb), dtype=np.float64)
+    lib().orc_group_logscore(_ptr(ell), B, Hq, heads_kv, nb, _ptr(out))
+    return out
 
 
 def topk_k(mode: int, i: int, rho: float, k_fixed: int, n_forced: int) -> int:

@@ -29,6 +29,8 @@
  *                        for a double are still ordered exactly.
  *   orc_select        -- Eq. 3 (TopK) and Eq. 4 (threshold) with the always-kept
  *                        first and diagonal blocks.
+ *   orc_group_logscore -- the shared-mask variant's score: the mean over a KV
+ *                        group's query heads of their gate probabilities.
  *   orc_attn          -- softmax(Q K^T / sqrt(d)) V restricted to the keys whose
  *                        64-token block is active in the block mask (section 3.3
  *                        "Block Sparse Flash-Attn Kernel"); an all-ones mask is
@@ -217,6 +219,42 @@ void orc_gate_logscore(const double *L, int64_t rows, int nb, double *ell) {
       if (l[j] != -INFINITY) s += exp(l[j] - m);
     const double lse = m + log(s);
     for (int j = 0; j < nb; ++j) e[j] = (l[j] == -INFINITY) ? -INFINITY : l[j] - lse;
+  }
+}
+
+/*
+ * Shared-mask variant (a mask per KV group instead of per query head; the
+ * paper's gate is per head, section 3.1): the group's score of block j for
+ * query block i is the mean over its G = Hq / Hkv query heads h of the gate
+ * probabilities P[h][i][j] = exp(ell[h][i][j]).  Returned in log form,
+ *   ellg[b][g][i][j] = log( (1/G) sum_h exp(ell[b][h][i][j]) ),
+ * formed as a log-sum-exp over the heads so that tiny probabilities keep their
+ * order; entries that are -inf for every head stay -inf.
+ */
+void orc_group_logscore(const double *ell, int B, int Hq, int Hkv, int nb, double *ellg) {
+  const int G = Hq / Hkv;
+  const int64_t rows = (int64_t)B * Hkv * nb;
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) {
+    const int i = (int)(r % nb);
+    const int g = (int)((r / nb) % Hkv);
+    const int b = (int)(r / ((int64_t)nb * Hkv));
+    double *out = ellg + r * nb;
+    for (int j = 0; j < nb; ++j) {
+      double m = -INFINITY;
+      for (int h = 0; h < G; ++h) {
+        const double x = ell[(((int64_t)b * Hq + (int64_t)g * G + h) * nb + i) * nb + j];
+        if (x > m) m = x;
+      }
+      if (m == -INFINITY) {
+        out[j] = -INFINITY;
+        continue;
+      }
+      double s = 0.0;
+      for (int h = 0; h < G; ++h)
+        s += exp(ell[(((int64_t)b * Hq + (int64_t)g * G + h) * nb + i) * nb + j] - m);
+      out[j] = m + log(s / (double)G);
+    }
   }
 }
 

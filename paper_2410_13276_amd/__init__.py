@@ -39,12 +39,13 @@ class GateDesc(C.Structure):
     _fields_ = [("block", C.c_int32), ("gate_dim", C.c_int32), ("w_per_head", C.c_int32),
                 ("mode", C.c_int32), ("topk_ratio", C.c_double), ("topk_k", C.c_int32),
                 ("threshold", C.c_float), ("head_thresholds", C.c_void_p),
-                ("keep_first", C.c_int32), ("keep_diag", C.c_int32), ("rope_theta", C.c_double)]
+                ("keep_first", C.c_int32), ("keep_diag", C.c_int32), ("rope_theta", C.c_double),
+                ("kv_shared", C.c_int32)]
 
 
 class BlockMaskStruct(C.Structure):
     _fields_ = [("n_blocks", C.c_int32), ("count", C.c_void_p), ("idx", C.c_void_p),
-                ("dense", C.c_void_p)]
+                ("dense", C.c_void_p), ("kv_shared", C.c_int32)]
 
 
 # every symbol include/seer.h declares, with its ctypes signature
@@ -155,11 +156,14 @@ def _check(status: int, where: str):
 @dataclass
 class BlockMask:
     """Compacted block mask: idx[b, h, i, :count[b, h, i]] ascending (device tensors)
-    of `block`-token blocks (64 or 128; the last block may be partial)."""
-    count: object  # int32 [B, Hq, nb]
-    idx: object    # int16 storage of uint16 [B, Hq, nb, nb]
-    dense: Optional[object] = None  # uint8 [B, Hq, nb, nb]
+    of `block`-token blocks (64 or 128; the last block may be partial).  With
+    kv_shared the rows are per KV head (h = KV head) and apply to every query
+    head of the group."""
+    count: object  # int32 [B, H, nb]  (H = Hq, or Hkv when kv_shared)
+    idx: object    # int16 storage of uint16 [B, H, nb, nb]
+    dense: Optional[object] = None  # uint8 [B, H, nb, nb]
     block: int = BLOCK
+    kv_shared: bool = False
 
     @property
     def n_blocks(self) -> int:
@@ -171,6 +175,7 @@ class BlockMask:
         m.count = _ptr(self.count)
         m.idx = _ptr(self.idx)
         m.dense = _ptr(self.dense)
+        m.kv_shared = int(bool(self.kv_shared))
         return m
 
     def indices(self):
@@ -178,15 +183,17 @@ class BlockMask:
         return self.idx.to(_torch().int32) & 0xFFFF
 
 
-def alloc_mask(batch: int, heads_q: int, seq_len: int, device="cuda", dense: bool = False,
-               block: int = BLOCK) -> BlockMask:
+def alloc_mask(batch: int, heads: int, seq_len: int, device="cuda", dense: bool = False,
+               block: int = BLOCK, kv_shared: bool = False) -> BlockMask:
+    """Mask buffers for `heads` row sets: the query heads, or the KV heads of a
+    kv_shared mask."""
     torch = _torch()
     nb = -(-seq_len // block)  # the last block may be partial
     return BlockMask(
-        count=torch.empty((batch, heads_q, nb), dtype=torch.int32, device=device),
-        idx=torch.empty((batch, heads_q, nb, nb), dtype=torch.int16, device=device),
-        dense=torch.empty((batch, heads_q, nb, nb), dtype=torch.uint8, device=device) if dense else None,
-        block=block)
+        count=torch.empty((batch, heads, nb), dtype=torch.int32, device=device),
+        idx=torch.empty((batch, heads, nb, nb), dtype=torch.int16, device=device),
+        dense=torch.empty((batch, heads, nb, nb), dtype=torch.uint8, device=device) if dense else None,
+        block=block, kv_shared=kv_shared)
 
 
 # ---------------------------------------------------------------------------
@@ -196,7 +203,7 @@ def alloc_mask(batch: int, heads_q: int, seq_len: int, device="cuda", dense: boo
 def gate_desc(gate_dim: int, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
               threshold: float = 0.0, head_thresholds=None, keep_first: bool = True,
               keep_diag: bool = True, w_per_head: bool = True, rope_theta: float = 0.0,
-              block: int = BLOCK) -> GateDesc:
+              block: int = BLOCK, kv_shared: bool = False) -> GateDesc:
     g = GateDesc()
     g.block = block
     g.gate_dim = gate_dim
@@ -209,6 +216,7 @@ def gate_desc(gate_dim: int, mode: int, topk_ratio: float = 0.0, topk_k: int = 0
     g.keep_first = int(bool(keep_first))
     g.keep_diag = int(bool(keep_diag))
     g.rope_theta = float(rope_theta)
+    g.kv_shared = int(bool(kv_shared))
     return g
 
 
@@ -222,17 +230,21 @@ def gate_workspace_bytes(q, k, gate_dim: int, mode: int = TOPK_RATIO, topk_ratio
 def gate(q, k, wq, wk, *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
          threshold: float = 0.0, head_thresholds=None, keep_first: bool = True,
          keep_diag: bool = True, w_per_head: bool = True, rope_theta: float = 0.0,
-         block: int = BLOCK, mask: Optional[BlockMask] = None, dense_out: bool = False,
-         logits_out=None, workspace=None, stream=None) -> BlockMask:
+         block: int = BLOCK, kv_shared: bool = False, mask: Optional[BlockMask] = None,
+         dense_out: bool = False, logits_out=None, workspace=None, stream=None) -> BlockMask:
     """AttnGate + block selection (seer_gate).  Returns the block mask (of
     `block`-token blocks, 64 or 128).  With rope_theta > 0 (the model's RoPE
-    base) q and k are pre-RoPE and the gate applies its block-level RoPE."""
+    base) q and k are pre-RoPE and the gate applies its block-level RoPE.  With
+    kv_shared one mask per KV group is selected from the mean of the group's
+    head probabilities."""
     torch = _torch()
     d = make_desc(q, k)
     gd = gate_desc(wq.shape[-1], mode, topk_ratio, topk_k, threshold, head_thresholds,
-                   keep_first, keep_diag, w_per_head, rope_theta, block)
+                   keep_first, keep_diag, w_per_head, rope_theta, block, kv_shared)
     if mask is None:
-        mask = alloc_mask(q.shape[0], q.shape[1], q.shape[2], q.device, dense=dense_out, block=block)
+        heads = k.shape[1] if kv_shared else q.shape[1]
+        mask = alloc_mask(q.shape[0], heads, q.shape[2], q.device, dense=dense_out, block=block,
+                          kv_shared=kv_shared)
     mask.block = block
     need = lib().seer_gate_workspace_bytes(C.byref(d), C.byref(gd), int(logits_out is None))
     if workspace is None:
@@ -368,16 +380,18 @@ def gate_distill(q, k, wq, wk, gt, *, w_per_head: bool = True, rope_theta: float
 
 
 def mask_from_dense(dense, heads_kv: int = 1, mask: Optional[BlockMask] = None,
-                    block: int = BLOCK, stream=None) -> BlockMask:
-    """Compacts a uint8 [B, Hq, nb, nb] device mask of `block`-token blocks
-    (seer_mask_from_dense)."""
+                    block: int = BLOCK, kv_shared: bool = False, stream=None) -> BlockMask:
+    """Compacts a uint8 [B, H, nb, nb] device mask of `block`-token blocks
+    (seer_mask_from_dense); H = Hq, or Hkv for a kv_shared mask."""
     torch = _torch()
-    B, Hq, nb, _ = dense.shape
+    B, H, nb, _ = dense.shape
     if mask is None:
-        mask = alloc_mask(B, Hq, nb * block, dense.device, block=block)
+        mask = alloc_mask(B, H, nb * block, dense.device, block=block, kv_shared=kv_shared)
     mask.block = block
+    mask.kv_shared = kv_shared
     d = AttnDesc()
-    d.batch, d.heads_q, d.heads_kv, d.seq_len, d.head_dim, d.dtype = B, Hq, heads_kv, nb * block, 128, BF16
+    d.batch, d.heads_q, d.heads_kv, d.seq_len, d.head_dim, d.dtype = B, H, (H if kv_shared else heads_kv), \
+        nb * block, 128, BF16
     ms = mask.struct()
     st = lib().seer_mask_from_dense(C.byref(d), block, _ptr(dense.contiguous()), C.byref(ms),
                                     _stream(stream))

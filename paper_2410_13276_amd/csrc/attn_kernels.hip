@@ -170,7 +170,9 @@ __device__ __forceinline__ RowList<SPARSE> make_list(const AttnArgs& a, const Ta
   if (SPARSE) {
     const int sh = a.mask_shift;
     const int nbm = a.mask_blocks;  // blocks of the mask
-    const int64_t mrow = ((int64_t)t.b * a.heads_q + t.h) * nbm + (t.i >> sh);
+    // a mask shared by a KV group has one row per (batch, KV head, block)
+    const int64_t mrow = a.mask_kv ? ((int64_t)t.b * a.heads_kv + t.h / (a.heads_q / a.heads_kv)) * nbm + (t.i >> sh)
+                                   : ((int64_t)t.b * a.heads_q + t.h) * nbm + (t.i >> sh);
     L.sh = sh;
     L.idx = a.idx + mrow * nbm;
     L.n = min(max(a.count[mrow], 0), nbm) << sh;
@@ -328,10 +330,34 @@ __device__ __forceinline__ void load_tile_lds(uint32_t lds, const uint16_t* __re
     dma16(lds + 1024u * (2 * e + wave_u), tile + (int64_t)(128 * e / Lay::CPR) * ss, off[e & 1]);
 }
 
+// With NW >= 4 wavefronts sharing the tile, wavefront w issues loads e =
+// 0 .. D / (8 NW) - 1, covering LDS chunk ch = NW e + w, i.e. chunks q = 64 ch +
+// lane: row q / CPR, physical chunk q % CPR.  The row advances by 64 NW / CPR
+// (a multiple of 16) per load, which leaves both swizzles unchanged, so each
+// lane needs one byte offset per tensor; the rest is the scalar base.
+template <int D, bool IS_V, int NW>
+__device__ __forceinline__ uint32_t dma_offset_nw(int ss, int wave, int lane) {
+  using Lay = Bf16Layout<D>;
+  static_assert(NW >= 4 && (64 * NW / Lay::CPR) % 16 == 0, "swizzle must not depend on the load");
+  const int ql = 64 * wave + lane;
+  const int r = ql / Lay::CPR;
+  const int gc = (ql % Lay::CPR) ^ (IS_V ? Lay::fv(r) : Lay::fk(r));
+  return (uint32_t)((r * ss + 8 * gc) * 2);
+}
+
+template <int D, int NW>
+__device__ __forceinline__ void load_tile_lds_nw(uint32_t lds, const uint16_t* __restrict__ tile, int ss,
+                                                 int wave_u, uint32_t off) {
+  using Lay = Bf16Layout<D>;
+#pragma unroll
+  for (int e = 0; e < D / (8 * NW); ++e)
+    dma16(lds + 1024u * (NW * e + wave_u), tile + (int64_t)(64 * NW * e / Lay::CPR) * ss, off);
+}
+
 // The last tile of a sequence that ends inside it: rows past the end are read
 // from the last row instead (finite data, masked or discarded later), so no
 // load leaves the tensor.  Row offsets are per lane and per load here.
-template <int D, bool IS_V>
+template <int D, bool IS_V, int NW = 2>
 __device__ __forceinline__ void load_tile_lds_clamped(uint32_t lds, const uint16_t* __restrict__ tile,
                                                       int ss, int wave, int wave_u, int lane,
                                                       int rows_valid) {
@@ -339,11 +365,11 @@ __device__ __forceinline__ void load_tile_lds_clamped(uint32_t lds, const uint16
   const int ql = 64 * wave + lane;
   const int pc = ql % Lay::CPR;
 #pragma unroll
-  for (int e = 0; e < Lay::LOADS; ++e) {
-    const int r = 128 * e / Lay::CPR + ql / Lay::CPR;  // the LDS row this lane fills
+  for (int e = 0; e < D / (8 * NW); ++e) {
+    const int r = 64 * NW * e / Lay::CPR + ql / Lay::CPR;  // the LDS row this lane fills
     const int gc = pc ^ (IS_V ? Lay::fv(r) : Lay::fk(r));
     const int rr = min(r, rows_valid - 1);
-    dma16(lds + 1024u * (2 * e + wave_u), tile, (uint32_t)((rr * ss + 8 * gc) * 2));
+    dma16(lds + 1024u * (NW * e + wave_u), tile, (uint32_t)((rr * ss + 8 * gc) * 2));
   }
 }
 
@@ -376,20 +402,31 @@ constexpr int kListChunk = 256;
 //
 // RAGGED: the sequence ends inside its last tile (the clamped loads and the
 // key mask past the end exist only in that instantiation).
-template <int D, bool SPARSE, bool SPLIT, bool RAGGED>
-__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(2, 2)))
+//
+// NH > 1 (sparse rows of a mask shared by a KV group): the workgroup holds NH
+// query heads of one group, two wavefronts each, for the same query block;
+// each K/V tile is loaded once into LDS for all of them, which divides the
+// K/V traffic by NH.  The task map then counts head slots of NH heads.
+template <int D, bool SPARSE, bool SPLIT, bool RAGGED, int NH = 1>
+__global__ __launch_bounds__(128 * NH) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_bf16_kernel(KernelArgs ka) {
   using Lay = Bf16Layout<D>;
+  constexpr int NW = 2 * NH;  // wavefronts
+  static_assert(NH == 1 || (SPARSE && !SPLIT), "shared-row workgroups serve sparse unsplit rows");
   __shared__ __attribute__((aligned(16))) uint16_t sK[Lay::TILE];
   __shared__ __attribute__((aligned(16))) uint16_t sV[Lay::TILE];
   __shared__ uint16_t sList[SPARSE ? kListChunk : 1];
   __shared__ __attribute__((aligned(16))) float sL2[SPARSE ? 1 : 64];
 
   const AttnArgs& a = ka.a;
-  const Task t = SPLIT ? decode_split(ka.split, blockIdx.x) : decode_task(ka.map, blockIdx.x);
+  Task t = SPLIT ? decode_split(ka.split, blockIdx.x) : decode_task(ka.map, blockIdx.x);
   const int tid = threadIdx.x;
-  const int wave = tid / 64;
-  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int wave_all = tid / 64;                       // 0 .. NW - 1
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave_all);
+  const int wave = wave_all % 2;                       // the query half of this wavefront's head
+  const int h0 = t.h * NH;                             // first query head of the workgroup
+  t.h = h0;                                            // (uniform: mask row and K/V group)
+  const int hq = h0 + wave_all / 2;                    // this wavefront's query head
   const int lane = tid % 64;
   const int hf = lane / 32;
   const int col = lane % 32;
@@ -397,10 +434,18 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   const int g = t.h / G;
   const int kss = (int)a.k.ss, vss = (int)a.v.ss;
   const uint32_t sK_a = lds_addr(sK), sV_a = lds_addr(sV);
-  const uint32_t koffd[2] = {dma_offset<D, false>(kss, wave, lane, 0), dma_offset<D, false>(kss, wave, lane, 1)};
-  const uint32_t voffd[2] = {dma_offset<D, true>(vss, wave, lane, 0), dma_offset<D, true>(vss, wave, lane, 1)};
+  uint32_t koffd[2], voffd[2];
+  if constexpr (NH == 1) {
+    koffd[0] = dma_offset<D, false>(kss, wave, lane, 0);
+    koffd[1] = dma_offset<D, false>(kss, wave, lane, 1);
+    voffd[0] = dma_offset<D, true>(vss, wave, lane, 0);
+    voffd[1] = dma_offset<D, true>(vss, wave, lane, 1);
+  } else {
+    koffd[0] = koffd[1] = dma_offset_nw<D, false, NW>(kss, wave_all, lane);
+    voffd[0] = voffd[1] = dma_offset_nw<D, true, NW>(vss, wave_all, lane);
+  }
 
-  const uint16_t* qp = static_cast<const uint16_t*>(a.q.ptr) + t.b * a.q.sb + t.h * a.q.sh;
+  const uint16_t* qp = static_cast<const uint16_t*>(a.q.ptr) + t.b * a.q.sb + hq * a.q.sh;
   const uint16_t* kp = static_cast<const uint16_t*>(a.k.ptr) + t.b * a.k.sb + g * a.k.sh;
   const uint16_t* vp = static_cast<const uint16_t*>(a.v.ptr) + t.b * a.v.sb + g * a.v.sh;
   const int64_t ktile = 64 * a.k.ss, vtile = 64 * a.v.ss;
@@ -449,7 +494,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   auto fetch_chunk = [&](int base) {  // mask entries [base, base + kListChunk) of the row
     if (SPARSE) {
       const int ne = list.n >> list.sh;
-      for (int p = tid; p < kListChunk; p += 128)
+      for (int p = tid; p < kListChunk; p += 128 * NH)
         if (base + p < ne) sList[p] = list.idx[base + p];
     }
   };
@@ -491,15 +536,19 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
 
   auto load_k = [&](int jt) {
     if (RAGGED && jt == a.n_blocks - 1)
-      load_tile_lds_clamped<D, false>(sK_a, kp + jt * ktile, kss, wave, wave_u, lane, n_last);
-    else
+      load_tile_lds_clamped<D, false, NW>(sK_a, kp + jt * ktile, kss, wave_all, wave_u, lane, n_last);
+    else if constexpr (NH == 1)
       load_tile_lds<D>(sK_a, kp + jt * ktile, kss, wave_u, koffd);
+    else
+      load_tile_lds_nw<D, NW>(sK_a, kp + jt * ktile, kss, wave_u, koffd[0]);
   };
   auto load_v = [&](int jt) {
     if (RAGGED && jt == a.n_blocks - 1)
-      load_tile_lds_clamped<D, true>(sV_a, vp + jt * vtile, vss, wave, wave_u, lane, n_last);
-    else
+      load_tile_lds_clamped<D, true, NW>(sV_a, vp + jt * vtile, vss, wave_all, wave_u, lane, n_last);
+    else if constexpr (NH == 1)
       load_tile_lds<D>(sV_a, vp + jt * vtile, vss, wave_u, voffd);
+    else
+      load_tile_lds_nw<D, NW>(sV_a, vp + jt * vtile, vss, wave_u, voffd[0]);
   };
 
   // diagonal tile: key kl visible to query ql iff kl <= ql.  Without causality
@@ -679,45 +728,50 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = (l_tot > 0.f) ? 1.0f / l_tot : 0.f;
   wait_loads();
-  __syncthreads();
   uint16_t* sO = sK;  // sK and sV are adjacent: 2 tiles of staging room
   const int ql = 32 * wave + col;
-#pragma unroll
-  for (int dt = 0; dt < D / 32; ++dt)
-#pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      bf16x4 o4;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) o4[r] = (__bf16)(acc[dt][4 * jj + r] * inv);
-      *reinterpret_cast<bf16x4*>(sO + ql * Lay::OSTR + 32 * dt + 8 * jj + 4 * hf) = o4;
-    }
-  __syncthreads();
   // destination: the output rows of the query block, or the task's partial slot
   int64_t slot = 0;
-  uint16_t* op;
   int64_t ors;
   if (SPLIT) {
     slot = ((int64_t)t.b * a.heads_q + t.h) * a.split_slots + split_offset(t.i, a.split_w) + t.p;
-    op = a.part_o + slot * 64 * D;
     ors = D;
   } else {
-    op = static_cast<uint16_t*>(a.o) + t.b * a.osb + t.h * a.osh + (int64_t)64 * t.i * a.oss;
     ors = a.oss;
   }
   const int rows_out = (SPLIT || !RAGGED) ? 64 : min(64, S - 64 * t.i);  // rows past the end are not stored
+  // the workgroup's heads take turns with the staging room (one query block each)
 #pragma unroll
-  for (int e = 0; e < 64 * Lay::CPR / 128; ++e) {
-    const int q = tid + 128 * e;
-    const int r = q / Lay::CPR, cc = q % Lay::CPR;
-    if (r < rows_out)
-      *reinterpret_cast<u32x4*>(op + (int64_t)r * ors + 8 * cc) =
-          *reinterpret_cast<const u32x4*>(sO + r * Lay::OSTR + 8 * cc);
+  for (int hs = 0; hs < NH; ++hs) {
+    __syncthreads();
+    if (wave_all / 2 == hs) {
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          bf16x4 o4;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) o4[r] = (__bf16)(acc[dt][4 * jj + r] * inv);
+          *reinterpret_cast<bf16x4*>(sO + ql * Lay::OSTR + 32 * dt + 8 * jj + 4 * hf) = o4;
+        }
+    }
+    __syncthreads();
+    uint16_t* op = SPLIT ? a.part_o + slot * 64 * D
+                         : static_cast<uint16_t*>(a.o) + t.b * a.osb + (h0 + hs) * a.osh + (int64_t)64 * t.i * a.oss;
+#pragma unroll
+    for (int e = 0; e < 64 * Lay::CPR / (128 * NH); ++e) {
+      const int q = tid + 128 * NH * e;
+      const int r = q / Lay::CPR, cc = q % Lay::CPR;
+      if (r < rows_out)
+        *reinterpret_cast<u32x4*>(op + (int64_t)r * ors + 8 * cc) =
+            *reinterpret_cast<const u32x4*>(sO + r * Lay::OSTR + 8 * cc);
+    }
   }
   if (SPLIT) {
     if (hf == 0) a.part_lse[slot * 64 + ql] = (l_tot > 0.f) ? m_run * c + __log2f(l_tot) : -INFINITY;
   } else if (a.lse && hf == 0 && qrow < S) {
     const float lse = (l_tot > 0.f) ? m_run * a.scale + __logf(l_tot) : -INFINITY;
-    a.lse[((int64_t)t.b * a.heads_q + t.h) * (int64_t)S + qrow] = lse;
+    a.lse[((int64_t)t.b * a.heads_q + hq) * (int64_t)S + qrow] = lse;
   }
   if (pool) {
     // padding rows take no part in the column max
@@ -1081,8 +1135,9 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
       const int64_t hrow = (int64_t)b * a.heads_q + h0;  // first query head of the group
       if (a.lse) c.lse = a.lse + hrow * a.seq_len;
       if (a.count) {
-        c.count = a.count + hrow * nbm;
-        c.idx = a.idx + hrow * nbm * nbm;
+        const int64_t mrow = a.mask_kv ? (int64_t)b * a.heads_kv + g : hrow;  // first mask row set
+        c.count = a.count + mrow * nbm;
+        c.idx = a.idx + mrow * nbm * nbm;
       }
       const hipError_t e = launch_attn_one(c, s);
       if (e != hipSuccess) return e;
@@ -1090,9 +1145,57 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   return hipSuccess;
 }
 
+// Query heads per workgroup for rows of a mask shared by a KV group: 2 when the
+// group size allows, else 1 (the environment variable SEER_KV_HEADS_PER_WG,
+// read at each call, sets the cap: 1, 2 or 4).  Measured at 131072 tokens,
+// 32 query / 8 KV heads, TopK 0.1: per-head rows 17.3 ms; shared rows with 1,
+// 2 and 4 heads per workgroup 14.3, 13.0 and 13.1 ms (two 4-wavefront
+// workgroups per CU keep their phases independent; one 8-wavefront workgroup
+// moves in lockstep).
+static int kv_heads_per_wg(const AttnArgs& a) {
+  if (!a.mask_kv || !a.bf16 || a.split_w > 0) return 1;
+  int cap = 2;
+  if (const char* e = getenv("SEER_KV_HEADS_PER_WG")) cap = atoi(e);
+  const int G = a.heads_q / a.heads_kv;
+  for (int nh = 4; nh >= 2; nh /= 2)
+    if (nh <= cap && G % nh == 0) return nh;
+  return 1;
+}
+
+template <int D, bool RAGGED>
+static void launch_sparse_nh(const KernelArgs& ka, int nh, dim3 grid, hipStream_t s) {
+  if (nh == 4) hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, true, false, RAGGED, 4>), grid, dim3(512), 0, s, ka);
+  else hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, true, false, RAGGED, 2>), grid, dim3(256), 0, s, ka);
+}
+
 static hipError_t launch_attn_one(const AttnArgs& a, hipStream_t s) {
   KernelArgs ka;
   ka.a = a;
+  const int nh = kv_heads_per_wg(a);
+  if (nh > 1) {  // tasks over head slots of nh heads: the task order sees heads_q / nh heads
+    AttnArgs v = a;
+    v.heads_q = a.heads_q / nh;
+    ka.map = make_map(v);
+    const int64_t total = (int64_t)a.batch * v.heads_q * a.n_blocks;
+    if (total == 0) return hipSuccess;
+    ka.split = SplitMap{a.heads_q, a.heads_kv, a.n_blocks, 0, 0};
+    ka.scale_log2 = a.scale * kLog2e;
+    if (a.seq_len <= 0 || (a.n_blocks - 1) * 64 >= a.seq_len || a.n_blocks * 64 < a.seq_len || !a.count ||
+        a.gt != nullptr)
+      return hipErrorInvalidValue;
+    const bool ragged = a.seq_len % 64 != 0;
+    const dim3 grid((unsigned)total);
+    if (a.head_dim == 128) {
+      if (ragged) launch_sparse_nh<128, true>(ka, nh, grid, s);
+      else launch_sparse_nh<128, false>(ka, nh, grid, s);
+    } else if (a.head_dim == 64) {
+      if (ragged) launch_sparse_nh<64, true>(ka, nh, grid, s);
+      else launch_sparse_nh<64, false>(ka, nh, grid, s);
+    } else {
+      return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   ka.map = make_map(a);
   ka.split = SplitMap{a.heads_q, a.heads_kv, a.n_blocks, a.split_w, a.split_parts};
   ka.scale_log2 = a.scale * kLog2e;

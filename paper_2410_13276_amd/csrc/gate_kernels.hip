@@ -322,11 +322,12 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   const int lane = threadIdx.x % kWave;
   const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
   const int nb = a.n_blocks;
-  const int64_t rows = (int64_t)a.batch * a.heads_q * nb;
+  const int G = a.group;  // > 0: rows of a mask shared by the G query heads of a KV group
+  const int mheads = G > 0 ? a.heads_q / G : a.heads_q;  // heads of the mask
+  const int64_t rows = (int64_t)a.batch * mheads * nb;
   if (row >= rows) return;
   const int i = (int)(row % nb);
-  const int h = (int)((row / nb) % a.heads_q);
-  const float* L = a.logits + row * nb;
+  const int h = (int)((row / nb) % mheads);  // query head, or KV head when shared
   const int M = i / 64 + 1;  // words holding the causal blocks j <= i (wave-uniform)
 
   // per-lane bit m describes block j = 64m + lane
@@ -334,14 +335,44 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   uint64_t valid = 0, forced = 0;
 #pragma unroll
   for (int m = 0; m < MAXM; ++m) {
-    v[m] = -INFINITY;
-    if (m < M) {
-      const int j = 64 * m + lane;
-      const bool ok = j <= i;
-      if (ok) v[m] = L[j];
-      valid |= (uint64_t)ok << m;
-      forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
+    const int j = 64 * m + lane;
+    const bool ok = m < M && j <= i;
+    valid |= (uint64_t)ok << m;
+    forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
+  }
+  if (G == 0) {
+    const float* L = a.logits + row * nb;
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? L[64 * m + lane] : -INFINITY;
+  } else {
+    // the group's score of block j: the mean over its query heads of their gate
+    // probabilities, held as its logarithm so that TopK (by value) and the
+    // threshold test (against the log of the row sum, 1) below apply unchanged
+    float sc[MAXM];
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) sc[m] = 0.f;
+    const int64_t b = row / ((int64_t)mheads * nb);
+    for (int hh = 0; hh < G; ++hh) {
+      const float* L = a.logits + (((b * a.heads_q) + (int64_t)h * G + hh) * nb + i) * nb;
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? L[64 * m + lane] : -INFINITY;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m)
+        if (m < M) mx = fmaxf(mx, v[m]);
+      mx = wave_max(mx);
+      float s = 0.f;
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m)
+        if (m < M) s += ((valid >> m) & 1) ? __expf(v[m] - mx) : 0.f;
+      const float lse = mx + __logf(wave_sum(s));
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m)
+        if (m < M) sc[m] += ((valid >> m) & 1) ? __expf(v[m] - lse) : 0.f;
     }
+    const float inv_g = 1.0f / (float)G;
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? __logf(sc[m] * inv_g) : -INFINITY;
   }
   uint64_t sel = forced;
 
@@ -460,7 +491,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
 
 template <int MAXM>
 static hipError_t select_launch(const SelectArgs& a, hipStream_t s) {
-  const int64_t rows = (int64_t)a.batch * a.heads_q * a.n_blocks;
+  const int64_t rows = (int64_t)a.batch * (a.group > 0 ? a.heads_q / a.group : a.heads_q) * a.n_blocks;
   dim3 grid((unsigned)((rows + 3) / 4));
   hipLaunchKernelGGL(select_kernel<MAXM>, grid, dim3(256), 0, s, a);
   return hipGetLastError();

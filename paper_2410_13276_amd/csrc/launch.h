@@ -43,7 +43,9 @@ struct SelectArgs {
   double topk_ratio;
   int topk_k;
   float threshold;
-  const float* head_thresholds;  // device [Hq] or nullptr
+  const float* head_thresholds;  // device [Hq] ([Hkv] when group > 0) or nullptr
+  int group;            // 0: one row per query head; G: one row per KV head, scored by
+                        // the mean of its G query heads' probabilities
   int keep_first, keep_diag;
   int32_t* count;
   uint16_t* idx;
@@ -73,6 +75,8 @@ struct AttnArgs {
   const uint16_t* idx;
   int mask_shift;        // 0: mask of 64-token blocks; 1: of 128-token blocks, each
                          // entry standing for two 64-key tiles
+  bool mask_kv;          // the mask has one row set per KV head, shared by the
+                         // group's query heads (count [B][Hkv][nb], idx [B][Hkv][nb][nb])
   // ground-truth mode (dense only): per-tile row maxima [rows][nb][64] and the
   // 2D max-pooled probability map [B][Hq][nb][nb]; both nullptr otherwise
   float* pool_r;

@@ -61,6 +61,7 @@ seer_status check_gate_common(const seer_attn_desc* d, const seer_gate_desc* g) 
   if (g->gate_dim != 32 && g->gate_dim != 64 && g->gate_dim != 128) return SEER_ERR_UNSUPPORTED;
   if (blocks_of(d->seq_len, g->block) > 4096) return SEER_ERR_UNSUPPORTED;
   if (!(g->rope_theta >= 0.0) || std::isinf(g->rope_theta)) return SEER_ERR_INVALID_ARG;
+  if (g->kv_shared != 0 && g->kv_shared != 1) return SEER_ERR_INVALID_ARG;
   return SEER_OK;
 }
 
@@ -161,6 +162,7 @@ seer::AttnArgs attn_args(const seer_attn_desc* desc, int32_t causal, float sm_sc
   a.count = nullptr;
   a.idx = nullptr;
   a.mask_shift = 0;
+  a.mask_kv = false;
   a.pool_r = nullptr;
   a.gt = nullptr;
   a.split_parts = 0;
@@ -245,7 +247,7 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   if (!q || !k || !wq || !wk || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
   const int nb = blocks_of(desc->seq_len, gate->block);
-  if (out->n_blocks != nb) return SEER_ERR_INVALID_ARG;
+  if (out->n_blocks != nb || out->kv_shared != gate->kv_shared) return SEER_ERR_INVALID_ARG;
   const bool logits_in_ws = logits_out == nullptr;
   const GateLayout L = gate_layout(desc, gate, logits_in_ws);
   if (!workspace || workspace_bytes < L.total) return SEER_ERR_WORKSPACE;
@@ -305,6 +307,7 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   sa.head_thresholds = gate->mode == SEER_THRESHOLD ? gate->head_thresholds : nullptr;
   sa.keep_first = gate->keep_first ? 1 : 0;
   sa.keep_diag = gate->keep_diag ? 1 : 0;
+  sa.group = gate->kv_shared ? desc->heads_q / desc->heads_kv : 0;
   sa.count = out->count;
   sa.idx = out->idx;
   sa.dense = out->dense;
@@ -322,6 +325,7 @@ static seer_status attn_common(const seer_attn_desc* desc, int32_t block, const 
     if (block != 64 && block != 128) return SEER_ERR_UNSUPPORTED;
     const int nbm = blocks_of(desc->seq_len, block);
     if (!mask->count || !mask->idx || mask->n_blocks != nbm) return SEER_ERR_INVALID_ARG;
+    if (mask->kv_shared != 0 && mask->kv_shared != 1) return SEER_ERR_INVALID_ARG;
     if (nbm > 65536) return SEER_ERR_UNSUPPORTED;
   }
   seer::AttnArgs a = attn_args(desc, causal, sm_scale, q, k, v, o, lse);
@@ -329,7 +333,8 @@ static seer_status attn_common(const seer_attn_desc* desc, int32_t block, const 
   a.idx = mask ? mask->idx : nullptr;
   a.mask_shift = (mask && block == 128) ? 1 : 0;
   a.mask_blocks = mask ? mask->n_blocks : 0;
-  if (workspace && a.mask_shift == 0) {  // the split runs on 64-token masks
+  a.mask_kv = mask && mask->kv_shared;
+  if (workspace && a.mask_shift == 0 && !a.mask_kv) {  // the split runs on per-head 64-token masks
     if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
     const SplitLayout L = split_layout(desc, split_parts_for(desc, causal, mask != nullptr));
     if (L.w > 0 && workspace_bytes >= L.total) {  // key-range split
@@ -387,10 +392,12 @@ seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, cons
   if (block != 64 && block != 128) return SEER_ERR_UNSUPPORTED;
   const int nb = blocks_of(desc->seq_len, block);
   if (out->n_blocks != nb) return SEER_ERR_INVALID_ARG;
+  if (out->kv_shared != 0 && out->kv_shared != 1) return SEER_ERR_INVALID_ARG;
+  if (out->kv_shared && (desc->heads_kv <= 0 || desc->heads_q % desc->heads_kv != 0)) return SEER_ERR_INVALID_ARG;
   if (nb > 4096) return SEER_ERR_UNSUPPORTED;
   seer::MaskFromDenseArgs a;
   a.dense = dense;
-  a.rows = (int64_t)desc->batch * desc->heads_q * nb;
+  a.rows = (int64_t)desc->batch * (out->kv_shared ? desc->heads_kv : desc->heads_q) * nb;
   a.n_blocks = nb;
   a.count = out->count;
   a.idx = out->idx;
@@ -459,6 +466,7 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
                               size_t workspace_bytes, void* stream) {
   seer_status s = check_gate_common(desc, gate);
   if (s != SEER_OK) return s;
+  if (gate->kv_shared) return SEER_ERR_UNSUPPORTED;  // the distillation target is per query head
   if (!q || !k || !wq || !wk || !gt || !loss || !dwq || !dwk) return SEER_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
   const DistillLayout W = distill_layout(desc, gate);

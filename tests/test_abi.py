@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert seer.abi_version() == 1
+    assert seer.abi_version() == 2
     assert seer.status_str(0) == "SEER_OK"
     assert seer.status_str(3) == "SEER_ERR_WORKSPACE"
     assert seer.status_str(99) == "SEER_ERR_UNKNOWN"
@@ -253,3 +253,24 @@ def test_partial_last_block_sizes():
     assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 0) == up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4)
     assert L.seer_attn_gt_workspace_bytes(C.byref(d), 64, 0) == 4 * nb * nb * 64 * 4
     assert _call_gate(d, g, mask_nb=15) == seer.ERR_INVALID_ARG
+
+
+def test_kv_shared_flags_are_validated():
+    """The shared-mask variant: the gate's and the mask's kv_shared flags must
+    agree and be 0 or 1; the distillation step is per head only."""
+    L = seer.lib()
+    d = _desc()
+    m = seer.BlockMaskStruct()
+    m.n_blocks, m.count, m.idx, m.dense = 16, FAKE, FAKE, None
+    m.kv_shared = 0
+    g = _gate(kv_shared=1)  # mask rows per KV head requested, mask says per query head
+    assert L.seer_gate(C.byref(d), C.byref(g), FAKE, FAKE, FAKE, FAKE, C.byref(m), None, FAKE * 16,
+                       1 << 40, None) == seer.ERR_INVALID_ARG
+    assert _call_gate(_desc(), _gate(kv_shared=2)) == seer.ERR_INVALID_ARG
+    m.kv_shared = 2
+    args = (FAKE, FAKE, FAKE, FAKE, None, None)
+    assert L.seer_bsattn(C.byref(d), 64, C.byref(m), 1, 0.0, *args) == seer.ERR_INVALID_ARG
+    assert L.seer_mask_from_dense(C.byref(d), 64, FAKE, C.byref(m), None) == seer.ERR_INVALID_ARG
+    gt = _gate(kv_shared=1)
+    assert L.seer_gate_distill(C.byref(d), C.byref(gt), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                               FAKE * 16, 1 << 40, None) == seer.ERR_UNSUPPORTED

@@ -653,3 +653,51 @@ def test_distill_zero_at_the_optimum_and_descent():
     l0, gq, gk = oracle.distill(q2, k2, wq2, wk2, gt2)
     l1 = oracle.distill(q2, k2, wq2 - 1e-2 * gq / np.abs(gq).max(), wk2 - 1e-2 * gk / np.abs(gk).max(), gt2)[0]
     assert l1 < l0
+
+
+# --------------------------------------------------------------------------
+# shared-mask variant: one mask per KV group, scored by the mean of the
+# group's head probabilities (the paper's gate is per head, section 3.1)
+# --------------------------------------------------------------------------
+
+def test_group_select_hand_fixture():
+    g = json.load(open(os.path.join(GOLDEN, "group_select.json")))
+    nb, i = g["n_blocks"], g["row"]
+    ell = np.full((1, g["heads_q"], nb, nb), -np.inf)
+    for h in range(g["heads_q"]):
+        for r in range(nb):  # rows other than the asserted one: uniform over their causal blocks
+            ell[0, h, r, :r + 1] = -math.log(r + 1)
+    ell[0, 0, i, :] = np.log(g["p_head0"])
+    ell[0, 1, i, :] = np.log(g["p_head1"])
+    ellg = oracle.group_logscore(ell, g["heads_kv"])
+    modes = {"topk_fixed": oracle.TOPK_FIXED, "topk_ratio": oracle.TOPK_RATIO, "threshold": oracle.THRESHOLD}
+    for c in g["cases"]:
+        sel = oracle.select(ellg, modes[c["mode"]], rho=c.get("rho", 0.0), k=c.get("k", 0),
+                            thresholds=np.array([c.get("threshold", 0.0)], np.float32),
+                            keep_first=c["keep_first"], keep_diag=c["keep_diag"])
+        want = np.zeros(nb, np.uint8)
+        want[c["selected"]] = 1
+        np.testing.assert_array_equal(sel["mask"][0, 0, i], want, err_msg=str(c))
+
+
+def test_group_score_of_one_head_is_the_head_score():
+    ell = oracle.gate_logscore(_rand((2, 3, 9, 9), 80).astype(np.float64) + np.triu(np.full((9, 9), -np.inf), 1))
+    np.testing.assert_array_equal(oracle.group_logscore(ell, 3), ell)
+    for mode, kw in ((oracle.TOPK_RATIO, dict(rho=0.4)), (oracle.THRESHOLD, dict(thresholds=np.float32(0.1)))):
+        a = oracle.select(oracle.group_logscore(ell, 3), mode, **kw)
+        b = oracle.select(ell, mode, **kw)
+        np.testing.assert_array_equal(a["mask"], b["mask"])
+
+
+def test_group_score_of_identical_heads_and_row_sums():
+    nb = 11
+    tri = np.triu(np.full((nb, nb), -np.inf), 1)
+    one = oracle.gate_logscore(_rand((1, 2, nb, nb), 81).astype(np.float64) + tri)
+    ell = np.repeat(one, 4, axis=1)  # 2 KV groups of 4 identical heads
+    ellg = oracle.group_logscore(ell, 2)
+    np.testing.assert_allclose(ellg, one, rtol=0, atol=1e-13)
+    # the group's scores are a distribution over the causal blocks of each row
+    mixed = oracle.gate_logscore(_rand((1, 8, nb, nb), 82).astype(np.float64) + tri)
+    p = np.exp(oracle.group_logscore(mixed, 2))
+    np.testing.assert_allclose(p.sum(-1), 1.0, rtol=0, atol=1e-12)
+    assert np.all(p[..., np.triu_indices(nb, 1)[0], np.triu_indices(nb, 1)[1]] == 0)
