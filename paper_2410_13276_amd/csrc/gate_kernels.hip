@@ -7,7 +7,7 @@
 //                       GEMV reuses each weight element for every block of the
 //                       workgroup.
 //   gate_logits_kernel  Eq. 1: Qg Kg^T / sqrt(Dg) on the block-causal lower
-//                       triangle, fp32 MFMA (v_mfma_f32_32x32x2_f32), 64x64 tiles.
+//                       triangle, fp32 MFMA (v_mfma_f32_32x32x2_f32), 128x128 tiles.
 //   select_kernel       Eq. 3 (TopK by exact radix select on order-preserving
 //                       keys, 8-bit digits from a per-wavefront LDS histogram,
 //                       ties to the smaller block index) or Eq. 4 (strict
@@ -227,11 +227,13 @@ hipError_t launch_pool_proj(const PoolProjArgs& a, hipStream_t s) {
 // gate logits: L = Qg Kg^T * scale on 64x64 lower-triangular tiles
 // ---------------------------------------------------------------------------
 
-// Each of the 4 wavefronts computes a 32x32 sub-tile with v_mfma_f32_32x32x2_f32.
-// Operand lanes: A (rows i of Qg) and B (rows j of Kg) both hold, in lane half
-// hf = lane/32 and MFMA step v of group u, the gate feature 8u + 4hf + v, so the
-// contraction pairs identical features.  Output lane holds column j = lane%32 and
-// rows 8*(e/4) + 4*hf + e%4 of its 32x32 sub-tile (e = accumulator index).
+// Each of the 4 wavefronts computes a 64x64 sub-tile of a 128x128 tile as 2x2
+// blocks of 32x32 with v_mfma_f32_32x32x2_f32 (each operand row read from L2
+// serves two blocks).  Operand lanes: A (rows i of Qg) and B (rows j of Kg)
+// both hold, in lane half hf = lane/32 and MFMA step v of group u, the gate
+// feature 8u + 4hf + v, so the contraction pairs identical features.  Output
+// lane holds column j = lane%32 and rows 8*(e/4) + 4*hf + e%4 of a 32x32 block
+// (e = accumulator index).  Blocks entirely above the diagonal are skipped.
 template <int DG>
 __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
   const int nb = a.n_blocks;
@@ -249,39 +251,63 @@ __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
   const int lane = threadIdx.x % kWave;
   const int wi = wave / 2, wj = wave % 2;
   if (I == J && wj > wi) return;  // sub-tile entirely above the diagonal
-  const int i0 = I * 64 + wi * 32;
-  const int j0 = J * 64 + wj * 32;
+  const int i0 = I * 128 + wi * 64;
+  const int j0 = J * 128 + wj * 64;
   if (i0 >= nb || j0 >= nb) return;
+  const bool diag = I == J && wi == wj;  // block (0, 1) of this sub-tile lies above the diagonal
   const int hf = lane / 32;
-  const int ra = min(i0 + lane % 32, nb - 1);
-  const int rb = min(j0 + lane % 32, nb - 1);
-  const float* qrow = a.qg + (((int64_t)b * a.heads_q + h) * nb + ra) * DG + 4 * hf;
-  const float* krow = a.kg + (((int64_t)b * a.heads_kv + g) * nb + rb) * DG + 4 * hf;
-
-  f32x16 acc;
+  const float* qbase = a.qg + ((int64_t)b * a.heads_q + h) * nb * DG + 4 * hf;
+  const float* kbase = a.kg + ((int64_t)b * a.heads_kv + g) * nb * DG + 4 * hf;
+  const float* qrow[2];
+  const float* krow[2];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-#pragma unroll 4
-  for (int u = 0; u < DG / 8; ++u) {
-    const f32x4 qa = *reinterpret_cast<const f32x4*>(qrow + 8 * u);
-    const f32x4 kb = *reinterpret_cast<const f32x4*>(krow + 8 * u);
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[0], kb[0], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[1], kb[1], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[2], kb[2], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[3], kb[3], acc, 0, 0, 0);
+  for (int s = 0; s < 2; ++s) {
+    qrow[s] = qbase + (int64_t)min(i0 + 32 * s + lane % 32, nb - 1) * DG;
+    krow[s] = kbase + (int64_t)min(j0 + 32 * s + lane % 32, nb - 1) * DG;
   }
-  const int jcol = j0 + lane % 32;
-  if (jcol >= nb) return;
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[r][c][e] = 0.f;
+#pragma unroll 2
+  for (int u = 0; u < DG / 8; ++u) {
+    f32x4 qa[2], kb[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      qa[s] = *reinterpret_cast<const f32x4*>(qrow[s] + 8 * u);
+      kb[s] = *reinterpret_cast<const f32x4*>(krow[s] + 8 * u);
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+          if (!(diag && c > r))
+            acc[r][c] = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[r][v], kb[c][v], acc[r][c], 0, 0, 0);
+  }
   float* out = a.logits + ((int64_t)b * a.heads_q + h) * nb * nb;
 #pragma unroll
-  for (int e = 0; e < 16; ++e) {
-    const int irow = i0 + 8 * (e / 4) + 4 * hf + (e % 4);
-    if (irow < nb) out[(int64_t)irow * nb + jcol] = acc[e] * a.scale;
-  }
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      if (diag && c > r) continue;
+      const int jcol = j0 + 32 * c + lane % 32;
+      if (jcol >= nb) continue;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int irow = i0 + 32 * r + 8 * (e / 4) + 4 * hf + (e % 4);
+        if (irow < nb) out[(int64_t)irow * nb + jcol] = acc[r][c][e] * a.scale;
+      }
+    }
 }
 
 hipError_t launch_gate_logits(const GateLogitsArgs& a, hipStream_t s) {
-  const int T = (a.n_blocks + 63) / 64;
+  const int T = (a.n_blocks + 127) / 128;
   dim3 grid(T * (T + 1) / 2, a.heads_q, a.batch);
   switch (a.gate_dim) {
     case 32: hipLaunchKernelGGL(gate_logits_kernel<32>, grid, dim3(256), 0, s, a); break;
