@@ -122,7 +122,7 @@ def main() -> int:
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the SeerAttention prefill path here is the "
               "single-GPU kernel pair (gate + block-sparse attention); multi-GPU runs are not "
-              "part of this build (see DESIGN.md for how it would shard by KV-head group).",
+              "supported (the path would shard by KV-head group, one group set per GPU).",
               file=sys.stderr)
         return 2
 
@@ -294,6 +294,11 @@ def main() -> int:
     attn_kernels = (f"split_bounds_kernel + attn_fwd_bf16_kernel<{D}, true, true, {rg}> + split_merge_kernel<{D}> "
                     "(one seer_bsattn_ws call)" if sparse_split else f"attn_fwd_bf16_kernel<{D}, true, false, {rg}>")
     attn_tflops = active_flops / (attn_ms * 1e-3) / 1e12
+    # one seer_bsattn call is one launch per KV group when a group's K and V alone
+    # fill the task order's 64 MiB phase budget (the library's launch rule), else one
+    kv_group_bytes = 2 * nb * 64 * D * 2
+    launches = w.batch * w.heads_kv if (kv_group_bytes >= 64 * 2 ** 20 and w.batch * w.heads_kv > 1
+                                        and not sparse_split and w.dtype == "bf16") else 1
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     speedup = dense_ms / attn_ms
     result = {
@@ -343,7 +348,12 @@ def main() -> int:
         "roofline": {"bound": "mfma", "kernel": attn_kernels,
                      "achieved": round(attn_tflops, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(attn_tflops / peak, 4), "traffic": _traffic(w.name),
-                     "flops_per_launch": active_flops},
+                     "launches_per_call": launches,
+                     "flops_per_launch": active_flops / launches,
+                     "launch_avg_ms": round(attn_ms / launches, 4),
+                     "note": "achieved = active-tile flops of one call / the call's mean HIP-event "
+                             "duration = flops_per_launch / launch_avg_ms (the call's launches run "
+                             "back to back on the stream)"},
     }
     log(f"[bench] step {ms_step:.3f} ms (gate {gate_ms:.3f} + attn {attn_ms:.3f}); "
         f"attn {attn_tflops:.1f} TF/s; dense {dense_ms:.2f} ms; speedup {speedup:.2f}x "
