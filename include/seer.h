@@ -20,6 +20,8 @@
  *                    appendix A.1)
  *   seer_gate_distill  the gate's distillation step (section 3.2, Eq. 2):
  *                    KL(ground truth || gate score) and its weight gradients
+ *   seer_gate_varlen, seer_bsattn_varlen  the gate and block-sparse attention
+ *                    of a packed batch of variable-length sequences
  *
  * Conventions shared by every entry point:
  *  - Pointers to tensors are DEVICE pointers (HIP device memory of the current
@@ -295,6 +297,50 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
                               const void* q, const void* k, const float* wq, const float* wk,
                               const float* gt, float* loss, float* dwq, float* dwk,
                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Packed variable-length batches (the prefill layout of a serving batch):
+ * desc->batch sequences, sequence b holding tokens [cu_seqlens_host[b],
+ * cu_seqlens_host[b + 1]) of packed Q/K/V/O.  cu_seqlens_host is a host array
+ * of batch + 1 non-decreasing offsets with cu[0] = 0 and cu[batch] =
+ * desc->seq_len (the total token count); a sequence may be empty.  Strides come
+ * from desc: q_stride[2] is the token stride and q_stride[1] the head stride
+ * (q_stride[0] is ignored), e.g. [T][H][D] packing.  Every sequence is its own
+ * causal (or non-causal) problem: no attention or pooling crosses a boundary,
+ * and each has nb_b = ceil(len_b / block) blocks.  The calls run one batch-1
+ * pass per sequence on `stream`, through the same kernels as seer_gate /
+ * seer_bsattn (so results equal separate per-sequence calls bit for bit);
+ * arguments of every sequence are validated before anything is launched.
+ *
+ * Mask layout: the sequences' row sets back to back.  Sequence b's count rows
+ * [H][nb_b] start at element sum_{b'<b} H nb_b' of mask->count, and its idx
+ * rows [H][nb_b][nb_b] at element sum_{b'<b} H nb_b'^2 of mask->idx (and of
+ * mask->dense when present); H = heads_q, or heads_kv when kv_shared.
+ * mask->n_blocks is ignored.  LSE (optional) is stored per sequence as
+ * [heads_q][len_b] starting at element heads_q * cu[b].
+ */
+
+/* Elements of the idx array of a packed variable-length mask (0 on invalid
+ * arguments); *count_elems (if not NULL) receives the elements of count. */
+size_t seer_varlen_mask_elems(const seer_attn_desc* desc, const int32_t* cu_seqlens_host, int32_t block,
+                              int32_t kv_shared, size_t* count_elems);
+
+/* Workspace bytes of seer_gate_varlen: the largest sequence's seer_gate workspace
+ * with the logits in the workspace (0 on invalid arguments). */
+size_t seer_gate_varlen_workspace_bytes(const seer_attn_desc* desc, const int32_t* cu_seqlens_host,
+                                        const seer_gate_desc* gate);
+
+/* seer_gate over every sequence of a packed batch (section 3.1, Eq. 1, Eq. 3 / 4
+ * per sequence); the workspace is reused by the sequences in stream order. */
+seer_status seer_gate_varlen(const seer_attn_desc* desc, const int32_t* cu_seqlens_host,
+                             const seer_gate_desc* gate, const void* q, const void* k, const float* wq,
+                             const float* wk, seer_block_mask* out, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/* seer_bsattn over every sequence of a packed batch (section 3.3 per sequence). */
+seer_status seer_bsattn_varlen(const seer_attn_desc* desc, const int32_t* cu_seqlens_host, int32_t block,
+                               const seer_block_mask* mask, int32_t causal, float sm_scale, const void* q,
+                               const void* k, const void* v, void* o, float* lse, void* stream);
 
 #ifdef __cplusplus
 }

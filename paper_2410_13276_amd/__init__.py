@@ -68,6 +68,10 @@ _SIGS = {
     "seer_gate_distill": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P], C.c_int),
     "seer_attn_gt": ([_P, C.c_int32, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P],
                      C.c_int),
+    "seer_varlen_mask_elems": ([_P, _P, C.c_int32, C.c_int32, _P], C.c_size_t),
+    "seer_gate_varlen_workspace_bytes": ([_P, _P, _P], C.c_size_t),
+    "seer_gate_varlen": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P], C.c_int),
+    "seer_bsattn_varlen": ([_P, _P, C.c_int32, _P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P], C.c_int),
 }
 
 _lib = None
@@ -397,3 +401,119 @@ def mask_from_dense(dense, heads_kv: int = 1, mask: Optional[BlockMask] = None,
                                     _stream(stream))
     _check(st, "seer_mask_from_dense")
     return mask
+
+
+# ---------------------------------------------------------------------------
+# packed variable-length batches
+# ---------------------------------------------------------------------------
+
+def make_varlen_desc(q, k, cu_seqlens, v=None, o=None) -> AttnDesc:
+    """Descriptor of packed [T, H, D] tensors holding len(cu_seqlens) - 1 sequences."""
+    for name, t in (("q", q), ("k", k), ("v", v), ("o", o)):
+        if t is not None and (t.dim() != 3 or t.stride(2) != 1):
+            raise ValueError(f"{name} must be packed [tokens, heads, head_dim] with unit last stride")
+    d = AttnDesc()
+    d.batch = len(cu_seqlens) - 1
+    d.heads_q, d.seq_len, d.head_dim = q.shape[1], q.shape[0], q.shape[2]
+    d.heads_kv = k.shape[1]
+    d.dtype = _dtype_code(q)
+    for field, t in (("q_stride", q), ("k_stride", k), ("v_stride", v if v is not None else k),
+                     ("o_stride", o if o is not None else q)):
+        arr = getattr(d, field)
+        arr[0], arr[1], arr[2] = 0, t.stride(1), t.stride(0)
+    return d
+
+
+def _cu_host(cu_seqlens):
+    cu = [int(x) for x in (cu_seqlens.tolist() if hasattr(cu_seqlens, "tolist") else cu_seqlens)]
+    return (C.c_int32 * len(cu))(*cu), cu
+
+
+@dataclass
+class VarlenMask:
+    """Block masks of a packed batch: sequence b's count rows [H, nb_b] and idx rows
+    [H, nb_b, nb_b] stored back to back in flat device arrays."""
+    count: object  # int32 [sum_b H nb_b]
+    idx: object    # int16 storage of uint16 [sum_b H nb_b^2]
+    cu_seqlens: list
+    heads: int
+    block: int = BLOCK
+    kv_shared: bool = False
+    dense: Optional[object] = None  # uint8, same layout as idx
+
+    def struct(self) -> BlockMaskStruct:
+        m = BlockMaskStruct()
+        m.n_blocks = 0
+        m.count = _ptr(self.count)
+        m.idx = _ptr(self.idx)
+        m.dense = _ptr(self.dense)
+        m.kv_shared = int(bool(self.kv_shared))
+        return m
+
+    def sequence(self, b: int):
+        """(count [H, nb_b], idx [H, nb_b, nb_b]) views of sequence b."""
+        nbs = [-(-(self.cu_seqlens[s + 1] - self.cu_seqlens[s]) // self.block) for s in range(len(self.cu_seqlens) - 1)]
+        c0 = sum(self.heads * n for n in nbs[:b])
+        i0 = sum(self.heads * n * n for n in nbs[:b])
+        nb = nbs[b]
+        return (self.count[c0:c0 + self.heads * nb].view(self.heads, nb),
+                self.idx[i0:i0 + self.heads * nb * nb].view(self.heads, nb, nb))
+
+
+def alloc_varlen_mask(q, k, cu_seqlens, block: int = BLOCK, kv_shared: bool = False,
+                      dense: bool = False) -> VarlenMask:
+    torch = _torch()
+    cu_arr, cu = _cu_host(cu_seqlens)
+    d = make_varlen_desc(q, k, cu)
+    n_count = C.c_size_t(0)
+    n_idx = lib().seer_varlen_mask_elems(C.byref(d), cu_arr, block, int(bool(kv_shared)), C.byref(n_count))
+    if n_idx == 0 and cu[-1] > 0:
+        raise ValueError("invalid packed batch description")
+    heads = k.shape[1] if kv_shared else q.shape[1]
+    return VarlenMask(count=torch.empty(max(n_count.value, 1), dtype=torch.int32, device=q.device),
+                      idx=torch.empty(max(n_idx, 1), dtype=torch.int16, device=q.device), cu_seqlens=cu,
+                      heads=heads, block=block, kv_shared=kv_shared,
+                      dense=torch.empty(max(n_idx, 1), dtype=torch.uint8, device=q.device) if dense else None)
+
+
+def gate_varlen(q, k, wq, wk, cu_seqlens, *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
+                threshold: float = 0.0, head_thresholds=None, keep_first: bool = True, keep_diag: bool = True,
+                w_per_head: bool = True, rope_theta: float = 0.0, block: int = BLOCK, kv_shared: bool = False,
+                mask: Optional[VarlenMask] = None, dense_out: bool = False, workspace=None,
+                stream=None) -> VarlenMask:
+    """seer_gate_varlen: the gate of every sequence of a packed [T, H, D] batch."""
+    torch = _torch()
+    cu_arr, cu = _cu_host(cu_seqlens)
+    d = make_varlen_desc(q, k, cu)
+    gd = gate_desc(wq.shape[-1], mode, topk_ratio, topk_k, threshold, head_thresholds,
+                   keep_first, keep_diag, w_per_head, rope_theta, block, kv_shared)
+    if mask is None:
+        mask = alloc_varlen_mask(q, k, cu, block, kv_shared, dense_out)
+    need = lib().seer_gate_varlen_workspace_bytes(C.byref(d), cu_arr, C.byref(gd))
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    ms = mask.struct()
+    st = lib().seer_gate_varlen(C.byref(d), cu_arr, C.byref(gd), _ptr(q), _ptr(k), _ptr(wq), _ptr(wk),
+                                C.byref(ms), _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "seer_gate_varlen")
+    return mask
+
+
+def bsattn_varlen(q, k, v, cu_seqlens, mask: VarlenMask, *, causal: bool = True, sm_scale: float = 0.0,
+                  out=None, lse=None, want_lse: bool = False, stream=None):
+    """seer_bsattn_varlen: block-sparse attention of every sequence of a packed batch.
+    Returns (O [T, Hq, D], LSE or None); LSE is flat, sequence b's [Hq, len_b] block
+    starting at element Hq * cu[b]."""
+    torch = _torch()
+    cu_arr, cu = _cu_host(cu_seqlens)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty(max(q.shape[0] * q.shape[1], 1), dtype=torch.float32, device=q.device)
+    d = make_varlen_desc(q, k, cu, v, out)
+    ms = mask.struct()
+    st = lib().seer_bsattn_varlen(C.byref(d), cu_arr, mask.block, C.byref(ms), int(bool(causal)),
+                                  float(sm_scale), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+                                  _stream(stream))
+    _check(st, "seer_bsattn_varlen")
+    return out, lse

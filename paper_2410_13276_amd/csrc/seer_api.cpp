@@ -605,3 +605,155 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// packed variable-length batches: one batch-1 pass per sequence on the stream
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// Checks cu_seqlens and builds the batch-1 descriptor of sequence b (strides of
+// the packed layout; tokens [cu[b], cu[b+1])).
+seer_status check_cu(const seer_attn_desc* d, const int32_t* cu) {
+  if (!d || !cu || d->batch <= 0) return SEER_ERR_INVALID_ARG;
+  if (cu[0] != 0) return SEER_ERR_INVALID_ARG;
+  for (int b = 0; b < d->batch; ++b)
+    if (cu[b + 1] < cu[b]) return SEER_ERR_INVALID_ARG;
+  if (cu[d->batch] != d->seq_len) return SEER_ERR_INVALID_ARG;
+  return SEER_OK;
+}
+
+seer_attn_desc seq_desc(const seer_attn_desc* d, const int32_t* cu, int b) {
+  seer_attn_desc s = *d;
+  s.batch = 1;
+  s.seq_len = cu[b + 1] - cu[b];
+  s.q_stride[0] = s.k_stride[0] = s.v_stride[0] = s.o_stride[0] = 0;
+  return s;
+}
+
+const void* at_token(const void* p, const int64_t* st, int64_t t, size_t es) {
+  return p ? static_cast<const char*>(p) + (size_t)(t * st[2]) * es : nullptr;
+}
+
+struct VarlenMaskOffsets {
+  int64_t count, idx;
+};
+
+// Offsets of sequence b's rows in a packed variable-length mask: count rows
+// [H][nb_b] and idx rows [H][nb_b][nb_b] of the sequences before it.
+VarlenMaskOffsets varlen_mask_offsets(const int32_t* cu, int b, int heads, int block) {
+  VarlenMaskOffsets o{0, 0};
+  for (int s = 0; s < b; ++s) {
+    const int64_t nb = blocks_of(cu[s + 1] - cu[s], block);
+    o.count += heads * nb;
+    o.idx += heads * nb * nb;
+  }
+  return o;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t seer_varlen_mask_elems(const seer_attn_desc* desc, const int32_t* cu_seqlens_host, int32_t block,
+                              int32_t kv_shared, size_t* count_elems) {
+  if (check_cu(desc, cu_seqlens_host) != SEER_OK || (block != 64 && block != 128) || desc->heads_q <= 0 ||
+      desc->heads_kv <= 0 || desc->heads_q % desc->heads_kv != 0)
+    return 0;
+  const int heads = kv_shared ? desc->heads_kv : desc->heads_q;
+  const VarlenMaskOffsets o = varlen_mask_offsets(cu_seqlens_host, desc->batch, heads, block);
+  if (count_elems) *count_elems = (size_t)o.count;
+  return (size_t)o.idx;
+}
+
+size_t seer_gate_varlen_workspace_bytes(const seer_attn_desc* desc, const int32_t* cu_seqlens_host,
+                                        const seer_gate_desc* gate) {
+  if (check_cu(desc, cu_seqlens_host) != SEER_OK) return 0;
+  size_t need = 0;
+  for (int b = 0; b < desc->batch; ++b) {
+    const seer_attn_desc sd = seq_desc(desc, cu_seqlens_host, b);
+    if (sd.seq_len == 0) continue;
+    if (check_gate(&sd, gate) != SEER_OK) return 0;
+    need = std::max(need, gate_layout(&sd, gate, true).total);
+  }
+  return need;
+}
+
+seer_status seer_gate_varlen(const seer_attn_desc* desc, const int32_t* cu_seqlens_host,
+                             const seer_gate_desc* gate, const void* q, const void* k, const float* wq,
+                             const float* wk, seer_block_mask* out, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  seer_status s = check_cu(desc, cu_seqlens_host);
+  if (s != SEER_OK) return s;
+  if (!gate || !out || !out->count || !out->idx || !q || !k) return SEER_ERR_INVALID_ARG;
+  if (out->kv_shared != gate->kv_shared) return SEER_ERR_INVALID_ARG;
+  const size_t es = elem_size(desc->dtype);
+  const int heads = gate->kv_shared ? desc->heads_kv : desc->heads_q;
+  // validate every sequence before launching anything
+  for (int b = 0; b < desc->batch; ++b) {
+    const seer_attn_desc sd = seq_desc(desc, cu_seqlens_host, b);
+    if (sd.seq_len == 0) continue;
+    if ((s = check_gate(&sd, gate)) != SEER_OK) return s;
+    if (workspace_bytes < gate_layout(&sd, gate, true).total || !workspace) return SEER_ERR_WORKSPACE;
+    if (!aligned16(at_token(q, desc->q_stride, cu_seqlens_host[b], es)) ||
+        !aligned16(at_token(k, desc->k_stride, cu_seqlens_host[b], es)))
+      return SEER_ERR_INVALID_ARG;
+  }
+  for (int b = 0; b < desc->batch; ++b) {
+    const seer_attn_desc sd = seq_desc(desc, cu_seqlens_host, b);
+    if (sd.seq_len == 0) continue;
+    const VarlenMaskOffsets o = varlen_mask_offsets(cu_seqlens_host, b, heads, gate->block);
+    seer_block_mask m = *out;
+    m.n_blocks = blocks_of(sd.seq_len, gate->block);
+    m.count = out->count + o.count;
+    m.idx = out->idx + o.idx;
+    m.dense = out->dense ? out->dense + o.idx : nullptr;
+    s = seer_gate(&sd, gate, at_token(q, desc->q_stride, cu_seqlens_host[b], es),
+                  at_token(k, desc->k_stride, cu_seqlens_host[b], es), wq, wk, &m, nullptr, workspace,
+                  workspace_bytes, stream);
+    if (s != SEER_OK) return s;
+  }
+  return SEER_OK;
+}
+
+seer_status seer_bsattn_varlen(const seer_attn_desc* desc, const int32_t* cu_seqlens_host, int32_t block,
+                               const seer_block_mask* mask, int32_t causal, float sm_scale, const void* q,
+                               const void* k, const void* v, void* o, float* lse, void* stream) {
+  seer_status s = check_cu(desc, cu_seqlens_host);
+  if (s != SEER_OK) return s;
+  if (!mask || !mask->count || !mask->idx) return SEER_ERR_INVALID_ARG;
+  if (block != 64 && block != 128) return SEER_ERR_UNSUPPORTED;
+  if (mask->kv_shared != 0 && mask->kv_shared != 1) return SEER_ERR_INVALID_ARG;
+  const size_t es = elem_size(desc->dtype);
+  const int heads = mask->kv_shared ? desc->heads_kv : desc->heads_q;
+  for (int b = 0; b < desc->batch; ++b) {
+    const seer_attn_desc sd = seq_desc(desc, cu_seqlens_host, b);
+    if (sd.seq_len == 0) continue;
+    if ((s = check_attn(&sd, sm_scale, at_token(q, desc->q_stride, cu_seqlens_host[b], es),
+                        at_token(k, desc->k_stride, cu_seqlens_host[b], es),
+                        at_token(v, desc->v_stride, cu_seqlens_host[b], es),
+                        at_token(o, desc->o_stride, cu_seqlens_host[b], es))) != SEER_OK)
+      return s;
+    if (blocks_of(sd.seq_len, block) > 65536) return SEER_ERR_UNSUPPORTED;
+  }
+  for (int b = 0; b < desc->batch; ++b) {
+    const seer_attn_desc sd = seq_desc(desc, cu_seqlens_host, b);
+    if (sd.seq_len == 0) continue;
+    const VarlenMaskOffsets mo = varlen_mask_offsets(cu_seqlens_host, b, heads, block);
+    seer_block_mask m = *mask;
+    m.n_blocks = blocks_of(sd.seq_len, block);
+    m.count = mask->count + mo.count;
+    m.idx = mask->idx + mo.idx;
+    m.dense = nullptr;
+    float* lb = lse ? lse + (int64_t)desc->heads_q * cu_seqlens_host[b] : nullptr;  // [Hq][len_b] per sequence
+    s = attn_common(&sd, block, &m, causal, sm_scale, at_token(q, desc->q_stride, cu_seqlens_host[b], es),
+                    at_token(k, desc->k_stride, cu_seqlens_host[b], es),
+                    at_token(v, desc->v_stride, cu_seqlens_host[b], es),
+                    const_cast<void*>(at_token(o, desc->o_stride, cu_seqlens_host[b], es)), lb, nullptr, 0,
+                    stream);
+    if (s != SEER_OK) return s;
+  }
+  return SEER_OK;
+}
+
+}  // extern "C"

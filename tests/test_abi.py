@@ -24,7 +24,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 15, names
+    assert len(names) == 19, names
     L = C.CDLL(seer.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -274,3 +274,27 @@ def test_kv_shared_flags_are_validated():
     gt = _gate(kv_shared=1)
     assert L.seer_gate_distill(C.byref(d), C.byref(gt), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                                FAKE * 16, 1 << 40, None) == seer.ERR_UNSUPPORTED
+
+
+def test_varlen_rejects_bad_offsets_and_sizes_the_mask():
+    L = seer.lib()
+    d = _desc(B=3, Hq=4, Hkv=2, S=300)
+    good = (C.c_int32 * 4)(0, 100, 100, 300)  # one empty sequence
+    n_count = C.c_size_t(0)
+    # nb = 2, 0, 4 blocks of 64: count 4 * (2 + 0 + 4), idx 4 * (4 + 0 + 16)
+    assert L.seer_varlen_mask_elems(C.byref(d), good, 64, 0, C.byref(n_count)) == 80
+    assert n_count.value == 24
+    assert L.seer_varlen_mask_elems(C.byref(d), good, 64, 1, C.byref(n_count)) == 40  # per KV head
+    m = seer.BlockMaskStruct()
+    m.n_blocks, m.count, m.idx, m.dense, m.kv_shared = 0, FAKE, FAKE, None, 0
+    g = _gate()
+    args = (FAKE, FAKE, FAKE, FAKE, None, None)
+    for bad in ((1, 100, 100, 300), (0, 200, 100, 300), (0, 100, 100, 299)):
+        cu = (C.c_int32 * 4)(*bad)
+        assert L.seer_varlen_mask_elems(C.byref(d), cu, 64, 0, None) == 0
+        assert L.seer_gate_varlen(C.byref(d), cu, C.byref(g), FAKE, FAKE, FAKE, FAKE, C.byref(m), FAKE * 16,
+                                  1 << 40, None) == seer.ERR_INVALID_ARG
+        assert L.seer_bsattn_varlen(C.byref(d), cu, 64, C.byref(m), 1, 0.0, *args) == seer.ERR_INVALID_ARG
+    assert L.seer_bsattn_varlen(C.byref(d), good, 96, C.byref(m), 1, 0.0, *args) == seer.ERR_UNSUPPORTED
+    assert L.seer_gate_varlen(C.byref(d), good, C.byref(g), FAKE, FAKE, FAKE, FAKE, C.byref(m), None, 0,
+                              None) == seer.ERR_WORKSPACE
