@@ -294,11 +294,14 @@ def main() -> int:
     attn_kernels = (f"split_bounds_kernel + attn_fwd_bf16_kernel<{D}, true, true, {rg}> + split_merge_kernel<{D}> "
                     "(one seer_bsattn_ws call)" if sparse_split else f"attn_fwd_bf16_kernel<{D}, true, false, {rg}>")
     attn_tflops = active_flops / (attn_ms * 1e-3) / 1e12
-    # one seer_bsattn call is one launch per KV group when a group's K and V alone
-    # fill the task order's 64 MiB phase budget (the library's launch rule), else one
-    kv_group_bytes = 2 * nb * 64 * D * 2
-    launches = w.batch * w.heads_kv if (kv_group_bytes >= 64 * 2 ** 20 and w.batch * w.heads_kv > 1
-                                        and not sparse_split and w.dtype == "bf16") else 1
+    # one seer_bsattn call is one launch per KV group when the task order's phases
+    # hold a single group (no phase of 2, 4 or 8 groups divides the groups, splits
+    # the query blocks evenly over the XCDs and keeps its K and V within 64 MiB),
+    # else one launch (the library's launch rule)
+    groups = w.batch * w.heads_kv
+    kv_group_bytes = 2 * nb * 64 * D * (2 if w.dtype == "bf16" else 4)
+    multi = any(groups % g == 0 and nb % (8 // g) == 0 and g * kv_group_bytes <= 64 * 2 ** 20 for g in (8, 4, 2))
+    launches = groups if (groups > 1 and not multi and not sparse_split) else 1
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     speedup = dense_ms / attn_ms
     result = {
