@@ -301,7 +301,7 @@ def main() -> int:
     groups = w.batch * w.heads_kv
     kv_group_bytes = 2 * nb * 64 * D * (2 if w.dtype == "bf16" else 4)
     multi = any(groups % g == 0 and nb % (8 // g) == 0 and g * kv_group_bytes <= 64 * 2 ** 20 for g in (8, 4, 2))
-    launches = groups if (groups > 1 and not multi and not sparse_split) else 1
+    launches = groups if (groups > 1 and not multi and nb % 8 == 0 and not sparse_split) else 1
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     speedup = dense_ms / attn_ms
     result = {
