@@ -342,13 +342,15 @@ __device__ __forceinline__ void emit_row(uint64_t sel, int nb, int64_t row, int3
   if (lane == 0) count[row] = base;
 }
 
-template <int MAXM>
+// GROUP: rows of a mask shared by a KV group (a separate instantiation, so the
+// per-head kernel keeps its register budget and occupancy).
+template <int MAXM, bool GROUP>
 __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_hist[4][256];  // per-wavefront digit histogram
   const int lane = threadIdx.x % kWave;
   const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
   const int nb = a.n_blocks;
-  const int G = a.group;  // > 0: rows of a mask shared by the G query heads of a KV group
+  const int G = GROUP ? a.group : 0;  // > 0: rows of a mask shared by the G query heads of a KV group
   const int mheads = G > 0 ? a.heads_q / G : a.heads_q;  // heads of the mask
   const int64_t rows = (int64_t)a.batch * mheads * nb;
   if (row >= rows) return;
@@ -359,18 +361,27 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   // per-lane bit m describes block j = 64m + lane
   float v[MAXM];
   uint64_t valid = 0, forced = 0;
-#pragma unroll
-  for (int m = 0; m < MAXM; ++m) {
-    const int j = 64 * m + lane;
-    const bool ok = m < M && j <= i;
-    valid |= (uint64_t)ok << m;
-    forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
-  }
-  if (G == 0) {
+  if constexpr (!GROUP) {
     const float* L = a.logits + row * nb;
 #pragma unroll
-    for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? L[64 * m + lane] : -INFINITY;
+    for (int m = 0; m < MAXM; ++m) {
+      v[m] = -INFINITY;
+      if (m < M) {
+        const int j = 64 * m + lane;
+        const bool ok = j <= i;
+        if (ok) v[m] = L[j];
+        valid |= (uint64_t)ok << m;
+        forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
+      }
+    }
   } else {
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) {
+      const int j = 64 * m + lane;
+      const bool ok = m < M && j <= i;
+      valid |= (uint64_t)ok << m;
+      forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
+    }
     // the group's score of block j: the mean over its query heads of their gate
     // probabilities, held as its logarithm so that TopK (by value) and the
     // threshold test (against the log of the row sum, 1) below apply unchanged
@@ -519,7 +530,8 @@ template <int MAXM>
 static hipError_t select_launch(const SelectArgs& a, hipStream_t s) {
   const int64_t rows = (int64_t)a.batch * (a.group > 0 ? a.heads_q / a.group : a.heads_q) * a.n_blocks;
   dim3 grid((unsigned)((rows + 3) / 4));
-  hipLaunchKernelGGL(select_kernel<MAXM>, grid, dim3(256), 0, s, a);
+  if (a.group > 0) hipLaunchKernelGGL((select_kernel<MAXM, true>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((select_kernel<MAXM, false>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
