@@ -296,11 +296,11 @@ def main() -> int:
     attn_tflops = active_flops / (attn_ms * 1e-3) / 1e12
     # one seer_bsattn call is one launch per KV group when the task order's phases
     # hold a single group (no phase of 2, 4 or 8 groups divides the groups, splits
-    # the query blocks evenly over the XCDs and keeps its K and V within 64 MiB),
+    # the query blocks evenly over the XCDs and keeps its K and V within 32 MiB),
     # else one launch (the library's launch rule)
     groups = w.batch * w.heads_kv
     kv_group_bytes = 2 * nb * 64 * D * (2 if w.dtype == "bf16" else 4)
-    multi = any(groups % g == 0 and nb % (8 // g) == 0 and g * kv_group_bytes <= 64 * 2 ** 20 for g in (8, 4, 2))
+    multi = any(groups % g == 0 and nb % (8 // g) == 0 and g * kv_group_bytes <= 32 * 2 ** 20 for g in (8, 4, 2))
     launches = groups if (groups > 1 and not multi and nb % 8 == 0 and not sparse_split) else 1
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     speedup = dense_ms / attn_ms

@@ -1027,13 +1027,17 @@ __global__ __launch_bounds__(256) void split_merge_kernel(AttnArgs a) {
     a.lse[bh * a.seq_len + 64 * i + q] = sum > 0.f ? (mx + __log2f(sum)) * 0.6931471805599453f : -INFINITY;
 }
 
-// Groups per phase: the largest power of two whose K + V stay within 64 MiB
-// (a quarter of the 256 MB Infinity Cache); each group is then spread over
-// R = 8 / gpp XCDs.  Measured at 131072 tokens (64 MiB of K + V per group):
-// one group at a time over all 8 XCDs beat one group per XCD by 11% (sparse)
-// and 7% (dense).
+// Groups per phase: the largest power of two whose K + V stay within 32 MiB;
+// each group is then spread over R = 8 / gpp XCDs.  Measured at 131072 tokens
+// (64 MiB of K + V per group): one group at a time over all 8 XCDs beat one
+// group per XCD by 11% (sparse) and 7% (dense).  At 65536 tokens with 7 query
+// heads per KV group and per-head densities of 5-40% (32 MiB per group), one
+// group at a time over all 8 XCDs beat two groups on 4 XCDs each by 17%: the
+// groups' unequal work no longer leaves half the XCDs idle at the end; 8k and
+// 32k shapes (4 and 16 MiB per group) ran the same with budgets of 32 and 64 MiB,
+// and slower with 16 or less.
 #ifndef SEER_KV_PHASE_BUDGET_MB
-#define SEER_KV_PHASE_BUDGET_MB 64
+#define SEER_KV_PHASE_BUDGET_MB 32
 #endif
 static TaskMap make_map(const AttnArgs& a) {
   TaskMap m;
