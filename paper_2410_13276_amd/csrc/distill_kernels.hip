@@ -10,7 +10,8 @@
 //                       workgroup, double accumulation: run-to-run identical).
 //   gemm_f32_kernel     fp32 strided batched products for the backward pass
 //                       (dQg = dL Kg, dKg = dL^T Qg, dW = pooled^T dG), 64x64
-//                       LDS tiles, triangular skipping of the causal zeros.
+//                       LDS tiles on fp32 MFMA, triangular skipping of the
+//                       causal zeros.
 //   rope_inverse_kernel rotates gradient rows back through the block-level
 //                       RoPE (the transpose of the forward rotation).
 #include "device_common.h"
@@ -80,8 +81,8 @@ __global__ __launch_bounds__(256) void loss_mean_kernel(const double* __restrict
   if (threadIdx.x == 0) loss[0] = (float)(part[0] / (double)rows);
 }
 
-// 64x64 output tile per 256-thread workgroup, 4x4 outputs per thread, K in
-// chunks of 16 staged through LDS.  Operand tiles are read along whichever
+// 64x64 output tile per 256-thread workgroup (a 32x32 fp32-MFMA block per
+// wavefront, v_mfma_f32_32x32x2_f32), K in chunks of 16 staged through LDS.  Operand tiles are read along whichever
 // index has unit stride, so that loads coalesce for every layout used here.
 constexpr int kT = 64;
 constexpr int kKc = 16;
@@ -94,12 +95,12 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
   const int z = blockIdx.z;
   const float* A = g.A + (int64_t)z * g.saz;
   const float* B = g.B + (int64_t)(z / g.bdiv) * g.sbz;
-  const int tx = t % 16, ty = t / 16;
-  float acc[4][4];
+  const int wave = t / kWave, lane = t % kWave;
+  const int wm = wave / 2, wn = wave % 2;
+  const int hf = lane / 32, col = lane % 32;
+  f32x16 acc;
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
-#pragma unroll
-    for (int b = 0; b < 4; ++b) acc[a][b] = 0.f;
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
 
   // k2 range that can hold non-zero A entries for this row tile
   int k2lo = 0, k2hi = g.K2;
@@ -125,30 +126,23 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
         sB[kb][n] = (gn < g.N && gkb < k2hi) ? Bk[(int64_t)gkb * g.sbk2 + (int64_t)gn * g.sbn] : 0.f;
       }
       __syncthreads();
+      // wavefront (wm, wn) accumulates the 32x32 block at rows 32 wm, columns 32 wn
+      // of the tile; each MFMA contracts the two k of one step, lane half hf
+      // supplying k = 2 s + hf of row (or column) lane % 32
 #pragma unroll
-      for (int k = 0; k < kKc; ++k) {
-        float av[4], bv[4];
-#pragma unroll
-        for (int a = 0; a < 4; ++a) av[a] = sA[k][ty * 4 + a];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) bv[b] = sB[k][tx * 4 + b];
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-#pragma unroll
-          for (int b = 0; b < 4; ++b) acc[a][b] = fmaf(av[a], bv[b], acc[a][b]);
-      }
+      for (int st = 0; st < kKc / 2; ++st)
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sA[2 * st + hf][32 * wm + col], sB[2 * st + hf][32 * wn + col],
+                                                   acc, 0, 0, 0);
       __syncthreads();
     }
   }
   float* C = g.C + (int64_t)z * g.scz;
+  const int n = n0 + 32 * wn + col;
+  if (n < g.N) {
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const int m = m0 + ty * 4 + a;
-    if (m >= g.M) continue;
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int n = n0 + tx * 4 + b;
-      if (n < g.N) C[(int64_t)m * g.scm + n] = g.alpha * acc[a][b];
+    for (int e = 0; e < 16; ++e) {
+      const int m = m0 + 32 * wm + 8 * (e / 4) + 4 * hf + (e % 4);
+      if (m < g.M) C[(int64_t)m * g.scm + n] = g.alpha * acc[e];
     }
   }
 }
