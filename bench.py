@@ -291,8 +291,8 @@ def main() -> int:
     D = w.head_dim
     sparse_split = aws is not None and os.environ.get("SEER_SPLIT_SPARSE") == "1"
     rg = "true" if w.seq_len % 64 else "false"  # partial last tile
-    attn_kernels = (f"split_bounds_kernel + attn_fwd_bf16_kernel<{D}, true, true, {rg}> + split_merge_kernel<{D}> "
-                    "(one seer_bsattn_ws call)" if sparse_split else f"attn_fwd_bf16_kernel<{D}, true, false, {rg}>")
+    attn_kernels = (f"split_bounds_kernel + attn_fwd_bf16_kernel<{D}, true, true, {rg}, 1> + split_merge_kernel<{D}> "
+                    "(one seer_bsattn_ws call)" if sparse_split else f"attn_fwd_bf16_kernel<{D}, true, false, {rg}, 1>")
     attn_tflops = active_flops / (attn_ms * 1e-3) / 1e12
     # one seer_bsattn call is one launch per KV group when the task order's phases
     # hold a single group (no phase of 2, 4 or 8 groups divides the groups, splits
