@@ -8,9 +8,11 @@
 //                       workgroup.
 //   gate_logits_kernel  Eq. 1: Qg Kg^T / sqrt(Dg) on the block-causal lower
 //                       triangle, fp32 MFMA (v_mfma_f32_32x32x2_f32), 128x128 tiles.
-//   select_kernel       Eq. 3 (TopK by exact radix select on order-preserving
-//                       keys, 8-bit digits from a per-wavefront LDS histogram,
-//                       ties to the smaller block index) or Eq. 4 (strict
+//   select_kernel       Eq. 3 (TopK by an exact select: one pass over 256
+//                       equal-width value buckets, then 8-bit digits of
+//                       order-preserving keys inside the target bucket, each
+//                       from a per-wavefront LDS histogram; ties to the smaller
+//                       block index) or Eq. 4 (strict
 //                       threshold on the row softmax), plus the always-kept first
 //                       and diagonal blocks; one wavefront per query-block row,
 //                       writing the ascending index list by ballot compaction.
@@ -444,29 +446,40 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
     if (take >= ncand) {
       sel = valid;
     } else if (take > 0) {
-      uint32_t key[MAXM];
+      // T: the largest value with #{candidates : value >= T} >= take.  The
+      // first digit is a bucket of 256 equal-width value ranges over the row's
+      // candidate [min, max]; the bucket index is non-decreasing in the value,
+      // so the bucket holding T is found from bucket counts.  Logits spread
+      // over their range, so this pass has few LDS-atomic collisions, where the
+      // top bits of the order-preserving keys are shared by almost every
+      // candidate.  Inside that bucket T is then found exactly, 8 key bits at
+      // a time.  Each pass histograms the candidates still in play in a
+      // per-wavefront LDS histogram; `above` counts candidates already known to
+      // lie above; once exactly `take` candidates lie at or above the current
+      // prefix the selected set is fixed.
+      float cmx = -INFINITY, cmn = INFINITY;
 #pragma unroll
-      for (int m = 0; m < MAXM; ++m) key[m] = ((cand >> m) & 1) ? ordered_key(v[m]) : 0u;
-      // T: the largest value with #{candidates : key >= T} >= take, found 8 bits
-      // at a time from a per-wavefront LDS histogram of the candidates that
-      // match the digits fixed so far.  `above` counts candidates whose fixed
-      // digits are already larger.  Once exactly `take` candidates lie at or
-      // above the current prefix the selected set is fixed (cntT == take).
-      // (Starting the digits below the bits all candidates share was measured
-      // slower: the extra reduction raised register use and cost occupancy.)
+      for (int m = 0; m < MAXM; ++m)
+        if (m < M && ((cand >> m) & 1)) {
+          cmx = fmaxf(cmx, v[m]);
+          cmn = fminf(cmn, v[m]);
+        }
+      cmx = wave_max(cmx);
+      cmn = -wave_max(-cmn);
+      const float span = cmx - cmn;
+      const float scale = (span > 0.f && span < INFINITY) ? 256.f / span : 0.f;
+      auto bucket = [&](float x) -> uint32_t {
+        return scale > 0.f ? (uint32_t)min(255, max(0, (int)((x - cmn) * scale))) : 0u;
+      };
       uint32_t* hist = s_hist[threadIdx.x / kWave];
-      uint32_t prefix = 0;
-      int above = 0;
-      int cntT = take + 1;  // != take until the set closes early
-      int shift = 0;
-      for (int d = 3; d >= 0; --d) {
-        const int sh = 8 * d;
+      // one histogram pass: digit(m) of the candidates with in_play(m); returns
+      // the target bin and the counts above it and in it
+      auto pass = [&](auto in_play, auto digit, int above_in, int& bin, int& abv, int& cb) {
         *reinterpret_cast<u32x4*>(hist + 4 * lane) = u32x4{0u, 0u, 0u, 0u};
         __builtin_amdgcn_wave_barrier();
 #pragma unroll
         for (int m = 0; m < MAXM; ++m)
-          if (m < M && ((cand >> m) & 1) && (d == 3 || (key[m] >> (sh + 8)) == prefix))
-            atomicAdd(hist + ((key[m] >> sh) & 255u), 1u);
+          if (m < M && ((cand >> m) & 1) && in_play(m)) atomicAdd(hist + digit(m), 1u);
         __builtin_amdgcn_wave_barrier();
         const u32x4 c = *reinterpret_cast<const u32x4*>(hist + 4 * lane);  // bins 4 lane .. +3
         const int local = (int)(c[0] + c[1] + c[2] + c[3]);
@@ -477,47 +490,69 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
           if (lane + off < kWave) incl += t;
         }
         // the target bin: the highest b with above + #{digit >= b} >= take
-        int run = above + (incl - local);
-        int found = -1, abv = 0, cb = 0;
+        int run = above_in + (incl - local);
+        int found = -1, ab = 0, cc = 0;
 #pragma unroll
         for (int e = 3; e >= 0; --e) {
           if (found < 0 && run < take && run + (int)c[e] >= take) {
             found = e;
-            abv = run;
-            cb = (int)c[e];
+            ab = run;
+            cc = (int)c[e];
           }
           run += (int)c[e];
         }
         const uint64_t hit = __ballot(found >= 0);  // exactly one lane: bins are monotone
         const int src = __builtin_ctzll(hit);
-        const int b = 4 * src + __shfl(found, src);
-        abv = __shfl(abv, src);
-        cb = __shfl(cb, src);
-        prefix = (d == 3) ? (uint32_t)b : ((prefix << 8) | (uint32_t)b);
-        above = abv;
-        if (abv + cb == take) {
-          cntT = take;
-          shift = sh;
-          break;
+        bin = 4 * src + __shfl(found, src);
+        abv = __shfl(ab, src);
+        cb = __shfl(cc, src);
+      };
+      int bstar, above, cb;
+      pass([&](int) { return true; }, [&](int m) { return bucket(v[m]); }, 0, bstar, above, cb);
+      const bool closed_bucket = above + cb == take;
+      uint32_t prefix = 0;
+      int cntT = take + 1;  // != take until the set closes early
+      int shift = 0;
+      if (!closed_bucket) {
+        for (int d = 3; d >= 0; --d) {
+          const int sh = 8 * d;
+          int b;
+          pass([&](int m) {
+                 return bucket(v[m]) == (uint32_t)bstar &&
+                        (d == 3 || (ordered_key(v[m]) >> (sh + 8)) == prefix);
+               },
+               [&](int m) { return (ordered_key(v[m]) >> sh) & 255u; }, above, b, above, cb);
+          prefix = (d == 3) ? (uint32_t)b : ((prefix << 8) | (uint32_t)b);
+          if (above + cb == take) {
+            cntT = take;
+            shift = sh;
+            break;
+          }
         }
       }
       const uint32_t T = (cntT == take) ? (prefix << shift) : prefix;
-      const int gt = above;  // candidates with key > T (when the set did not close early)
-      // everything >= T when the set closed early; otherwise everything > T
-      // plus the (take - gt) smallest-index candidates tied at T
-      const int need = (cntT == take) ? 0 : take - gt;
-      const uint32_t strict_from = (cntT == take) ? T : T + 1;  // key >= strict_from is taken
+      const int gt = above;  // candidates with value > T (when the set did not close early)
+      // candidates in higher buckets are taken; in the target bucket, everything
+      // when the bucket closed the set, everything >= T when the key digits
+      // closed it, otherwise everything > T plus the (take - gt)
+      // smallest-index candidates tied at T
+      const int need = (closed_bucket || cntT == take) ? 0 : take - gt;
+      const uint32_t strict_from = (cntT == take) ? T : T + 1;  // in-bucket key >= strict_from is taken
       const uint64_t lt = lanemask_lt();
       int before = 0;
 #pragma unroll
       for (int m = 0; m < MAXM; ++m) {
         if (m < M) {
           const bool c = (cand >> m) & 1;
-          const bool above = c && key[m] >= strict_from && (cntT == take || key[m] != T);
-          const bool eq = c && cntT != take && key[m] == T;
+          const uint32_t bk = bucket(v[m]);
+          const uint32_t key = ordered_key(v[m]);
+          const bool in_b = c && bk == (uint32_t)bstar;
+          const bool take_it = (c && bk > (uint32_t)bstar) ||
+                               (in_b && (closed_bucket || (key >= strict_from && (cntT == take || key != T))));
+          const bool eq = in_b && !closed_bucket && cntT != take && key == T;
           const uint64_t bal = __ballot(eq);
           const int rank = before + __popcll(bal & lt);
-          sel |= (uint64_t)(above || (eq && rank < need)) << m;
+          sel |= (uint64_t)(take_it || (eq && rank < need)) << m;
           before += __popcll(bal);
         }
       }

@@ -1,0 +1,73 @@
+"""GPU TopK selection on rows whose gate logits tie exactly.
+
+Q and K are constant over every 64-token block, with small integer entries, and
+the gate weights pick the pooled mean unchanged, so every pooled row, every
+logit dot product and hence every tie is exact in fp32 as in fp64.  Distinct
+logits differ by at least 1/sqrt(Dg), far above fp32 rounding, so the device's
+selection must equal the oracle's bit for bit, including which tied blocks it
+keeps (the smaller block index wins, Eq. 3 with the tie rule of the ABI).  This
+drives the select kernel through its exact paths: rows whose cut falls inside a
+run of equal logits, all-equal rows (zero query weights), and buckets holding a
+single value."""
+import numpy as np
+import pytest
+
+import oracle
+import workload as W
+from helpers import gpu_mask_numpy, stable_seed, to_device
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+seer = pytest.importorskip("paper_2410_13276_amd")
+
+
+def _blockwise_integers(rng, B, H, nb, D, lo, hi):
+    """[B, H, 64 nb, D] bf16 bits, constant over each 64-row block."""
+    a = rng.integers(lo, hi + 1, size=(B, H, nb, D)).astype(np.float32)
+    return W.f32_to_bf16_bits(np.ascontiguousarray(np.repeat(a, 64, axis=2)))
+
+
+def _mean_picking_weights(Hq, Hkv, D, Dg, zero_q=False):
+    wq = np.zeros((Hq, D, Dg), np.float32)
+    wk = np.zeros((Hkv, 3 * D, Dg), np.float32)
+    for d in range(Dg):
+        if not zero_q:
+            wq[:, d, d] = 1.0
+        wk[:, 2 * D + d, d] = 1.0  # the mean third of [max | min | mean]
+    return wq, wk
+
+
+CASES = [
+    # B, Hq, Hkv, nb, D, Dg, integer range
+    (1, 4, 2, 5, 64, 64, (-1, 1)),
+    (2, 2, 1, 65, 64, 32, (-1, 1)),
+    (1, 4, 1, 130, 128, 64, (-2, 2)),
+    (1, 2, 1, 700, 64, 64, (-1, 1)),
+    (1, 2, 2, 1100, 64, 32, (0, 1)),   # few distinct dot products: long runs of ties
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c[:6])))
+@pytest.mark.parametrize("sel", ["ratio", "fixed", "ratio_noforce", "zero_q"])
+def test_topk_with_exact_ties_matches_oracle(case, sel):
+    B, Hq, Hkv, nb, D, Dg, (lo, hi) = case
+    print(f"[ties] {case} {sel}", flush=True)
+    rng = np.random.default_rng(stable_seed("ties", case, sel))
+    q = _blockwise_integers(rng, B, Hq, nb, D, lo, hi)
+    k = _blockwise_integers(rng, B, Hkv, nb, D, lo, hi)
+    wq, wk = _mean_picking_weights(Hq, Hkv, D, Dg, zero_q=sel == "zero_q")
+    keep = 0 if sel == "ratio_noforce" else 1
+    if sel == "fixed":
+        mode, oargs, gargs = oracle.TOPK_FIXED, dict(k=5), dict(mode=seer.TOPK_FIXED, topk_k=5)
+    else:
+        mode, oargs, gargs = oracle.TOPK_RATIO, dict(rho=0.3), dict(mode=seer.TOPK_RATIO, topk_ratio=0.3)
+    _, ell = oracle.gate(q, k, wq, wk, 64, True)
+    orc = oracle.select(ell, mode, **oargs, keep_first=keep, keep_diag=keep)
+    mask = seer.gate(to_device(q), to_device(k), torch.from_numpy(wq).cuda(), torch.from_numpy(wk).cuda(),
+                     **gargs, keep_first=keep, keep_diag=keep, dense_out=True)
+    torch.cuda.synchronize()
+    count, idx, dense = gpu_mask_numpy(mask)
+    np.testing.assert_array_equal(count, orc["count"])
+    bad = np.argwhere(dense != orc["mask"])
+    assert bad.size == 0, f"{len(bad)} entries differ, first at {bad[:3].tolist()}"
