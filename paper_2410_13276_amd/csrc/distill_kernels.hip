@@ -6,14 +6,20 @@
 //                       the gate logits, the ground-truth row renormalised to a
 //                       distribution T, the row's KL(T || P) and the logit
 //                       gradient (P sum(T) - T) / rows written over the logits.
-//   loss_mean_kernel    the mean of the row losses in a fixed order (one
-//                       workgroup, double accumulation: run-to-run identical).
+//   loss_part_kernel,   the mean of the row losses in a fixed order (two
+//   loss_mean_kernel    levels of workgroup sums in double: run-to-run
+//                       identical).
 //   gemm_f32_kernel     fp32 strided batched products for the backward pass
 //                       (dQg = dL Kg, dKg = dL^T Qg, dW = pooled^T dG), 64x64
 //                       LDS tiles on fp32 MFMA, triangular skipping of the
-//                       causal zeros.
+//                       causal zeros, K split over several workgroups when
+//                       the output tiles are few.
+//   gemm_reduce_kernel  sums the split parts in a fixed order.
 //   rope_inverse_kernel rotates gradient rows back through the block-level
 //                       RoPE (the transpose of the forward rotation).
+#include <algorithm>
+#include <cstdlib>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -23,6 +29,10 @@ namespace {
 
 constexpr int kRowsPerBlock = 4;  // wavefronts (rows) per workgroup
 
+// V consecutive entries per lane (V = 4: 16-byte loads; needs nb % 4 == 0 and
+// 16-byte aligned rows).  Two passes over the row: an online max / sum of the
+// exponentials with the target's sum, then the loss and the gradient.
+template <int V>
 __global__ __launch_bounds__(256) void kl_rows_kernel(KlArgs a) {
   const int wave = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
@@ -30,36 +40,66 @@ __global__ __launch_bounds__(256) void kl_rows_kernel(KlArgs a) {
   if (r >= a.rows) return;
   const int nb = a.n_blocks;
   const int i = (int)(r % nb);
-  const int M = i + 1;  // causal entries j <= i
+  const int M = i + 1;                                  // causal entries j <= i
+  const int Mz = min(nb, (i / kKlTile + 1) * kKlTile);  // entries the gradient covers
   float* Lr = a.logits + r * nb;
   const float* gr = a.gt + r * nb;
+  auto load = [&](const float* p, int j0, float (&x)[V]) {
+    if constexpr (V == 4) {
+      const f32x4 u = *reinterpret_cast<const f32x4*>(p + j0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[e] = u[e];
+    } else {
+      x[0] = p[j0];
+    }
+  };
 
-  float mx = -INFINITY, gs = 0.f;
-  for (int j = lane; j < M; j += kWave) {
-    mx = fmaxf(mx, Lr[j]);
-    gs += gr[j];
+  float mx = -INFINITY, es = 0.f, gs = 0.f;
+  for (int j0 = V * lane; j0 < M; j0 += V * kWave) {
+    float l[V], g[V];
+    load(Lr, j0, l);
+    load(gr, j0, g);
+#pragma unroll
+    for (int e = 0; e < V; ++e)
+      if (j0 + e < M) {
+        if (l[e] > mx) {
+          es = es * __expf(mx - l[e]) + 1.f;
+          mx = l[e];
+        } else {
+          es += __expf(l[e] - mx);
+        }
+        gs += g[e];
+      }
   }
-  mx = wave_max(mx);
+  const float mw = wave_max(mx);
+  es = wave_sum(mx == -INFINITY ? 0.f : es * __expf(mx - mw));
   gs = wave_sum(gs);
-  float es = 0.f;
-  for (int j = lane; j < M; j += kWave) es += __expf(Lr[j] - mx);
-  es = wave_sum(es);
-  const float lse = mx + __logf(es);
+  const float lse = mw + __logf(es);
   const float inv_gs = gs > 0.f ? 1.0f / gs : 0.f;
   const float tsum = gs > 0.f ? 1.0f : 0.f;  // sum of T
   const float log_gs = gs > 0.f ? __logf(gs) : 0.f;
   float loss = 0.f;
-  for (int j = lane; j < nb; j += kWave) {
-    float d = 0.f;
-    if (j < M) {
-      const float l = Lr[j];
-      const float g = gr[j];
-      const float logp = l - lse;
-      const float t = g * inv_gs;
-      if (t > 0.f) loss += t * ((__logf(g) - log_gs) - logp);
-      d = (__expf(logp) * tsum - t) * a.inv_rows;
+  for (int j0 = V * lane; j0 < Mz; j0 += V * kWave) {
+    float l[V], g[V], d[V];
+    if (j0 < M) {
+      load(Lr, j0, l);
+      load(gr, j0, g);
     }
-    Lr[j] = d;
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      d[e] = 0.f;
+      if (j0 + e < M) {
+        const float logp = l[e] - lse;
+        const float t = g[e] * inv_gs;
+        if (t > 0.f) loss += t * ((__logf(g[e]) - log_gs) - logp);
+        d[e] = (__expf(logp) * tsum - t) * a.inv_rows;
+      }
+    }
+    if constexpr (V == 4) {
+      *reinterpret_cast<f32x4*>(Lr + j0) = f32x4{d[0], d[1], d[2], d[3]};
+    } else {
+      Lr[j0] = d[0];
+    }
   }
   double dl = (double)loss;
 #pragma unroll
@@ -67,32 +107,54 @@ __global__ __launch_bounds__(256) void kl_rows_kernel(KlArgs a) {
   if (lane == 0) a.row_loss[r] = dl;
 }
 
-__global__ __launch_bounds__(256) void loss_mean_kernel(const double* __restrict__ row_loss,
-                                                         int64_t rows, float* __restrict__ loss) {
-  __shared__ double part[256];
-  double s = 0.0;
-  for (int64_t r = threadIdx.x; r < rows; r += 256) s += row_loss[r];
+// The mean of the row losses in a fixed order (double accumulation: identical
+// run to run): kLossParts workgroups sum contiguous ranges of rows, then one
+// workgroup sums their results.
+__device__ __forceinline__ double block_sum_256(double s, double* part) {
   part[threadIdx.x] = s;
   __syncthreads();
   for (int w = 128; w >= 1; w >>= 1) {
     if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
     __syncthreads();
   }
-  if (threadIdx.x == 0) loss[0] = (float)(part[0] / (double)rows);
+  return part[0];
+}
+
+__global__ __launch_bounds__(256) void loss_part_kernel(const double* __restrict__ row_loss, int64_t rows,
+                                                         double* __restrict__ parts) {
+  __shared__ double part[256];
+  const int64_t lo = rows * blockIdx.x / kLossParts, hi = rows * (blockIdx.x + 1) / kLossParts;
+  double s = 0.0;
+  for (int64_t r = lo + threadIdx.x; r < hi; r += 256) s += row_loss[r];
+  s = block_sum_256(s, part);
+  if (threadIdx.x == 0) parts[blockIdx.x] = s;
+}
+
+__global__ __launch_bounds__(256) void loss_mean_kernel(const double* __restrict__ parts, int64_t rows,
+                                                         float* __restrict__ loss) {
+  __shared__ double part[256];
+  const double s = block_sum_256((int)threadIdx.x < kLossParts ? parts[threadIdx.x] : 0.0, part);
+  if (threadIdx.x == 0) loss[0] = (float)(s / (double)rows);
 }
 
 // 64x64 output tile per 256-thread workgroup (a 32x32 fp32-MFMA block per
-// wavefront, v_mfma_f32_32x32x2_f32), K in chunks of 16 staged through LDS.  Operand tiles are read along whichever
-// index has unit stride, so that loads coalesce for every layout used here.
+// wavefront, v_mfma_f32_32x32x2_f32), K in chunks of 32 staged through two LDS
+// buffers: the next chunk's global loads are in flight in registers while the
+// current chunk's MFMAs run, one barrier per chunk.  Operand tiles are read
+// along whichever index has unit stride, so that loads coalesce for every
+// layout used here.  blockIdx.z = z * splits + s: part s of the tile's (k1, k2)
+// chunks; with splits > 1 the part's product goes to g.part.
 constexpr int kT = 64;
-constexpr int kKc = 16;
+constexpr int kKc = 32;
+constexpr int kLoads = kT * kKc / 256;  // elements of each operand per thread and chunk
+static_assert(kT == kKlTile, "the logit gradient is written up to the end of each row's GEMM tile");
 
-__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
-  __shared__ float sA[kKc][kT + 4];
-  __shared__ float sB[kKc][kT + 4];
+__global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
+  __shared__ float sA[2][kKc][kT + 4];
+  __shared__ float sB[2][kKc][kT + 4];
   const int t = threadIdx.x;
   const int m0 = blockIdx.y * kT, n0 = blockIdx.x * kT;
-  const int z = blockIdx.z;
+  const int z = blockIdx.z / splits, sp = blockIdx.z % splits;
   const float* A = g.A + (int64_t)z * g.saz;
   const float* B = g.B + (int64_t)(z / g.bdiv) * g.sbz;
   const int wave = t / kWave, lane = t % kWave;
@@ -108,43 +170,87 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g) {
   if (g.tri == 2) k2lo = min(g.K2, m0);
   const bool a_mfast = g.sam == 1;
   const bool b_nfast = g.sbn == 1;
+  const int nck = (k2hi - k2lo + kKc - 1) / kKc;  // chunks per k1
+  const int64_t total = (int64_t)g.K1 * nck;
+  const int64_t c0 = total * sp / splits, c1 = total * (sp + 1) / splits;
 
-  for (int k1 = 0; k1 < g.K1; ++k1) {
+  float ra[kLoads], rb[kLoads];
+  auto fetch = [&](int64_t c) {
+    const int k1 = (int)(c / nck);
+    const int kk = k2lo + (int)(c % nck) * kKc;
     const float* Ak = A + (int64_t)k1 * g.sak1;
     const float* Bk = B + (int64_t)k1 * g.sbk1;
-    for (int kk = k2lo; kk < k2hi; kk += kKc) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int e = t + 256 * u;
-        const int m = a_mfast ? e % kT : e / kKc;
-        const int k = a_mfast ? e / kT : e % kKc;
-        const int gm = m0 + m, gk = kk + k;
-        sA[k][m] = (gm < g.M && gk < k2hi) ? Ak[(int64_t)gm * g.sam + (int64_t)gk * g.sak2] : 0.f;
-        const int n = b_nfast ? e % kT : e / kKc;
-        const int kb = b_nfast ? e / kT : e % kKc;
-        const int gn = n0 + n, gkb = kk + kb;
-        sB[kb][n] = (gn < g.N && gkb < k2hi) ? Bk[(int64_t)gkb * g.sbk2 + (int64_t)gn * g.sbn] : 0.f;
-      }
-      __syncthreads();
-      // wavefront (wm, wn) accumulates the 32x32 block at rows 32 wm, columns 32 wn
-      // of the tile; each MFMA contracts the two k of one step, lane half hf
-      // supplying k = 2 s + hf of row (or column) lane % 32
-#pragma unroll
-      for (int st = 0; st < kKc / 2; ++st)
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sA[2 * st + hf][32 * wm + col], sB[2 * st + hf][32 * wn + col],
-                                                   acc, 0, 0, 0);
-      __syncthreads();
+    for (int u = 0; u < kLoads; ++u) {
+      const int e = t + 256 * u;
+      const int m = a_mfast ? e % kT : e / kKc;
+      const int k = a_mfast ? e / kT : e % kKc;
+      const int gm = m0 + m, gk = kk + k;
+      ra[u] = (gm < g.M && gk < k2hi) ? Ak[(int64_t)gm * g.sam + (int64_t)gk * g.sak2] : 0.f;
+      const int n = b_nfast ? e % kT : e / kKc;
+      const int kb = b_nfast ? e / kT : e % kKc;
+      const int gn = n0 + n, gkb = kk + kb;
+      rb[u] = (gn < g.N && gkb < k2hi) ? Bk[(int64_t)gkb * g.sbk2 + (int64_t)gn * g.sbn] : 0.f;
     }
+  };
+  auto stash = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < kLoads; ++u) {
+      const int e = t + 256 * u;
+      sA[buf][a_mfast ? e / kT : e % kKc][a_mfast ? e % kT : e / kKc] = ra[u];
+      sB[buf][b_nfast ? e / kT : e % kKc][b_nfast ? e % kT : e / kKc] = rb[u];
+    }
+  };
+  if (c0 < c1) {
+    fetch(c0);
+    stash(0);
   }
-  float* C = g.C + (int64_t)z * g.scz;
+  __syncthreads();
+  int buf = 0;
+  for (int64_t c = c0; c < c1; ++c) {
+    const bool more = c + 1 < c1;
+    if (more) fetch(c + 1);
+    // wavefront (wm, wn) accumulates the 32x32 block at rows 32 wm, columns 32 wn
+    // of the tile; each MFMA contracts the two k of one step, lane half hf
+    // supplying k = 2 s + hf of row (or column) lane % 32
+#pragma unroll
+    for (int st = 0; st < kKc / 2; ++st)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sA[buf][2 * st + hf][32 * wm + col],
+                                                 sB[buf][2 * st + hf][32 * wn + col], acc, 0, 0, 0);
+    if (more) stash(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
   const int n = n0 + 32 * wn + col;
   if (n < g.N) {
+    if (splits == 1) {
+      float* C = g.C + (int64_t)z * g.scz;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int m = m0 + 32 * wm + 8 * (e / 4) + 4 * hf + (e % 4);
-      if (m < g.M) C[(int64_t)m * g.scm + n] = g.alpha * acc[e];
+      for (int e = 0; e < 16; ++e) {
+        const int m = m0 + 32 * wm + 8 * (e / 4) + 4 * hf + (e % 4);
+        if (m < g.M) C[(int64_t)m * g.scm + n] = g.alpha * acc[e];
+      }
+    } else {
+      float* P = g.part + ((int64_t)z * splits + sp) * g.M * g.N;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int m = m0 + 32 * wm + 8 * (e / 4) + 4 * hf + (e % 4);
+        if (m < g.M) P[(int64_t)m * g.N + n] = acc[e];
+      }
     }
   }
+}
+
+// C = alpha * (sum of the parts in order s = 0, 1, ...): identical run to run.
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(GemmArgs g, int splits) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t mn = (int64_t)g.M * g.N;
+  if (idx >= (int64_t)g.Z * mn) return;
+  const int64_t z = idx / mn, r = idx % mn;
+  const float* P = g.part + z * splits * mn + r;
+  float s = 0.f;
+  for (int p = 0; p < splits; ++p) s += P[p * mn];
+  g.C[z * g.scz + (r / g.N) * g.scm + r % g.N] = g.alpha * s;
 }
 
 // Inverse block-level RoPE: plane (d, d + Dg/2) of row i rotates by
@@ -170,15 +276,51 @@ __global__ __launch_bounds__(256) void rope_inverse_kernel(RopeArgs a) {
 hipError_t launch_kl_rows(const KlArgs& a, hipStream_t s) {
   if (a.rows <= 0) return hipSuccess;
   const int64_t blocks = (a.rows + kRowsPerBlock - 1) / kRowsPerBlock;
-  hipLaunchKernelGGL(kl_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
-  hipLaunchKernelGGL(loss_mean_kernel, dim3(1), dim3(256), 0, s, a.row_loss, a.rows, a.loss);
+  const bool vec = a.n_blocks % 4 == 0 && reinterpret_cast<uintptr_t>(a.logits) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(a.gt) % 16 == 0;
+  if (vec) hipLaunchKernelGGL(kl_rows_kernel<4>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(kl_rows_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  double* parts = a.row_loss + a.rows;
+  hipLaunchKernelGGL(loss_part_kernel, dim3(kLossParts), dim3(256), 0, s, a.row_loss, a.rows, parts);
+  hipLaunchKernelGGL(loss_mean_kernel, dim3(1), dim3(256), 0, s, parts, a.rows, a.loss);
   return hipGetLastError();
+}
+
+// Parts per output tile: enough workgroups to fill the chip (about 2048) when
+// the tiles alone are fewer, but at least 8 chunks of K per part on the
+// longest tile.  The environment variable SEER_GEMM_MIN_CHUNKS (read on the
+// host at each call and at each workspace query) overrides the 8, so that
+// tests can split small products.
+int gemm_splits(const GemmArgs& a) {
+  if (a.M <= 0 || a.N <= 0 || a.Z <= 0) return 1;
+  int min_chunks = 8;
+  if (const char* e = getenv("SEER_GEMM_MIN_CHUNKS")) {
+    const int v = atoi(e);
+    if (v >= 1) min_chunks = v;
+  }
+  const int64_t tiles = (int64_t)((a.N + kT - 1) / kT) * ((a.M + kT - 1) / kT) * a.Z;
+  const int64_t chunks = (int64_t)a.K1 * ((a.K2 + kKc - 1) / kKc);
+  int64_t sp = (2048 + tiles - 1) / tiles;
+  sp = std::min<int64_t>(sp, chunks / min_chunks);
+  sp = std::min<int64_t>(sp, 64);
+  return (int)std::max<int64_t>(sp, 1);
+}
+
+int64_t gemm_partial_elems(const GemmArgs& a) {
+  const int sp = gemm_splits(a);
+  return sp > 1 ? (int64_t)a.Z * sp * a.M * a.N : 0;
 }
 
 hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.Z <= 0) return hipSuccess;
-  dim3 grid((a.N + kT - 1) / kT, (a.M + kT - 1) / kT, a.Z);
-  hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, a);
+  const int sp = gemm_splits(a);
+  if (sp > 1 && a.part == nullptr) return hipErrorInvalidValue;
+  dim3 grid((a.N + kT - 1) / kT, (a.M + kT - 1) / kT, a.Z * sp);
+  hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, a, sp);
+  if (sp > 1) {
+    const int64_t n = (int64_t)a.Z * a.M * a.N;
+    hipLaunchKernelGGL(gemm_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a, sp);
+  }
   return hipGetLastError();
 }
 

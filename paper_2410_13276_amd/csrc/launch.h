@@ -96,18 +96,26 @@ constexpr int kMaxSplitParts = 16;
 
 // Gate distillation (Eq. 2): row-wise KL between the renormalised ground truth
 // and the gate softmax, and the logit gradient written over the logits.
+// The gradient is written for j < min(nb, 64 (i / 64 + 1)): entries j > i up to
+// the end of the row's 64-row tile are 0, and entries beyond are never read
+// (the backward products skip them by causality at 64-row tile granularity).
+constexpr int kKlTile = 64;
+constexpr int kLossParts = 64;  // first-level partial sums of the row losses
 struct KlArgs {
-  float* logits;       // [rows][nb] in: logits (j <= i), out: dloss/dlogit (0 for j > i)
+  float* logits;       // [rows][nb] in: logits (j <= i), out: dloss/dlogit (see above)
   const float* gt;     // [rows][nb] ground truth (j <= i read)
   int64_t rows;
   int n_blocks;
   float inv_rows;      // 1 / rows: the loss is the mean over rows
-  double* row_loss;    // [rows]
-  float* loss;         // device scalar: mean of row_loss
+  double* row_loss;    // [rows + kLossParts]: per-row losses, then the partial sums
+  float* loss;         // device scalar: mean of the row losses
 };
 
 // C[z][m][n] = alpha * sum_{k1 < K1, k2 < K2} A(z, m, k1, k2) * B(z / bdiv, k1, k2, n), fp32,
 // with element strides; tri = 1: A vanishes for k2 > m, tri = 2: for k2 < m.
+// When gemm_splits() > 1 the (k1, k2) range is cut into that many parts whose
+// products go to `part` ([Z][splits][M][N], gemm_partial_elems() floats) and
+// are summed in a fixed order by a second kernel.
 struct GemmArgs {
   const float* A;
   const float* B;
@@ -117,7 +125,10 @@ struct GemmArgs {
   int64_t sbk1, sbk2, sbn, sbz;
   int64_t scm, scz;
   float alpha;
+  float* part;
 };
+int gemm_splits(const GemmArgs& a);
+int64_t gemm_partial_elems(const GemmArgs& a);
 
 struct RopeArgs {  // inverse block-level RoPE of rows [rows][nb][Dg], in place
   float* x;

@@ -98,10 +98,88 @@ GateLayout gate_layout(const seer_attn_desc* d, const seer_gate_desc* g, bool lo
   return L;
 }
 
+// The four backward products of seer_gate_distill (pointers may be null when
+// only the shapes are wanted):
+//   dQg[b,h] = dL[b,h] Kg[b,g] / sqrt(Dg)                       (dL lower triangular)
+//   dKg[b,g][j] = sum over the group's heads h and rows i of dL[b,h][i][j] Qg[b,h][i] / sqrt(Dg)
+//   dWq[h] = sum over b, i of Qp[b,h,i]^T dQg[b,h,i]           (shared weights: also over h)
+//   dWk[g] = sum over b, j of Kp[b,g,j]^T dKg[b,g,j]
+struct DistillGemms {
+  seer::GemmArgs dqg, dkg, dwq, dwk;
+};
+
+DistillGemms distill_gemms(int B, int Hq, int Hkv, int D, int Dg, int nb, bool ph, const float* dl,
+                           const float* qg, const float* kg, const float* qp, const float* kp, float* dqg,
+                           float* dkg, float* dwq, float* dwk, float* part) {
+  const int G = Hq / Hkv;
+  const int64_t nn = (int64_t)nb * nb;
+  const float rsqrt_dg = (float)(1.0 / std::sqrt((double)Dg));
+  DistillGemms r;
+  seer::GemmArgs g{};
+  g.A = dl; g.B = kg; g.C = dqg;
+  g.M = nb; g.N = Dg; g.K1 = 1; g.K2 = nb; g.Z = B * Hq; g.bdiv = G; g.tri = 1;
+  g.sam = nb; g.sak1 = 0; g.sak2 = 1; g.saz = nn;
+  g.sbk1 = 0; g.sbk2 = Dg; g.sbn = 1; g.sbz = (int64_t)nb * Dg;
+  g.scm = Dg; g.scz = (int64_t)nb * Dg;
+  g.alpha = rsqrt_dg;
+  g.part = part;
+  r.dqg = g;
+
+  g = seer::GemmArgs{};
+  g.A = dl; g.B = qg; g.C = dkg;
+  g.M = nb; g.N = Dg; g.K1 = G; g.K2 = nb; g.Z = B * Hkv; g.bdiv = 1; g.tri = 2;
+  g.sam = 1; g.sak1 = nn; g.sak2 = nb; g.saz = G * nn;
+  g.sbk1 = (int64_t)nb * Dg; g.sbk2 = Dg; g.sbn = 1; g.sbz = (int64_t)G * nb * Dg;
+  g.scm = Dg; g.scz = (int64_t)nb * Dg;
+  g.alpha = rsqrt_dg;
+  g.part = part;
+  r.dkg = g;
+
+  g = seer::GemmArgs{};
+  g.A = qp; g.B = dqg; g.C = dwq;
+  g.M = D; g.N = Dg; g.K2 = nb; g.bdiv = 1; g.tri = 0;
+  g.sam = 1; g.sak2 = D;
+  g.sbk2 = Dg; g.sbn = 1;
+  g.scm = Dg; g.scz = (int64_t)D * Dg;
+  g.alpha = 1.0f;
+  g.part = part;
+  if (ph) {
+    g.Z = Hq; g.K1 = B;
+    g.saz = (int64_t)nb * D; g.sak1 = (int64_t)Hq * nb * D;
+    g.sbz = (int64_t)nb * Dg; g.sbk1 = (int64_t)Hq * nb * Dg;
+  } else {
+    g.Z = 1; g.K1 = B * Hq;
+    g.saz = 0; g.sak1 = (int64_t)nb * D;
+    g.sbz = 0; g.sbk1 = (int64_t)nb * Dg;
+  }
+  r.dwq = g;
+
+  g = seer::GemmArgs{};
+  g.A = kp; g.B = dkg; g.C = dwk;
+  g.M = 3 * D; g.N = Dg; g.K2 = nb; g.bdiv = 1; g.tri = 0;
+  g.sam = 1; g.sak2 = 3 * D;
+  g.sbk2 = Dg; g.sbn = 1;
+  g.scm = Dg; g.scz = (int64_t)3 * D * Dg;
+  g.alpha = 1.0f;
+  g.part = part;
+  if (ph) {
+    g.Z = Hkv; g.K1 = B;
+    g.saz = (int64_t)nb * 3 * D; g.sak1 = (int64_t)Hkv * nb * 3 * D;
+    g.sbz = (int64_t)nb * Dg; g.sbk1 = (int64_t)Hkv * nb * Dg;
+  } else {
+    g.Z = 1; g.K1 = B * Hkv;
+    g.saz = 0; g.sak1 = (int64_t)nb * 3 * D;
+    g.sbz = 0; g.sbk1 = (int64_t)nb * Dg;
+  }
+  r.dwk = g;
+  return r;
+}
+
 // Workspace of seer_gate_distill: projected rows, pooled rows, logits (then
-// their gradient), projected-row gradients, per-row losses.
+// their gradient), projected-row gradients, per-row losses, and the split
+// products of the backward GEMMs (run one after another, so one buffer).
 struct DistillLayout {
-  size_t qg, kg, qp, kp, logits, dqg, dkg, row_loss, total;
+  size_t qg, kg, qp, kp, logits, dqg, dkg, row_loss, part, total;
 };
 
 DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g) {
@@ -121,7 +199,14 @@ DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g) {
   L.logits = take(B * Hq * nb * nb * 4);
   L.dqg = take(B * Hq * nb * Dg * 4);
   L.dkg = take(B * Hkv * nb * Dg * 4);
-  L.row_loss = take(B * Hq * nb * 8);
+  L.row_loss = take((B * Hq * nb + seer::kLossParts) * 8);
+  const DistillGemms gm = distill_gemms((int)B, (int)Hq, (int)Hkv, (int)D, (int)Dg, (int)nb, g->w_per_head != 0,
+                                        nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                        nullptr, nullptr);
+  int64_t part = 0;
+  for (const seer::GemmArgs* a : {&gm.dqg, &gm.dkg, &gm.dwq, &gm.dwk})
+    part = std::max(part, seer::gemm_partial_elems(*a));
+  L.part = take((size_t)part * 4);
   L.total = off;
   return L;
 }
@@ -484,7 +569,7 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   double* row_loss = reinterpret_cast<double*>(ws + W.row_loss);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int B = desc->batch, Hq = desc->heads_q, Hkv = desc->heads_kv, D = desc->head_dim;
-  const int Dg = gate->gate_dim, G = Hq / Hkv;
+  const int Dg = gate->gate_dim;
   const int nb = blocks_of(desc->seq_len, gate->block);
   const double rope_base = gate->rope_theta > 0.0 ? gate->rope_theta / gate->block : 0.0;
   const float rsqrt_dg = (float)(1.0 / std::sqrt((double)Dg));
@@ -536,72 +621,18 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   ka.loss = loss;
   if ((s = from_hip(seer::launch_kl_rows(ka, st))) != SEER_OK) return s;
 
-  const int64_t nn = (int64_t)nb * nb;
-  // dQg[b,h] = dL[b,h] Kg[b,g] / sqrt(Dg)   (dL lower triangular)
-  seer::GemmArgs g{};
-  g.A = dl; g.B = kg; g.C = dqg;
-  g.M = nb; g.N = Dg; g.K1 = 1; g.K2 = nb; g.Z = B * Hq; g.bdiv = G; g.tri = 1;
-  g.sam = nb; g.sak1 = 0; g.sak2 = 1; g.saz = nn;
-  g.sbk1 = 0; g.sbk2 = Dg; g.sbn = 1; g.sbz = (int64_t)nb * Dg;
-  g.scm = Dg; g.scz = (int64_t)nb * Dg;
-  g.alpha = rsqrt_dg;
-  if ((s = from_hip(seer::launch_gemm_f32(g, st))) != SEER_OK) return s;
-
-  // dKg[b,g][j] = sum over the group's heads h and rows i of dL[b,h][i][j] Qg[b,h][i] / sqrt(Dg)
-  g = seer::GemmArgs{};
-  g.A = dl; g.B = qg; g.C = dkg;
-  g.M = nb; g.N = Dg; g.K1 = G; g.K2 = nb; g.Z = B * Hkv; g.bdiv = 1; g.tri = 2;
-  g.sam = 1; g.sak1 = nn; g.sak2 = nb; g.saz = G * nn;
-  g.sbk1 = (int64_t)nb * Dg; g.sbk2 = Dg; g.sbn = 1; g.sbz = (int64_t)G * nb * Dg;
-  g.scm = Dg; g.scz = (int64_t)nb * Dg;
-  g.alpha = rsqrt_dg;
-  if ((s = from_hip(seer::launch_gemm_f32(g, st))) != SEER_OK) return s;
-
+  const DistillGemms gm = distill_gemms(B, Hq, Hkv, D, Dg, nb, gate->w_per_head != 0, dl, qg, kg, qp, kp, dqg,
+                                        dkg, dwq, dwk, reinterpret_cast<float*>(ws + W.part));
+  if ((s = from_hip(seer::launch_gemm_f32(gm.dqg, st))) != SEER_OK) return s;
+  if ((s = from_hip(seer::launch_gemm_f32(gm.dkg, st))) != SEER_OK) return s;
   if (rope_base > 0.0) {  // back through the block-level RoPE
     seer::RopeArgs ra{dqg, (int64_t)B * Hq, nb, Dg, rope_base};
     if ((s = from_hip(seer::launch_rope_inverse(ra, st))) != SEER_OK) return s;
     ra = seer::RopeArgs{dkg, (int64_t)B * Hkv, nb, Dg, rope_base};
     if ((s = from_hip(seer::launch_rope_inverse(ra, st))) != SEER_OK) return s;
   }
-
-  // dWq[h] = sum over b, i of Qp[b,h,i]^T dQg[b,h,i] (shared weights: also over h)
-  const bool ph = gate->w_per_head != 0;
-  g = seer::GemmArgs{};
-  g.A = qp; g.B = dqg; g.C = dwq;
-  g.M = D; g.N = Dg; g.K2 = nb; g.bdiv = 1; g.tri = 0;
-  g.sam = 1; g.sak2 = D;
-  g.sbk2 = Dg; g.sbn = 1;
-  g.scm = Dg; g.scz = (int64_t)D * Dg;
-  g.alpha = 1.0f;
-  if (ph) {
-    g.Z = Hq; g.K1 = B;
-    g.saz = (int64_t)nb * D; g.sak1 = (int64_t)Hq * nb * D;
-    g.sbz = (int64_t)nb * Dg; g.sbk1 = (int64_t)Hq * nb * Dg;
-  } else {
-    g.Z = 1; g.K1 = B * Hq;
-    g.saz = 0; g.sak1 = (int64_t)nb * D;
-    g.sbz = 0; g.sbk1 = (int64_t)nb * Dg;
-  }
-  if ((s = from_hip(seer::launch_gemm_f32(g, st))) != SEER_OK) return s;
-
-  // dWk[g] = sum over b, j of Kp[b,g,j]^T dKg[b,g,j]
-  g = seer::GemmArgs{};
-  g.A = kp; g.B = dkg; g.C = dwk;
-  g.M = 3 * D; g.N = Dg; g.K2 = nb; g.bdiv = 1; g.tri = 0;
-  g.sam = 1; g.sak2 = 3 * D;
-  g.sbk2 = Dg; g.sbn = 1;
-  g.scm = Dg; g.scz = (int64_t)3 * D * Dg;
-  g.alpha = 1.0f;
-  if (ph) {
-    g.Z = Hkv; g.K1 = B;
-    g.saz = (int64_t)nb * 3 * D; g.sak1 = (int64_t)Hkv * nb * 3 * D;
-    g.sbz = (int64_t)nb * Dg; g.sbk1 = (int64_t)Hkv * nb * Dg;
-  } else {
-    g.Z = 1; g.K1 = B * Hkv;
-    g.saz = 0; g.sak1 = (int64_t)nb * 3 * D;
-    g.sbz = 0; g.sbk1 = (int64_t)nb * Dg;
-  }
-  return from_hip(seer::launch_gemm_f32(g, st));
+  if ((s = from_hip(seer::launch_gemm_f32(gm.dwq, st))) != SEER_OK) return s;
+  return from_hip(seer::launch_gemm_f32(gm.dwk, st));
 }
 
 }  // extern "C"

@@ -54,7 +54,12 @@ def _weights(B, Hq, Hkv, D, Dg, per_head, seed):
 
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
-def test_gate_distill_parity(case):
+@pytest.mark.parametrize("min_chunks", [None, 1], ids=["default", "split"])
+def test_gate_distill_parity(case, min_chunks, monkeypatch):
+    """`split`: every backward product cut into as many K parts as it has
+    K chunks (empty parts included), summed by the reduction kernel."""
+    if min_chunks is not None:
+        monkeypatch.setenv("SEER_GEMM_MIN_CHUNKS", str(min_chunks))
     B, Hq, Hkv, S, D, dt, Dg, per_head, theta = case
     seed = stable_seed(case, "distill")
     _, q, k, _, _, _ = small_inputs(B, Hq, Hkv, S, D, dt, seed=seed, spikes=True)
