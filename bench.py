@@ -303,6 +303,9 @@ def main() -> int:
     multi = any(groups % g == 0 and nb % (8 // g) == 0 and g * kv_group_bytes <= 32 * 2 ** 20 for g in (8, 4, 2))
     launches = groups if (groups > 1 and not multi and nb % 8 == 0 and not sparse_split) else 1
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
+    traffic = _traffic(w.name)
+    es = 2 if w.dtype == "bf16" else 4
+    alg_bytes = es * w.batch * w.seq_len * w.head_dim * (2 * w.heads_q + 2 * w.heads_kv)  # Q, O, K, V
     speedup = dense_ms / attn_ms
     result = {
         "metric": "block-sparse prefill attn TFLOPS (active tiles) + speedup vs dense @128k",
@@ -350,13 +353,20 @@ def main() -> int:
             "ms": round(distill_ms, 3)},
         "roofline": {"bound": "mfma", "kernel": attn_kernels,
                      "achieved": round(attn_tflops, 2), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(attn_tflops / peak, 4), "traffic": _traffic(w.name),
+                     "frac": round(attn_tflops / peak, 4), "traffic": traffic,
                      "launches_per_call": launches,
                      "flops_per_launch": active_flops / launches,
                      "launch_avg_ms": round(attn_ms / launches, 4),
+                     "algorithmic_bytes_per_launch": alg_bytes / launches,
+                     "traffic_tb_per_s": None if traffic is None else
+                     round(traffic / (attn_ms / launches * 1e-3) / 1e12, 3),
                      "note": "achieved = active-tile flops of one call / the call's mean HIP-event "
                              "duration = flops_per_launch / launch_avg_ms (the call's launches run "
-                             "back to back on the stream)"},
+                             "back to back on the stream). traffic = bytes past L2 per launch "
+                             "(scaled rocprofv3 FETCH_SIZE + WRITE_SIZE); traffic_tb_per_s = traffic "
+                             "/ launch_avg_ms, against algorithmic_bytes_per_launch (Q, K, V read "
+                             "once, O written once): tiles of near-random masks are reused little "
+                             "in a 4 MB L2, so the launch streams K/V from the Infinity Cache"},
     }
     log(f"[bench] step {ms_step:.3f} ms (gate {gate_ms:.3f} + attn {attn_ms:.3f}); "
         f"attn {attn_tflops:.1f} TF/s; dense {dense_ms:.2f} ms; speedup {speedup:.2f}x "

@@ -175,8 +175,9 @@ def test_gate_distill_workspace_and_rejects_bad_args():
     L = seer.lib()
     d, g = _desc(B=1, Hq=4, Hkv=2, S=1024, D=128), _gate()
     nb, up = 16, (lambda x: (x + 255) // 256 * 256)
+    # Qg, Kg, Qp, Kp, logits, dQg, dKg, row losses + 64 partial sums; no product splits at this size
     want = (up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up(4 * nb * 128 * 4) + up(2 * nb * 384 * 4)
-            + up(4 * nb * nb * 4) + up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up(4 * nb * 8))
+            + up(4 * nb * nb * 4) + up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up((4 * nb + 64) * 8))
     need = L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g))
     assert need == want
     g.mode = 9  # the selection mode is not used by the distillation step
@@ -189,6 +190,40 @@ def test_gate_distill_workspace_and_rejects_bad_args():
     assert call(ws=FAKE * 16 + 16) == seer.ERR_INVALID_ARG
     assert call(gd=_gate(gate_dim=48)) == seer.ERR_UNSUPPORTED
     assert call(gd=_gate(rope_theta=-2.0)) == seer.ERR_INVALID_ARG
+
+
+def _gemm_splits(M, N, K1, K2, Z, min_chunks=8):
+    """The split rule of the distillation products: about 2048 workgroups when
+    the 64x64 output tiles are fewer, at least `min_chunks` 32-wide K chunks per
+    part, at most 64 parts."""
+    tiles = -(-N // 64) * -(-M // 64) * Z
+    chunks = K1 * -(-K2 // 32)
+    return max(1, min(-(-2048 // tiles), chunks // min_chunks, 64))
+
+
+@pytest.mark.parametrize("min_chunks", [None, 1])
+def test_gate_distill_workspace_split_products(min_chunks, monkeypatch):
+    """At 32k tokens (32 q / 8 kv heads) the backward products split their K
+    range; the workspace holds the largest product's parts."""
+    if min_chunks is None:
+        monkeypatch.delenv("SEER_GEMM_MIN_CHUNKS", raising=False)
+    else:
+        monkeypatch.setenv("SEER_GEMM_MIN_CHUNKS", str(min_chunks))
+    mc = min_chunks or 8
+    L = seer.lib()
+    B, Hq, Hkv, D, Dg, nb = 1, 32, 8, 128, 128, 512
+    d, g = _desc(B=B, Hq=Hq, Hkv=Hkv, S=64 * nb, D=D), _gate()
+    up = lambda x: (x + 255) // 256 * 256
+    base = (up(Hq * nb * Dg * 4) + up(Hkv * nb * Dg * 4) + up(Hq * nb * D * 4) + up(Hkv * nb * 3 * D * 4)
+            + up(Hq * nb * nb * 4) + up(Hq * nb * Dg * 4) + up(Hkv * nb * Dg * 4) + up((Hq * nb + 64) * 8))
+    products = [(nb, Dg, 1, nb, Hq), (nb, Dg, Hq // Hkv, nb, Hkv), (D, Dg, 1, nb, Hq), (3 * D, Dg, 1, nb, Hkv)]
+    part = 0
+    for M, N, K1, K2, Z in products:
+        sp = _gemm_splits(M, N, K1, K2, Z, mc)
+        if sp > 1:
+            part = max(part, Z * sp * M * N)
+    assert part > 0
+    assert L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g)) == base + up(4 * part)
 
 
 def test_attn_workspace_bytes_formula(monkeypatch):
