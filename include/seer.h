@@ -203,15 +203,16 @@ seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm
 /*
  * Workspace bytes that let seer_bsattn_ws / seer_dense_attn_ws run the
  * key-range split for this shape, or 0 when the shape does not split (then
- * those calls need no workspace).  The split applies to causal bf16 attention
+ * those calls need no workspace).  The split is opt-in: dense calls split only
+ * when the environment variable SEER_SPLIT_DENSE is 1, sparse calls only when
+ * SEER_SPLIT_SPARSE is 1 (both read at each call; the unsplit kernels measured
+ * as fast or faster on this hardware).  It applies to causal bf16 attention
  * with nb a multiple of 16 and nb / 16 >= the minimum range width (32 blocks;
- * the environment variable SEER_SPLIT_MIN_WIDTH, read at each call, overrides
- * it).  Dense calls split whenever the shape allows; sparse calls only when
- * the environment variable SEER_SPLIT_SPARSE is 1 (at 10% density the
- * unsplit sparse kernel measured as fast), then with 8 ranges when
- * batch * heads_kv is even, else 16.  Size: 68 bytes per query block plus (256 + 128 head_dim) bytes per
- * partial slot; a query head has sum over i of (floor(i / (nb / 16)) + 1),
- * about 8.5 nb, slots (9.3 GB for 32 heads of 131072 tokens, head_dim 128).
+ * the environment variable SEER_SPLIT_MIN_WIDTH overrides it); dense rows take
+ * 16 ranges, sparse rows 8 when batch * heads_kv is even, else 16.  Size: 68
+ * bytes per query block plus (256 + 128 head_dim) bytes per partial slot; a
+ * query head has sum over i of (floor(i / (nb / 16)) + 1), about 8.5 nb, slots
+ * (9.3 GB for 32 heads of 131072 tokens, head_dim 128).
  */
 size_t seer_attn_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t causal);
 

@@ -405,20 +405,21 @@ constexpr int kListChunk = 256;
 // RAGGED: the sequence ends inside its last tile (the clamped loads and the
 // key mask past the end exist only in that instantiation).
 //
-// NH > 1 (sparse rows of a mask shared by a KV group): the workgroup holds NH
-// query heads of one group, two wavefronts each, for the same query block;
-// each K/V tile is loaded once into LDS for all of them, which divides the
-// K/V traffic by NH.  The task map then counts head slots of NH heads.
+// NH > 1 (rows shared by the query heads of a KV group: a mask shared by the
+// group, or dense rows): the workgroup holds NH query heads of one group, two
+// wavefronts each, for the same query block; each K/V tile is loaded once into
+// LDS for all of them, which divides the K/V loads by NH.  The task map then
+// counts head slots of NH heads.
 template <int D, bool SPARSE, bool SPLIT, bool RAGGED, int NH = 1>
 __global__ __launch_bounds__(128 * NH) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void attn_fwd_bf16_kernel(KernelArgs ka) {
   using Lay = Bf16Layout<D>;
   constexpr int NW = 2 * NH;  // wavefronts
-  static_assert(NH == 1 || (SPARSE && !SPLIT), "shared-row workgroups serve sparse unsplit rows");
+  static_assert(NH == 1 || !SPLIT, "shared-row workgroups serve unsplit rows");
   __shared__ __attribute__((aligned(16))) uint16_t sK[Lay::TILE];
   __shared__ __attribute__((aligned(16))) uint16_t sV[Lay::TILE];
   __shared__ uint16_t sList[SPARSE ? kListChunk : 1];
-  __shared__ __attribute__((aligned(16))) float sL2[SPARSE ? 1 : 64];
+  __shared__ __attribute__((aligned(16))) float sL2[SPARSE ? 1 : 64 * NH];
 
   const AttnArgs& a = ka.a;
   Task t = SPLIT ? decode_split(ka.split, blockIdx.x) : decode_task(ka.map, blockIdx.x);
@@ -491,7 +492,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   // row list
   const RowList<SPARSE> list = make_list<SPARSE, SPLIT>(a, t);
   const bool pool = !SPARSE && !SPLIT && a.gt != nullptr;  // ground-truth mode
-  const int64_t trow = ((int64_t)t.b * a.heads_q + t.h) * a.n_blocks + t.i;
+  const int64_t trow = ((int64_t)t.b * a.heads_q + hq) * a.n_blocks + t.i;  // this wavefront's head
   float* const rrow = pool ? a.pool_r + trow * a.n_blocks * 64 : nullptr;
   auto fetch_chunk = [&](int base) {  // mask entries [base, base + kListChunk) of the row
     if (SPARSE) {
@@ -777,10 +778,15 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   }
   if (pool) {
     // padding rows take no part in the column max
-    if (hf == 0) sL2[ql] = (l_tot > 0.f && qrow < S) ? m_run * c + __log2f(l_tot) : INFINITY;
+    if (hf == 0) sL2[64 * (wave_all / 2) + ql] = (l_tot > 0.f && qrow < S) ? m_run * c + __log2f(l_tot) : INFINITY;
     wait_loads();  // the row-max stores of this workgroup have completed
     __syncthreads();
-    pool_epilogue(rrow, sL2, c, list.n, a.n_blocks, a.gt + trow * a.n_blocks, tid, 128);
+#pragma unroll
+    for (int hs = 0; hs < NH; ++hs) {
+      const int64_t hrow = ((int64_t)t.b * a.heads_q + h0 + hs) * a.n_blocks + t.i;
+      pool_epilogue(a.pool_r + hrow * a.n_blocks * 64, sL2 + 64 * hs, c, list.n, a.n_blocks,
+                    a.gt + hrow * a.n_blocks, tid, 128 * NH);
+    }
   }
 }
 
@@ -1071,18 +1077,20 @@ static TaskMap make_map(const AttnArgs& a) {
 // variable SEER_SPLIT_MIN_WIDTH (read on the host at each call) overrides it.
 constexpr int kSplitMinWidth = 32;
 
-// Dense rows use 16 ranges.  Sparse rows are not split unless the environment
-// variable SEER_SPLIT_SPARSE=1 asks for it: at 131072 tokens and 10% density
-// the unsplit sparse kernel (18.3 ms) matched 8 ranges (18.7 ms incl. the
-// merge) and beat 16 (20.0 ms), the short tasks' set-up and the partial traffic
-// eating the L2 gain.  When enabled, sparse rows take 8 ranges if the number
-// of KV groups is even (fewer tasks and partials), else 16.
+// Rows are split only on request: the environment variable SEER_SPLIT_DENSE=1
+// (dense rows) or SEER_SPLIT_SPARSE=1 (sparse rows), read at each call.  Dense
+// rows then take 16 ranges.  Measured at 131072 tokens: the unsplit dense
+// kernel with two query heads per workgroup (117 ms) beat 16 ranges (133 ms,
+// one head per workgroup, as the split runs); at 32768 tokens 7.4 against
+// 9.0 ms, at 8192 equal.  Sparse rows at 10% density: the unsplit kernel
+// (18.3 ms) matched 8 ranges (18.7 ms incl. the merge) and beat 16 (20.0 ms),
+// the short tasks' set-up and the partial traffic eating the L2 gain; when
+// enabled they take 8 ranges if the number of KV groups is even (fewer tasks
+// and partials), else 16.
 int split_parts(int n_blocks, int kv_groups, bool causal, bool bf16, bool sparse) {
   if (!causal || !bf16) return 0;
-  if (sparse) {
-    const char* e = getenv("SEER_SPLIT_SPARSE");
-    if (!e || atoi(e) != 1) return 0;
-  }
+  const char* e = getenv(sparse ? "SEER_SPLIT_SPARSE" : "SEER_SPLIT_DENSE");
+  if (!e || atoi(e) != 1) return 0;
   int min_w = kSplitMinWidth;
   if (const char* e = getenv("SEER_SPLIT_MIN_WIDTH")) {
     const int v = atoi(e);
@@ -1151,15 +1159,16 @@ hipError_t launch_attn(const AttnArgs& a, hipStream_t s) {
   return hipSuccess;
 }
 
-// Query heads per workgroup for rows of a mask shared by a KV group: 2 when the
-// group size allows, else 1 (the environment variable SEER_KV_HEADS_PER_WG,
-// read at each call, sets the cap: 1, 2 or 4).  Measured at 131072 tokens,
-// 32 query / 8 KV heads, TopK 0.1: per-head rows 17.3 ms; shared rows with 1,
-// 2 and 4 heads per workgroup 14.3, 13.0 and 13.1 ms (two 4-wavefront
-// workgroups per CU keep their phases independent; one 8-wavefront workgroup
-// moves in lockstep).
+// Query heads per workgroup for rows shared by the query heads of a KV group
+// (a mask shared by the group, or dense rows): 2 when the group size allows,
+// else 1 (the environment variable SEER_KV_HEADS_PER_WG, read at each call,
+// sets the cap: 1, 2 or 4).  Measured at 131072 tokens, 32 query / 8 KV heads,
+// TopK 0.1: per-head rows 17.3 ms; shared rows with 1, 2 and 4 heads per
+// workgroup 14.3, 13.0 and 13.1 ms (two 4-wavefront workgroups per CU keep
+// their phases independent; one 8-wavefront workgroup moves in lockstep).
 static int kv_heads_per_wg(const AttnArgs& a) {
-  if (!a.mask_kv || !a.bf16 || a.split_w > 0) return 1;
+  const bool shared_rows = a.count ? a.mask_kv : true;
+  if (!shared_rows || !a.bf16 || a.split_w > 0) return 1;
   int cap = 2;
   if (const char* e = getenv("SEER_KV_HEADS_PER_WG")) cap = atoi(e);
   const int G = a.heads_q / a.heads_kv;
@@ -1168,10 +1177,21 @@ static int kv_heads_per_wg(const AttnArgs& a) {
   return 1;
 }
 
-template <int D, bool RAGGED>
-static void launch_sparse_nh(const KernelArgs& ka, int nh, dim3 grid, hipStream_t s) {
-  if (nh == 4) hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, true, false, RAGGED, 4>), grid, dim3(512), 0, s, ka);
-  else hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, true, false, RAGGED, 2>), grid, dim3(256), 0, s, ka);
+template <int D, bool SPARSE, bool RAGGED>
+static void launch_nh(const KernelArgs& ka, int nh, dim3 grid, hipStream_t s) {
+  if (nh == 4) hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, SPARSE, false, RAGGED, 4>), grid, dim3(512), 0, s, ka);
+  else hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, SPARSE, false, RAGGED, 2>), grid, dim3(256), 0, s, ka);
+}
+
+template <int D>
+static void launch_nh_d(const KernelArgs& ka, int nh, bool sparse, bool ragged, dim3 grid, hipStream_t s) {
+  if (sparse) {
+    if (ragged) launch_nh<D, true, true>(ka, nh, grid, s);
+    else launch_nh<D, true, false>(ka, nh, grid, s);
+  } else {
+    if (ragged) launch_nh<D, false, true>(ka, nh, grid, s);
+    else launch_nh<D, false, false>(ka, nh, grid, s);
+  }
 }
 
 static hipError_t launch_attn_one(const AttnArgs& a, hipStream_t s) {
@@ -1186,20 +1206,15 @@ static hipError_t launch_attn_one(const AttnArgs& a, hipStream_t s) {
     if (total == 0) return hipSuccess;
     ka.split = SplitMap{a.heads_q, a.heads_kv, a.n_blocks, 0, 0};
     ka.scale_log2 = a.scale * kLog2e;
-    if (a.seq_len <= 0 || (a.n_blocks - 1) * 64 >= a.seq_len || a.n_blocks * 64 < a.seq_len || !a.count ||
-        a.gt != nullptr)
+    const bool sparse = a.count != nullptr;
+    if (a.seq_len <= 0 || (a.n_blocks - 1) * 64 >= a.seq_len || a.n_blocks * 64 < a.seq_len ||
+        (a.gt != nullptr && (sparse || !a.pool_r)))
       return hipErrorInvalidValue;
     const bool ragged = a.seq_len % 64 != 0;
     const dim3 grid((unsigned)total);
-    if (a.head_dim == 128) {
-      if (ragged) launch_sparse_nh<128, true>(ka, nh, grid, s);
-      else launch_sparse_nh<128, false>(ka, nh, grid, s);
-    } else if (a.head_dim == 64) {
-      if (ragged) launch_sparse_nh<64, true>(ka, nh, grid, s);
-      else launch_sparse_nh<64, false>(ka, nh, grid, s);
-    } else {
-      return hipErrorInvalidValue;
-    }
+    if (a.head_dim == 128) launch_nh_d<128>(ka, nh, sparse, ragged, grid, s);
+    else if (a.head_dim == 64) launch_nh_d<64>(ka, nh, sparse, ragged, grid, s);
+    else return hipErrorInvalidValue;
     return hipGetLastError();
   }
   ka.map = make_map(a);

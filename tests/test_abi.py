@@ -230,8 +230,11 @@ def test_attn_workspace_bytes_formula(monkeypatch):
     L = seer.lib()
     monkeypatch.delenv("SEER_SPLIT_MIN_WIDTH", raising=False)
     monkeypatch.delenv("SEER_SPLIT_SPARSE", raising=False)
+    monkeypatch.delenv("SEER_SPLIT_DENSE", raising=False)
     up = lambda x: (x + 255) // 256 * 256
     d = _desc(B=1, Hq=32, Hkv=8, S=131072, D=128)
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == 0      # the split is opt-in
+    monkeypatch.setenv("SEER_SPLIT_DENSE", "1")
     nb, w = 2048, 128
     slots = sum(i // w + 1 for i in range(nb))
     want = up(32 * nb * 17 * 4) + up(32 * slots * 64 * 4) + up(32 * slots * 64 * 128 * 2)

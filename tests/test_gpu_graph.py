@@ -44,8 +44,9 @@ def _valid_idx(count, idx):
     return torch.where(keep, idx, torch.zeros_like(idx))
 
 
-def test_gate_sparse_and_split_dense_attention_replay(monkeypatch):
+def test_gate_sparse_and_dense_attention_replay(monkeypatch):
     monkeypatch.setenv("SEER_SPLIT_MIN_WIDTH", "1")  # the dense call splits its rows at this size
+    monkeypatch.setenv("SEER_SPLIT_DENSE", "1")
     B, Hq, Hkv, S, D = 1, 8, 2, 4096, 128
     host = [small_inputs(B, Hq, Hkv, S, D, "bf16", seed=stable_seed("graph", r), spikes=True)
             for r in range(REPLAYS)]
@@ -53,9 +54,9 @@ def test_gate_sparse_and_split_dense_attention_replay(monkeypatch):
     qd, kd, vd = (_bf16(x).cuda() for x in (q0, k0, v0))
     wqd, wkd = torch.from_numpy(wq).cuda(), torch.from_numpy(wk).cuda()
     mask = seer.alloc_mask(B, Hq, S, "cuda")
-    o_s, o_d = torch.empty_like(qd), torch.empty_like(qd)
+    o_s, o_d, o_u = torch.empty_like(qd), torch.empty_like(qd), torch.empty_like(qd)
     l_s = torch.empty((B, Hq, S), dtype=torch.float32, device="cuda")
-    l_d = torch.empty_like(l_s)
+    l_d, l_u = torch.empty_like(l_s), torch.empty_like(l_s)
     gws = torch.empty(seer.gate_workspace_bytes(qd, kd, wq.shape[-1]), dtype=torch.uint8, device="cuda")
     aws = torch.empty(max(seer.attn_workspace_bytes(qd, kd, vd), 1), dtype=torch.uint8, device="cuda")
     assert aws.numel() > 1, "the dense call should take the key-range split here"
@@ -64,6 +65,7 @@ def test_gate_sparse_and_split_dense_attention_replay(monkeypatch):
         seer.gate(qd, kd, wqd, wkd, mode=seer.TOPK_RATIO, topk_ratio=0.2, mask=mask, workspace=gws)
         seer.bsattn(qd, kd, vd, mask, out=o_s, lse=l_s)
         seer.dense_attn(qd, kd, vd, out=o_d, lse=l_d, workspace=aws)
+        seer.dense_attn(qd, kd, vd, out=o_u, lse=l_u)  # unsplit: two query heads per workgroup
 
     g = _capture(step)
     for r in range(REPLAYS):
@@ -73,12 +75,16 @@ def test_gate_sparse_and_split_dense_attention_replay(monkeypatch):
             dst.copy_(_bf16(src))
         g.replay()
         torch.cuda.synchronize()
-        got = [t.clone() for t in (mask.count, _valid_idx(mask.count, mask.idx), o_s, l_s, o_d, l_d)]
-        o_s.zero_(), o_d.zero_(), l_s.zero_(), l_d.zero_()
+        outs = (o_s, l_s, o_d, l_d, o_u, l_u)
+        got = [t.clone() for t in (mask.count, _valid_idx(mask.count, mask.idx)) + outs]
+        for t in outs:
+            t.zero_()
         step()
         torch.cuda.synchronize()
-        ref = (mask.count, _valid_idx(mask.count, mask.idx), o_s, l_s, o_d, l_d)
-        for name, a, b in zip(("count", "idx", "o sparse", "lse sparse", "o dense", "lse dense"), got, ref):
+        ref = (mask.count, _valid_idx(mask.count, mask.idx)) + outs
+        names = ("count", "idx", "o sparse", "lse sparse", "o split dense", "lse split dense", "o dense",
+                 "lse dense")
+        for name, a, b in zip(names, got, ref):
             assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), f"replay {r}: {name} differs"
 
 

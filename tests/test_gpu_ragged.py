@@ -122,6 +122,7 @@ def test_ragged_bsattn_parity(case, pattern, causal, block):
 @pytest.mark.parametrize("causal", [True, False])
 def test_ragged_dense_and_split_parity(case, causal, monkeypatch):
     monkeypatch.setenv("SEER_SPLIT_MIN_WIDTH", "1")
+    monkeypatch.setenv("SEER_SPLIT_DENSE", "1")
     B, Hq, Hkv, S, D, dt, Dg = case
     w, q, k, v, _, _ = _inputs(case, ("dense", causal))
     O_ref, lse_ref = oracle.attn(q, k, v, causal=causal)

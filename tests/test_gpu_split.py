@@ -1,10 +1,10 @@
 """GPU parity of the key-range split (seer_bsattn_ws / seer_dense_attn_ws): rows
 cut into 8 or 16 key ranges computed as separate tasks, bf16 partials merged.
 
-The split normally starts at 32 key blocks per range and applies to sparse
-rows only on request; these tests set SEER_SPLIT_MIN_WIDTH=1 and
-SEER_SPLIT_SPARSE=1 so that small shapes (1 to 4 blocks per range, both range
-counts, ragged GQA layouts) exercise it.  Bars as for the
+The split runs only on request and starts at 32 key blocks per range; these
+tests set SEER_SPLIT_DENSE=1, SEER_SPLIT_SPARSE=1 and SEER_SPLIT_MIN_WIDTH=1 so
+that small shapes (1 to 4 blocks per range, both range counts, ragged GQA
+layouts) exercise it.  Bars as for the
 unsplit kernel (max-abs 2e-2 against the fp64 oracle, LSE 1e-3, empty rows
 O = 0 and LSE = -inf); the split result also stays within 1e-2 of the unsplit
 one (the partials' bf16 rounding) and is bitwise reproducible."""
@@ -34,7 +34,8 @@ CASES = [
 @pytest.fixture(autouse=True)
 def _small_ranges(monkeypatch):
     monkeypatch.setenv("SEER_SPLIT_MIN_WIDTH", "1")
-    monkeypatch.setenv("SEER_SPLIT_SPARSE", "1")   # sparse rows split only on request
+    monkeypatch.setenv("SEER_SPLIT_SPARSE", "1")   # rows split only on request
+    monkeypatch.setenv("SEER_SPLIT_DENSE", "1")
 
 
 def _ws(qd, kd, vd):
