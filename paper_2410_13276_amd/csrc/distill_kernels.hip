@@ -148,6 +148,7 @@ constexpr int kT = 64;
 constexpr int kKc = 32;
 constexpr int kLoads = kT * kKc / 256;  // elements of each operand per thread and chunk
 static_assert(kT == kKlTile, "the logit gradient is written up to the end of each row's GEMM tile");
+static_assert(kT == 64 && kKc == 32 && kLoads == 8, "the element mapping of fetch and stash");
 
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
   __shared__ float sA[2][kKc][kT + 4];
@@ -174,42 +175,69 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
   const int64_t total = (int64_t)g.K1 * nck;
   const int64_t c0 = total * sp / splits, c1 = total * (sp + 1) / splits;
 
+  // Element u of this thread's share of a chunk: along the unit-stride index the
+  // thread's position is fixed and u steps the other index, so one offset per
+  // operand plus u times a uniform stride addresses every element (and the LDS
+  // side takes immediate offsets).
+  //   A, m fast: m = t % 64, k = t / 64 + 4u      A, k fast: m = t / 32 + 8u, k = t % 32
+  //   B, n fast: n = t % 64, k = t / 64 + 4u      B, k fast: n = t / 32 + 8u, k = t % 32
+  const int am = a_mfast ? t % 64 : t / 32, ak = a_mfast ? t / 64 : t % 32;
+  const int bn = b_nfast ? t % 64 : t / 32, bk = b_nfast ? t / 64 : t % 32;
+  const int64_t a_off = (int64_t)(m0 + am) * g.sam + (int64_t)ak * g.sak2;
+  const int64_t b_off = (int64_t)(n0 + bn) * g.sbn + (int64_t)bk * g.sbk2;
+  const int64_t a_du = a_mfast ? 4 * g.sak2 : 8 * g.sam;  // offset step per u
+  const int64_t b_du = b_nfast ? 4 * g.sbk2 : 8 * g.sbn;
+  const bool full_mn = m0 + kT <= g.M && n0 + kT <= g.N;
+
   float ra[kLoads], rb[kLoads];
-  auto fetch = [&](int64_t c) {
-    const int k1 = (int)(c / nck);
-    const int kk = k2lo + (int)(c % nck) * kKc;
-    const float* Ak = A + (int64_t)k1 * g.sak1;
-    const float* Bk = B + (int64_t)k1 * g.sbk1;
+  int k1 = 0, kc = 0;  // the chunk being fetched: K1 index, chunk within the k2 range
+  if (c0 < c1) {
+    k1 = (int)(c0 / nck);
+    kc = (int)(c0 % nck);
+  }
+  auto fetch = [&]() {
+    const int kk = k2lo + kc * kKc;
+    const float* Ak = A + (int64_t)k1 * g.sak1 + (int64_t)kk * g.sak2 + a_off;
+    const float* Bk = B + (int64_t)k1 * g.sbk1 + (int64_t)kk * g.sbk2 + b_off;
+    const int kmax = k2hi - kk;  // k of this chunk below kmax hold data
+    if (full_mn && kmax >= kKc) {
 #pragma unroll
-    for (int u = 0; u < kLoads; ++u) {
-      const int e = t + 256 * u;
-      const int m = a_mfast ? e % kT : e / kKc;
-      const int k = a_mfast ? e / kT : e % kKc;
-      const int gm = m0 + m, gk = kk + k;
-      ra[u] = (gm < g.M && gk < k2hi) ? Ak[(int64_t)gm * g.sam + (int64_t)gk * g.sak2] : 0.f;
-      const int n = b_nfast ? e % kT : e / kKc;
-      const int kb = b_nfast ? e / kT : e % kKc;
-      const int gn = n0 + n, gkb = kk + kb;
-      rb[u] = (gn < g.N && gkb < k2hi) ? Bk[(int64_t)gkb * g.sbk2 + (int64_t)gn * g.sbn] : 0.f;
+      for (int u = 0; u < kLoads; ++u) {
+        ra[u] = Ak[u * a_du];
+        rb[u] = Bk[u * b_du];
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < kLoads; ++u) {
+        const bool aok = a_mfast ? (m0 + am < g.M && ak + 4 * u < kmax) : (m0 + am + 8 * u < g.M && ak < kmax);
+        const bool bok = b_nfast ? (n0 + bn < g.N && bk + 4 * u < kmax) : (n0 + bn + 8 * u < g.N && bk < kmax);
+        ra[u] = aok ? Ak[u * a_du] : 0.f;
+        rb[u] = bok ? Bk[u * b_du] : 0.f;
+      }
+    }
+    if (++kc == nck) {
+      kc = 0;
+      ++k1;
     }
   };
   auto stash = [&](int buf) {
 #pragma unroll
     for (int u = 0; u < kLoads; ++u) {
-      const int e = t + 256 * u;
-      sA[buf][a_mfast ? e / kT : e % kKc][a_mfast ? e % kT : e / kKc] = ra[u];
-      sB[buf][b_nfast ? e / kT : e % kKc][b_nfast ? e % kT : e / kKc] = rb[u];
+      if (a_mfast) sA[buf][ak + 4 * u][am] = ra[u];
+      else sA[buf][ak][am + 8 * u] = ra[u];
+      if (b_nfast) sB[buf][bk + 4 * u][bn] = rb[u];
+      else sB[buf][bk][bn + 8 * u] = rb[u];
     }
   };
   if (c0 < c1) {
-    fetch(c0);
+    fetch();
     stash(0);
   }
   __syncthreads();
   int buf = 0;
   for (int64_t c = c0; c < c1; ++c) {
     const bool more = c + 1 < c1;
-    if (more) fetch(c + 1);
+    if (more) fetch();
     // wavefront (wm, wn) accumulates the 32x32 block at rows 32 wm, columns 32 wn
     // of the tile; each MFMA contracts the two k of one step, lane half hf
     // supplying k = 2 s + hf of row (or column) lane % 32
