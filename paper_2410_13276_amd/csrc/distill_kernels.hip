@@ -140,19 +140,24 @@ __global__ __launch_bounds__(256) void loss_mean_kernel(const double* __restrict
 // 64x64 output tile per 256-thread workgroup (a 32x32 fp32-MFMA block per
 // wavefront, v_mfma_f32_32x32x2_f32), K in chunks of 32 staged through two LDS
 // buffers: the next chunk's global loads are in flight in registers while the
-// current chunk's MFMAs run, one barrier per chunk.  Operand tiles are read
-// along whichever index has unit stride, so that loads coalesce for every
-// layout used here.  blockIdx.z = z * splits + s: part s of the tile's (k1, k2)
-// chunks; with splits > 1 the part's product goes to g.part.
+// current chunk's MFMAs run, one barrier per chunk.  The LDS tiles are
+// [row][k] with k contiguous (rows padded to 36 floats, 16-byte aligned and
+// conflict-free for 16-byte reads), so a lane reads the 16 k values of its
+// next 16 MFMAs with four 16-byte reads: MFMA step s contracts k = s (lanes
+// 0-31) and k = 16 + s (lanes 32-63).  Operand tiles are read from global
+// memory along whichever index has unit stride, so that loads coalesce for
+// every layout used here.  blockIdx.z = z * splits + s: part s of the tile's
+// (k1, k2) chunks; with splits > 1 the part's product goes to g.part.
 constexpr int kT = 64;
 constexpr int kKc = 32;
+constexpr int kKp = kKc + 4;              // LDS row stride (floats)
 constexpr int kLoads = kT * kKc / 256;  // elements of each operand per thread and chunk
 static_assert(kT == kKlTile, "the logit gradient is written up to the end of each row's GEMM tile");
 static_assert(kT == 64 && kKc == 32 && kLoads == 8, "the element mapping of fetch and stash");
 
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
-  __shared__ float sA[2][kKc][kT + 4];
-  __shared__ float sB[2][kKc][kT + 4];
+  __shared__ __attribute__((aligned(16))) float sA[2][kT][kKp];
+  __shared__ __attribute__((aligned(16))) float sB[2][kT][kKp];
   const int t = threadIdx.x;
   const int m0 = blockIdx.y * kT, n0 = blockIdx.x * kT;
   const int z = blockIdx.z / splits, sp = blockIdx.z % splits;
@@ -175,18 +180,17 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
   const int64_t total = (int64_t)g.K1 * nck;
   const int64_t c0 = total * sp / splits, c1 = total * (sp + 1) / splits;
 
-  // Element u of this thread's share of a chunk: along the unit-stride index the
-  // thread's position is fixed and u steps the other index, so one offset per
-  // operand plus u times a uniform stride addresses every element (and the LDS
-  // side takes immediate offsets).
-  //   A, m fast: m = t % 64, k = t / 64 + 4u      A, k fast: m = t / 32 + 8u, k = t % 32
-  //   B, n fast: n = t % 64, k = t / 64 + 4u      B, k fast: n = t / 32 + 8u, k = t % 32
-  const int am = a_mfast ? t % 64 : t / 32, ak = a_mfast ? t / 64 : t % 32;
-  const int bn = b_nfast ? t % 64 : t / 32, bk = b_nfast ? t / 64 : t % 32;
-  const int64_t a_off = (int64_t)(m0 + am) * g.sam + (int64_t)ak * g.sak2;
-  const int64_t b_off = (int64_t)(n0 + bn) * g.sbn + (int64_t)bk * g.sbk2;
-  const int64_t a_du = a_mfast ? 4 * g.sak2 : 8 * g.sam;  // offset step per u
-  const int64_t b_du = b_nfast ? 4 * g.sbk2 : 8 * g.sbn;
+  // Element u of this thread's share of a chunk.  Row index fast in memory:
+  // row = t % 64, k = 8 (t / 64) + u (the thread's 8 values are contiguous in
+  // the LDS row: two 16-byte writes).  k fast: row = t / 32 + 8u, k = t % 32.
+  // Either way one offset per operand plus u times a uniform stride addresses
+  // every element.
+  const int ar = a_mfast ? t % 64 : t / 32, ak = a_mfast ? 8 * (t / 64) : t % 32;
+  const int br = b_nfast ? t % 64 : t / 32, bk = b_nfast ? 8 * (t / 64) : t % 32;
+  const int64_t a_off = (int64_t)(m0 + ar) * g.sam + (int64_t)ak * g.sak2;
+  const int64_t b_off = (int64_t)(n0 + br) * g.sbn + (int64_t)bk * g.sbk2;
+  const int64_t a_du = a_mfast ? g.sak2 : 8 * g.sam;  // offset step per u
+  const int64_t b_du = b_nfast ? g.sbk2 : 8 * g.sbn;
   const bool full_mn = m0 + kT <= g.M && n0 + kT <= g.N;
 
   float ra[kLoads], rb[kLoads];
@@ -209,8 +213,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
     } else {
 #pragma unroll
       for (int u = 0; u < kLoads; ++u) {
-        const bool aok = a_mfast ? (m0 + am < g.M && ak + 4 * u < kmax) : (m0 + am + 8 * u < g.M && ak < kmax);
-        const bool bok = b_nfast ? (n0 + bn < g.N && bk + 4 * u < kmax) : (n0 + bn + 8 * u < g.N && bk < kmax);
+        const bool aok = a_mfast ? (m0 + ar < g.M && ak + u < kmax) : (m0 + ar + 8 * u < g.M && ak < kmax);
+        const bool bok = b_nfast ? (n0 + br < g.N && bk + u < kmax) : (n0 + br + 8 * u < g.N && bk < kmax);
         ra[u] = aok ? Ak[u * a_du] : 0.f;
         rb[u] = bok ? Bk[u * b_du] : 0.f;
       }
@@ -221,12 +225,19 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
     }
   };
   auto stash = [&](int buf) {
+    if (a_mfast) {
+      *reinterpret_cast<f32x4*>(&sA[buf][ar][ak]) = f32x4{ra[0], ra[1], ra[2], ra[3]};
+      *reinterpret_cast<f32x4*>(&sA[buf][ar][ak + 4]) = f32x4{ra[4], ra[5], ra[6], ra[7]};
+    } else {
 #pragma unroll
-    for (int u = 0; u < kLoads; ++u) {
-      if (a_mfast) sA[buf][ak + 4 * u][am] = ra[u];
-      else sA[buf][ak][am + 8 * u] = ra[u];
-      if (b_nfast) sB[buf][bk + 4 * u][bn] = rb[u];
-      else sB[buf][bk][bn + 8 * u] = rb[u];
+      for (int u = 0; u < kLoads; ++u) sA[buf][ar + 8 * u][ak] = ra[u];
+    }
+    if (b_nfast) {
+      *reinterpret_cast<f32x4*>(&sB[buf][br][bk]) = f32x4{rb[0], rb[1], rb[2], rb[3]};
+      *reinterpret_cast<f32x4*>(&sB[buf][br][bk + 4]) = f32x4{rb[4], rb[5], rb[6], rb[7]};
+    } else {
+#pragma unroll
+      for (int u = 0; u < kLoads; ++u) sB[buf][br + 8 * u][bk] = rb[u];
     }
   };
   if (c0 < c1) {
@@ -238,13 +249,18 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
   for (int64_t c = c0; c < c1; ++c) {
     const bool more = c + 1 < c1;
     if (more) fetch();
-    // wavefront (wm, wn) accumulates the 32x32 block at rows 32 wm, columns 32 wn
-    // of the tile; each MFMA contracts the two k of one step, lane half hf
-    // supplying k = 2 s + hf of row (or column) lane % 32
+    // wavefront (wm, wn) accumulates the 32x32 block at rows 32 wm, columns 32
+    // wn of the tile; lane (hf, col) supplies k = 16 hf + s of its row (A) and
+    // column (B) to MFMA step s
+    f32x4 av[4], bv[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      av[q] = *reinterpret_cast<const f32x4*>(&sA[buf][32 * wm + col][16 * hf + 4 * q]);
+      bv[q] = *reinterpret_cast<const f32x4*>(&sB[buf][32 * wn + col][16 * hf + 4 * q]);
+    }
 #pragma unroll
     for (int st = 0; st < kKc / 2; ++st)
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sA[buf][2 * st + hf][32 * wm + col],
-                                                 sB[buf][2 * st + hf][32 * wn + col], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[st / 4][st % 4], bv[st / 4][st % 4], acc, 0, 0, 0);
     if (more) stash(buf ^ 1);
     __syncthreads();
     buf ^= 1;
