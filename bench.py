@@ -176,6 +176,12 @@ def main() -> int:
         step()
     torch.cuda.synchronize()
     active = int(mask.count.sum().item())
+    # active diagonal tiles (half of each is above the causal diagonal): a row's
+    # list is ascending, so the diagonal is active iff its last entry is i
+    cnt = mask.count.long()
+    last = mask.idx.gather(-1, (cnt - 1).clamp(min=0).unsqueeze(-1)).squeeze(-1).long() & 0xFFFF
+    rows_i = torch.arange(cnt.shape[-1], device=cnt.device)
+    active_diag = int(((cnt > 0) & (last == rows_i)).sum().item())
     nb = w.n_blocks
     causal_tiles = w.batch * w.heads_q * nb * (nb + 1) // 2
     sparsity = 1.0 - active / causal_tiles
@@ -328,11 +334,15 @@ def main() -> int:
                    "parallelism": "single GPU"},
         "value_definition": "active-tile attention flops / (gate + block-sparse attention) step time",
         "attn_tflops": round(attn_tflops, 2),
+        "useful_attn_tflops": round(flops_tile * (active - 0.5 * active_diag) / (attn_ms * 1e-3) / 1e12, 2),
         "attn_ms": round(attn_ms, 4),
         "attn_ms_min": round(attn_min, 4),
         "gate_ms": round(gate_ms, 4),
         "dense_ms": round(dense_ms, 3),
         "dense_tflops": round(dense_flops / (dense_ms * 1e-3) / 1e12, 2),
+        "useful_dense_tflops": round(flops_tile * (causal_tiles - 0.5 * w.batch * w.heads_q * nb)
+                                     / (dense_ms * 1e-3) / 1e12, 2),
+        "useful_flops_note": "useful_* count each diagonal tile as half (its upper triangle is masked)",
         "sparsity": round(sparsity, 5),
         "active_tiles": active,
         "speedup_vs_dense": round(speedup, 3),
