@@ -10,9 +10,10 @@
 // query block) row of the block mask: 64 queries, 32 per wavefront.  It walks
 // the row's ascending list of active key blocks; per key block the K and V
 // tiles reach LDS by direct loads (row-major, swizzled), the next tile's loads
-// in flight while the current one is consumed.  With a mask shared by a KV
-// group, one workgroup holds 2 (or 4) query heads of the group for the same
-// query block and each K/V tile load serves all of them.
+// in flight while the current one is consumed.  Where every query head of a
+// KV group walks the same row (a mask shared by the group, and dense rows), one
+// workgroup holds 2 (or 4) query heads of the group for the same query block
+// and each K/V tile load serves all of them.
 //
 // Ground-truth mode (appendix A.1, Eq. 5-6; the distillation target of Eq. 2):
 // the dense kernel also stores, per query and key tile, the tile row maximum of
