@@ -44,9 +44,13 @@ def _valid_idx(count, idx):
     return torch.where(keep, idx, torch.zeros_like(idx))
 
 
-def test_gate_sparse_and_dense_attention_replay(monkeypatch):
+@pytest.mark.parametrize("batched", [False, True], ids=["one_launch", "batched_launches"])
+def test_gate_sparse_and_dense_attention_replay(batched, monkeypatch):
     monkeypatch.setenv("SEER_SPLIT_MIN_WIDTH", "1")  # the dense call splits its rows at this size
     monkeypatch.setenv("SEER_SPLIT_DENSE", "1")
+    if batched:  # the sparse call launches its rows in batches of 64 workgroups
+        monkeypatch.setenv("SEER_EPOCH_MIN_BLOCKS", "1")
+        monkeypatch.setenv("SEER_EPOCH_WGS", "64")
     B, Hq, Hkv, S, D = 1, 8, 2, 4096, 128
     host = [small_inputs(B, Hq, Hkv, S, D, "bf16", seed=stable_seed("graph", r), spikes=True)
             for r in range(REPLAYS)]
