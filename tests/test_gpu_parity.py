@@ -228,17 +228,18 @@ def test_strided_views():
     assert _max_abs(from_device(o.contiguous()).reshape(-1, 64, D), O_ref) <= ATOL_BF16
 
 
-@pytest.mark.parametrize("case", [(1, 8, 2, 4096, 128), (2, 4, 1, 3000, 64), (1, 4, 4, 2048, 128)],
+@pytest.mark.parametrize("case", [(1, 8, 2, 4096, 128, 64), (2, 4, 1, 3000, 64, 64), (1, 4, 4, 2048, 128, 64),
+                                  (1, 4, 2, 4096, 128, 128)],
                          ids=lambda c: "x".join(map(str, c)))
 def test_batched_launches_equal_single_launch(case, monkeypatch):
     """Long sparse rows launch in batches of the resident workgroups (task ids
     continue across batches); forced here on small shapes with small batches,
     the outputs must equal the single launch's bit for bit."""
-    B, Hq, Hkv, S, D = case
+    B, Hq, Hkv, S, D, blk = case
     w, q, k, v, wq, wk = small_inputs(B, Hq, Hkv, S, D, "bf16", seed=stable_seed("batches", case), spikes=True)
     qd, kd, vd = (to_device(x) for x in (q, k, v))
     mask = seer.gate(qd, kd, torch.from_numpy(wq).cuda(), torch.from_numpy(wk).cuda(), mode=seer.TOPK_RATIO,
-                     topk_ratio=0.3)
+                     topk_ratio=0.3, block=blk)
     monkeypatch.setenv("SEER_EPOCH_WGS", "0")
     o1, l1 = seer.bsattn(qd, kd, vd, mask, want_lse=True)
     monkeypatch.setenv("SEER_EPOCH_MIN_BLOCKS", "1")
