@@ -1206,10 +1206,10 @@ static void launch_nh_d(const KernelArgs& ka, int nh, bool sparse, bool ragged, 
 // box, 18.1 -> 17.1 ms on another, and 48.9 -> 48.2 ms with per-head densities
 // spread over 5-40%; at 32768 tokens the batch ends' idle time outweighed the
 // gain (1.84 -> 2.06 ms; at 65536 tokens with 7 heads of 5-40% density 7.6 ->
-// 10.6 ms), hence the size threshold.  The
-// environment variables SEER_EPOCH_MIN_BLOCKS (the threshold in 64-token
-// blocks, default 2048) and SEER_EPOCH_WGS (the batch size; 0 disables) are
-// read on the host at each call.
+// 10.6 ms), hence the size threshold.  The environment variables
+// SEER_EPOCH_MIN_BLOCKS (the threshold in 64-token blocks, default 2048) and
+// SEER_EPOCH_WGS (the batch size; 0 disables) are read on the host at each
+// call.
 static int epoch_min_blocks() {
   int v = 2048;
   if (const char* e = getenv("SEER_EPOCH_MIN_BLOCKS")) v = atoi(e);
