@@ -308,15 +308,17 @@ def main() -> int:
     kv_group_bytes = 2 * nb * 64 * D * (2 if w.dtype == "bf16" else 4)
     multi = any(groups % g == 0 and nb % (8 // g) == 0 and g * kv_group_bytes <= 32 * 2 ** 20 for g in (8, 4, 2))
     launches = groups if (groups > 1 and not multi and nb % 8 == 0 and not sparse_split) else 1
-    # rows of 2048 or more blocks launch in batches of the resident workgroups
-    # (4 per CU for the per-head sparse kernel: 2-wavefront workgroups, 2
-    # wavefronts per SIMD), continuing the task ids across batches
+    # rows of 2048 or more blocks launch the heavier half of their tasks in
+    # batches of the resident workgroups (4 per CU for the per-head sparse
+    # kernel: 2-wavefront workgroups, 2 wavefronts per SIMD) and the rest in one
+    # launch, continuing the task ids across launches
     if w.dtype == "bf16" and not sparse_split and nb >= int(os.environ.get("SEER_EPOCH_MIN_BLOCKS", "2048")):
         resident = int(os.environ.get("SEER_EPOCH_WGS", "0")) // 8 * 8 if "SEER_EPOCH_WGS" in os.environ \
             else torch.cuda.get_device_properties(0).multi_processor_count * 4 // 8 * 8
         tasks = w.batch * w.heads_q * nb // launches
         if resident > 0 and tasks > resident:
-            launches *= -(-tasks // resident)
+            batched = -(-(tasks // 2) // resident) * resident  # the heavier half in batches
+            launches *= batched // resident + (1 if tasks > batched else 0)
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     traffic = _traffic(w.name)
     es = 2 if w.dtype == "bf16" else 4

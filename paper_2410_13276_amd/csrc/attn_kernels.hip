@@ -1201,12 +1201,14 @@ static void launch_nh_d(const KernelArgs& ka, int nh, bool sparse, bool ragged, 
 // GPU holds at once (4 per CU), so that the rows of a batch start together and
 // walk their ascending lists roughly in step: concurrent rows then share more
 // of their K/V tiles in L2.  Within a batch the order is the usual one (task
-// ids continue across batches), so every output is unchanged.  Measured at
-// 131072 tokens (32 q / 8 KV heads, TopK 0.1): 17.6 -> 17.0 ms per call on one
-// box, 18.1 -> 17.1 ms on another, and 48.9 -> 48.2 ms with per-head densities
-// spread over 5-40%; at 32768 tokens the batch ends' idle time outweighed the
-// gain (1.84 -> 2.06 ms; at 65536 tokens with 7 heads of 5-40% density 7.6 ->
-// 10.6 ms), hence the size threshold.  The environment variables
+// ids continue across batches), so every output is unchanged.  Only the
+// heavier half of the tasks is batched: the later batches' short rows leave too
+// much idle time at their ends.  Measured at 131072 tokens (32 q / 8 KV heads,
+// TopK 0.1): 17.29 ms unbatched, 16.92 ms with every task batched, 16.65 ms
+// with the heavier half batched; 48.9 -> 48.2 ms (all batched) with per-head
+// densities spread over 5-40%; at 32768 tokens the batch ends' idle time
+// outweighed the gain (1.84 -> 2.06 ms; at 65536 tokens with 7 heads of 5-40%
+// density 7.6 -> 10.6 ms), hence the size threshold.  The environment variables
 // SEER_EPOCH_MIN_BLOCKS (the threshold in 64-token blocks, default 2048) and
 // SEER_EPOCH_WGS (the batch size; 0 disables) are read on the host at each
 // call.
@@ -1293,9 +1295,13 @@ static hipError_t launch_attn_one(const AttnArgs& a, hipStream_t s) {
   if (a.bf16 && sparse && !pool && a.n_blocks >= epoch_min_blocks()) {
     const int E = resident_workgroups(a.head_dim, ragged);
     if (E > 0 && total > E) {
-      for (int64_t b0 = 0; b0 < total; b0 += E) {
+      // the heavier half of the tasks (the longest rows) in batches, the rest
+      // (whose short rows would leave batch ends idle) in one launch
+      const int64_t batched = (total / 2 + E - 1) / E * E;
+      for (int64_t b0 = 0, cnt = 0; b0 < total; b0 += cnt) {
+        cnt = b0 < batched ? std::min<int64_t>(E, total - b0) : total - b0;
         ka.task_base = (int)b0;
-        const dim3 g((unsigned)std::min<int64_t>(E, total - b0));
+        const dim3 g((unsigned)cnt);
         if (a.head_dim == 128) {
           if (ragged) hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true, false, true>), g, block, 0, s, ka);
           else hipLaunchKernelGGL((attn_fwd_bf16_kernel<128, true, false, false>), g, block, 0, s, ka);
