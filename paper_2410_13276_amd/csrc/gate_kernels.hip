@@ -9,9 +9,10 @@
 //   gate_logits_kernel  Eq. 1: Qg Kg^T / sqrt(Dg) on the block-causal lower
 //                       triangle, fp32 MFMA (v_mfma_f32_32x32x2_f32), 128x128 tiles.
 //   select_kernel       Eq. 3 (TopK by an exact select: one pass over 256
-//                       equal-width value buckets, then 8-bit digits of
-//                       order-preserving keys inside the target bucket, each
-//                       from a per-wavefront LDS histogram; ties to the smaller
+//                       equal-width value buckets, then, inside the target
+//                       bucket, ranks of its gathered keys (at most 64) or
+//                       8-bit digits of order-preserving keys, each from a
+//                       per-wavefront LDS histogram; ties to the smaller
 //                       block index) or Eq. 4 (strict
 //                       threshold on the row softmax), plus the always-kept first
 //                       and diagonal blocks; one wavefront per query-block row,
@@ -472,7 +473,11 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
       // a time.  Each pass histograms the candidates still in play in a
       // per-wavefront LDS histogram; `above` counts candidates already known to
       // lie above; once exactly `take` candidates lie at or above the current
-      // prefix the selected set is fixed.
+      // prefix the selected set is fixed.  When the target bucket holds at most
+      // 64 candidates (the usual case: a few per bucket) their keys are instead
+      // gathered one per lane and T is read off their ranks, which costs one
+      // scan of the row instead of one per digit (gate 0.806 -> 0.777 ms at
+      // 131072 tokens, the same masks).
       float cmx = -INFINITY, cmn = INFINITY;
 #pragma unroll
       for (int m = 0; m < MAXM; ++m)
@@ -529,7 +534,37 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
       uint32_t prefix = 0;
       int cntT = take + 1;  // != take until the set closes early
       int shift = 0;
-      if (!closed_bucket) {
+      if (!closed_bucket && cb <= kWave) {
+        // few candidates in the target bucket: gather their keys, one per lane,
+        // and find T as the key of rank take - above among them (by value)
+        __builtin_amdgcn_wave_barrier();
+        const uint64_t lt = lanemask_lt();
+        int n = 0;
+#pragma unroll
+        for (int m = 0; m < MAXM; ++m) {
+          if (m < M) {
+            const bool in_b = ((cand >> m) & 1) && bucket(v[m]) == (uint32_t)bstar;
+            const uint64_t bal = __ballot(in_b);
+            if (bal) {
+              if (in_b) hist[n + __popcll(bal & lt)] = ordered_key(v[m]);
+              n += __popcll(bal);
+            }
+          }
+        }
+        __builtin_amdgcn_wave_barrier();
+        const uint32_t key = lane < cb ? hist[lane] : 0u;
+        int g = 0, eqc = 0;
+        for (int t = 0; t < cb; ++t) {
+          const uint32_t kt = hist[t];
+          g += kt > key ? 1 : 0;
+          eqc += kt == key ? 1 : 0;
+        }
+        const int want = take - above;  // 1 <= want <= cb - 1
+        const uint64_t hit = __ballot(lane < cb && g < want && g + eqc >= want);
+        const int src = __builtin_ctzll(hit);
+        prefix = __shfl(key, src);
+        above += __shfl(g, src);
+      } else if (!closed_bucket) {
         for (int d = 3; d >= 0; --d) {
           const int sh = 8 * d;
           int b;
