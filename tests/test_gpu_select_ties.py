@@ -8,7 +8,10 @@ selection must equal the oracle's bit for bit, including which tied blocks it
 keeps (the smaller block index wins, Eq. 3 with the tie rule of the ABI).  This
 drives the select kernel through its exact paths: rows whose cut falls inside a
 run of equal logits, all-equal rows (zero query weights), and buckets holding a
-single value."""
+single value; cut buckets of at most 64 candidates (resolved from the ranks of
+their gathered keys: hundreds of rows per case from 65 blocks up) and of more
+(resolved digit by digit: over a thousand rows in the 700- and 1100-block
+cases)."""
 import numpy as np
 import pytest
 
