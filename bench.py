@@ -164,7 +164,7 @@ def main() -> int:
     o = torch.empty_like(qd)
     od = torch.empty_like(qd)
     # key-range split workspace (sparse and dense get the same treatment)
-    n_aws = seer.attn_workspace_bytes(qd, kd, vd)
+    n_aws = seer.attn_workspace_bytes(qd, kd, vd)  # 0: the split is opt-in
     aws = torch.empty(n_aws, dtype=torch.uint8, device="cuda") if n_aws else None
     stream = torch.cuda.current_stream()
 
@@ -295,30 +295,10 @@ def main() -> int:
 
     active_flops = flops_tile * active
     D = w.head_dim
-    sparse_split = aws is not None and os.environ.get("SEER_SPLIT_SPARSE") == "1"
-    rg = "true" if w.seq_len % 64 else "false"  # partial last tile
-    attn_kernels = (f"split_bounds_kernel + attn_fwd_bf16_kernel<{D}, true, true, {rg}, 1> + split_merge_kernel<{D}> "
-                    "(one seer_bsattn_ws call)" if sparse_split else f"attn_fwd_bf16_kernel<{D}, true, false, {rg}, 1>")
+    attn_kernels = f"attn_fwd_bf16_kernel<{D}, true, false, {'true' if w.seq_len % 64 else 'false'}, 1>"
     attn_tflops = active_flops / (attn_ms * 1e-3) / 1e12
-    # one seer_bsattn call is one launch per KV group when the task order's phases
-    # hold a single group (no phase of 2, 4 or 8 groups divides the groups, splits
-    # the query blocks evenly over the XCDs and keeps its K and V within 32 MiB),
-    # else one launch (the library's launch rule)
-    groups = w.batch * w.heads_kv
-    kv_group_bytes = 2 * nb * 64 * D * (2 if w.dtype == "bf16" else 4)
-    multi = any(groups % g == 0 and nb % (8 // g) == 0 and g * kv_group_bytes <= 32 * 2 ** 20 for g in (8, 4, 2))
-    launches = groups if (groups > 1 and not multi and nb % 8 == 0 and not sparse_split) else 1
-    # rows of 2048 or more blocks launch the heavier half of their tasks in
-    # batches of the resident workgroups (4 per CU for the per-head sparse
-    # kernel: 2-wavefront workgroups, 2 wavefronts per SIMD) and the rest in one
-    # launch, continuing the task ids across launches
-    if w.dtype == "bf16" and not sparse_split and nb >= int(os.environ.get("SEER_EPOCH_MIN_BLOCKS", "2048")):
-        resident = int(os.environ.get("SEER_EPOCH_WGS", "0")) // 8 * 8 if "SEER_EPOCH_WGS" in os.environ \
-            else torch.cuda.get_device_properties(0).multi_processor_count * 4 // 8 * 8
-        tasks = w.batch * w.heads_q * nb // launches
-        if resident > 0 and tasks > resident:
-            batched = -(-(tasks // 2) // resident) * resident  # the heavier half in batches
-            launches *= batched // resident + (1 if tasks > batched else 0)
+    # launches of the attention kernel one seer_bsattn call makes (the library's own count)
+    launches = seer.attn_launches(qd, kd, vd, mask, workspace_bytes=0 if aws is None else aws.numel())
     peak = PEAK_BF16_TFLOPS if w.dtype == "bf16" else PEAK_F32_TFLOPS
     traffic = _traffic(w.name)
     es = 2 if w.dtype == "bf16" else 4

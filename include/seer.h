@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SEER_ABI_VERSION 2
+#define SEER_ABI_VERSION 3
 #define SEER_BLOCK 64 /* the attention tile edge and the default gate block (section 4); gate
                         blocks and masks of 128 tokens are the other size the paper names */
 
@@ -91,8 +91,9 @@ typedef struct {
 
 /* AttnGate parameters (section 3.1, Eq. 1; selection per Eq. 3 / Eq. 4). */
 typedef struct {
-  int32_t block;       /* pooling kernel = stride = mask block: 64 or 128 tokens (the paper's
-                          sparse kernel takes "64 or 128", section 3.3); seq_len % block == 0 */
+  int32_t block;       /* pooling kernel = stride = mask block: 64 or 128 tokens (the two block
+                          sizes section 3.3 gives for the sparse kernel); the last block may be
+                          partial (see the conventions above) */
   int32_t gate_dim;    /* Dg, output width of the gate linear layers: 32, 64 or 128 */
   int32_t w_per_head;  /* 1: wq [heads_q][D][Dg], wk [heads_kv][3D][Dg];
                           0: one wq [D][Dg] and one wk [3D][Dg] shared by all heads */
@@ -128,6 +129,31 @@ typedef struct {
   uint8_t* dense;    /* optional device [batch][heads][nb][nb] 0/1 copy, or NULL */
   int32_t kv_shared; /* 0: rows per query head; 1: rows per KV head (see above) */
 } seer_block_mask;
+
+/* Launch options of the attention calls.  They choose how the work is
+ * scheduled, never what is computed (apart from the split's bf16 rounding of
+ * its partial outputs).  A NULL pointer or a zero field selects the default. */
+typedef struct {
+  int32_t split;            /* 1: cut long causal bf16 rows into key ranges (seer_bsattn_ws /
+                               seer_dense_attn_ws with a workspace of seer_attn_workspace_bytes);
+                               0: never (default) */
+  int32_t split_width;      /* key blocks per range; <= 0: sized so that a range's K and V fill
+                               an XCD's 4 MB L2 (128 blocks at head_dim 128) */
+  int32_t heads_per_wg;     /* cap on the query heads one workgroup serves where the heads of a
+                               KV group share their rows (dense attention, the ground truth, a
+                               kv_shared mask): 1, 2 or 4; 0: 2 */
+  int32_t batch_min_blocks; /* per-head sparse rows of at least this many 64-token blocks launch
+                               the heavier half of their tasks in batches of resident workgroups;
+                               0: 2048; < 0: never */
+  int32_t batch_wgs;        /* workgroups per such batch (rounded down to a multiple of 8);
+                               0: as many as the GPU holds at once */
+} seer_attn_opts;
+
+/* Options of seer_gate_distill (NULL or zero fields: defaults). */
+typedef struct {
+  int32_t gemm_min_chunks;  /* the backward products split their reduction into parts of at
+                               least this many 32-wide chunks; 0: 8 */
+} seer_distill_opts;
 
 /* ABI version (SEER_ABI_VERSION of the built library). */
 int seer_abi_version(void);
@@ -202,39 +228,52 @@ seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm
 
 /*
  * Workspace bytes that let seer_bsattn_ws / seer_dense_attn_ws run the
- * key-range split for this shape, or 0 when the shape does not split (then
- * those calls need no workspace).  The split is opt-in: dense calls split only
- * when the environment variable SEER_SPLIT_DENSE is 1, sparse calls only when
- * SEER_SPLIT_SPARSE is 1 (both read at each call; the unsplit kernels measured
- * as fast or faster on this hardware).  It applies to causal bf16 attention
- * with nb a multiple of 16 and nb / 16 >= the minimum range width (32 blocks;
- * the environment variable SEER_SPLIT_MIN_WIDTH overrides it); dense rows take
- * 16 ranges, sparse rows 8 when batch * heads_kv is even, else 16.  Size: 68
- * bytes per query block plus (256 + 128 head_dim) bytes per partial slot; a
- * query head has sum over i of (floor(i / (nb / 16)) + 1), about 8.5 nb, slots
- * (9.3 GB for 32 heads of 131072 tokens, head_dim 128).
+ * key-range split for this shape and options, or 0 when the call does not
+ * split (then it needs no workspace).  The split is opt-in (opts->split = 1;
+ * the unsplit kernels measured faster on this hardware at the workloads here)
+ * and applies to causal bf16 attention when a row can reach more than one
+ * range of w key blocks (w = opts->split_width, or 128 at head_dim 128 and 256
+ * at head_dim 64).  With P = ceil(nb / w) ranges: (P + 3) ints per query block,
+ * 32 bytes of task-queue tickets, and (256 + 128 head_dim) bytes per partial
+ * slot; a query head has sum over i of (floor(i / w) + 1) slots (8.6 GB for 32
+ * heads of 131072 tokens at head_dim 128).  0 on invalid arguments.
  */
-size_t seer_attn_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t causal);
+size_t seer_attn_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t causal,
+                                 const seer_attn_opts* opts);
 
 /*
- * seer_bsattn / seer_dense_attn with a workspace for the key-range split: each
- * causal row is cut into 16 ranges of key blocks computed as separate tasks,
- * the ranges of one KV group distributed over the XCDs so that each XCD's L2
- * holds the K/V it reads; the normalised partial outputs (bf16) and their
- * log-sum-exps go to the workspace and a merge kernel writes O and LSE.  O may
- * differ from the unsplit call by the rounding of the partials (well inside
- * the bf16 output tolerance).  With workspace NULL, or smaller than
- * seer_attn_workspace_bytes, or a shape that does not split, the call is the
- * unsplit one.  workspace: device memory, 256-byte aligned; contents on
- * return unspecified.
+ * seer_bsattn / seer_dense_attn with launch options and a workspace for the
+ * key-range split (section 3.3's kernel, scheduled for L2 locality): each
+ * causal row is cut into ranges of w key blocks computed as separate tasks by
+ * persistent workgroups that take the tasks in (KV group, range, query block)
+ * order, so that every XCD reads one range's K and V at a time; a task writes
+ * its normalised partial output (bf16) and log-sum-exp to the workspace, and a
+ * row's last task merges them in a fixed order (results are reproducible bit
+ * for bit).  O may differ from the unsplit call by the rounding of the
+ * partials (well inside the bf16 output tolerance).  With opts NULL or
+ * opts->split = 0, workspace NULL or smaller than seer_attn_workspace_bytes,
+ * or a shape that does not split, the call is the unsplit one with the other
+ * options applied.  workspace: device memory, 256-byte aligned; contents on
+ * return unspecified.  SEER_ERR_INVALID_ARG for an option outside its range.
  */
 seer_status seer_bsattn_ws(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
                            int32_t causal, float sm_scale, const void* q, const void* k,
                            const void* v, void* o, float* lse, void* workspace,
-                           size_t workspace_bytes, void* stream);
+                           size_t workspace_bytes, const seer_attn_opts* opts, void* stream);
 seer_status seer_dense_attn_ws(const seer_attn_desc* desc, int32_t causal, float sm_scale,
                                const void* q, const void* k, const void* v, void* o, float* lse,
-                               void* workspace, size_t workspace_bytes, void* stream);
+                               void* workspace, size_t workspace_bytes, const seer_attn_opts* opts,
+                               void* stream);
+
+/*
+ * Number of attention-kernel launches one seer_bsattn_ws / seer_dense_attn_ws
+ * call with these arguments makes (mask_kind 0: dense, 1: a per-query-head
+ * mask of `block`-token blocks, 2: a kv_shared mask), on the current device;
+ * -1 on invalid arguments.  Launches nothing.  (Long sparse rows launch in
+ * batches and a KV group at a time, so one call can be tens of launches.)
+ */
+int32_t seer_attn_launches(const seer_attn_desc* desc, int32_t block, int32_t mask_kind, int32_t causal,
+                           const seer_attn_opts* opts, size_t workspace_bytes);
 
 /*
  * Compacts a 0/1 block mask dense (device uint8 [B][heads][nb][nb], heads =
@@ -266,16 +305,19 @@ size_t seer_attn_gt_workspace_bytes(const seer_attn_desc* desc, int32_t block, i
  * groups per launch as it holds (all at once with
  * seer_attn_gt_workspace_bytes(desc, block, 0)), several launches on `stream`
  * otherwise.  Its contents on return are unspecified.
+ * opts (may be NULL): heads_per_wg applies; the split does not.
  * Errors: as seer_dense_attn; SEER_ERR_WORKSPACE if the workspace is missing
  * or smaller than one KV group needs.
  */
 seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t causal, float sm_scale,
                          const void* q, const void* k, const void* v, void* o, float* lse,
-                         float* gt, void* workspace, size_t workspace_bytes, void* stream);
+                         float* gt, void* workspace, size_t workspace_bytes, const seer_attn_opts* opts,
+                         void* stream);
 
-/* Bytes of device workspace seer_gate_distill needs for this shape (0 on
- * invalid arguments). */
-size_t seer_gate_distill_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate);
+/* Bytes of device workspace seer_gate_distill needs for this shape and options
+ * (0 on invalid arguments). */
+size_t seer_gate_distill_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate,
+                                         const seer_distill_opts* opts);
 
 /*
  * One distillation step of the gate (section 3.2, Eq. 2): the forward of
@@ -290,14 +332,16 @@ size_t seer_gate_distill_workspace_bytes(const seer_attn_desc* desc, const seer_
  * gt: device fp32 [batch][heads_q][nb][nb] (seer_attn_gt's output; entries
  * j > i are not read).  loss: device fp32 scalar.  q, k, wq, wk as seer_gate.
  * Of gate, only block, gate_dim, w_per_head and rope_theta are used.
- * workspace: device memory of at least seer_gate_distill_workspace_bytes
- * bytes, 256-byte aligned.  No atomics: results are identical run to run.
+ * workspace: device memory of at least seer_gate_distill_workspace_bytes(desc,
+ * gate, opts) bytes, 256-byte aligned (opts may be NULL).  No atomics: results
+ * are identical run to run.
  * Errors: as seer_gate; SEER_ERR_INVALID_ARG for a NULL gt, loss, dwq or dwk.
  */
 seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* gate,
                               const void* q, const void* k, const float* wq, const float* wk,
                               const float* gt, float* loss, float* dwq, float* dwk,
-                              void* workspace, size_t workspace_bytes, void* stream);
+                              void* workspace, size_t workspace_bytes, const seer_distill_opts* opts,
+                              void* stream);
 
 /*
  * Packed variable-length batches (the prefill layout of a serving batch):

@@ -43,6 +43,28 @@ class GateDesc(C.Structure):
                 ("kv_shared", C.c_int32)]
 
 
+class AttnOpts(C.Structure):
+    """seer_attn_opts: launch options of the attention calls (zero fields: defaults)."""
+    _fields_ = [("split", C.c_int32), ("split_width", C.c_int32), ("heads_per_wg", C.c_int32),
+                ("batch_min_blocks", C.c_int32), ("batch_wgs", C.c_int32)]
+
+
+class DistillOpts(C.Structure):
+    """seer_distill_opts (zero fields: defaults)."""
+    _fields_ = [("gemm_min_chunks", C.c_int32)]
+
+
+def _opts_ref(opts, cls):
+    """None, a dict of fields, or a ctypes options struct -> pointer argument."""
+    if opts is None:
+        return None
+    if isinstance(opts, dict):
+        opts = cls(**opts)
+    if not isinstance(opts, cls):
+        raise TypeError(f"options must be a dict or {cls.__name__}")
+    return C.byref(opts)
+
+
 class BlockMaskStruct(C.Structure):
     _fields_ = [("n_blocks", C.c_int32), ("count", C.c_void_p), ("idx", C.c_void_p),
                 ("dense", C.c_void_p), ("kv_shared", C.c_int32)]
@@ -60,13 +82,14 @@ _SIGS = {
     "seer_dense_attn": ([_P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P], C.c_int),
     "seer_mask_from_dense": ([_P, C.c_int32, _P, _P, _P], C.c_int),
     "seer_attn_gt_workspace_bytes": ([_P, C.c_int32, C.c_int32], C.c_size_t),
-    "seer_gate_distill_workspace_bytes": ([_P, _P], C.c_size_t),
-    "seer_attn_workspace_bytes": ([_P, C.c_int32, C.c_int32], C.c_size_t),
-    "seer_bsattn_ws": ([_P, C.c_int32, _P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, C.c_size_t, _P],
+    "seer_gate_distill_workspace_bytes": ([_P, _P, _P], C.c_size_t),
+    "seer_attn_workspace_bytes": ([_P, C.c_int32, C.c_int32, _P], C.c_size_t),
+    "seer_bsattn_ws": ([_P, C.c_int32, _P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, C.c_size_t, _P, _P],
                        C.c_int),
-    "seer_dense_attn_ws": ([_P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, C.c_size_t, _P], C.c_int),
-    "seer_gate_distill": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P], C.c_int),
-    "seer_attn_gt": ([_P, C.c_int32, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P],
+    "seer_dense_attn_ws": ([_P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, C.c_size_t, _P, _P], C.c_int),
+    "seer_attn_launches": ([_P, C.c_int32, C.c_int32, C.c_int32, _P, C.c_size_t], C.c_int32),
+    "seer_gate_distill": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P, _P], C.c_int),
+    "seer_attn_gt": ([_P, C.c_int32, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P, _P],
                      C.c_int),
     "seer_varlen_mask_elems": ([_P, _P, C.c_int32, C.c_int32, _P], C.c_size_t),
     "seer_gate_varlen_workspace_bytes": ([_P, _P, _P], C.c_size_t),
@@ -261,11 +284,25 @@ def gate(q, k, wq, wk, *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
     return mask
 
 
-def attn_workspace_bytes(q, k, v=None, causal: bool = True) -> int:
+def attn_workspace_bytes(q, k, v=None, causal: bool = True, opts=None) -> int:
     """Workspace that enables the key-range split of bsattn / dense_attn for
-    this shape (0: the shape does not split)."""
+    this shape and options (0: the call does not split)."""
     d = make_desc(q, k, v)
-    return lib().seer_attn_workspace_bytes(C.byref(d), BLOCK, int(bool(causal)))
+    return lib().seer_attn_workspace_bytes(C.byref(d), BLOCK, int(bool(causal)), _opts_ref(opts, AttnOpts))
+
+
+def attn_launches(q, k, v=None, mask: Optional["BlockMask"] = None, *, causal: bool = True, opts=None,
+                  workspace_bytes: int = 0) -> int:
+    """Attention-kernel launches one bsattn (mask given) or dense_attn call with
+    these arguments makes on the current device (seer_attn_launches)."""
+    d = make_desc(q, k, v)
+    kind = 0 if mask is None else (2 if mask.kv_shared else 1)
+    block = BLOCK if mask is None else mask.block
+    n = lib().seer_attn_launches(C.byref(d), block, kind, int(bool(causal)), _opts_ref(opts, AttnOpts),
+                                 int(workspace_bytes))
+    if n < 0:
+        raise ValueError("seer_attn_launches: invalid arguments")
+    return n
 
 
 def _ws_args(workspace):
@@ -275,9 +312,10 @@ def _ws_args(workspace):
 
 
 def bsattn(q, k, v, mask: BlockMask, *, causal: bool = True, sm_scale: float = 0.0, out=None,
-           lse: Optional[object] = None, want_lse: bool = False, workspace=None, stream=None):
-    """Block-sparse attention (seer_bsattn; seer_bsattn_ws with a workspace,
-    which enables the key-range split).  Returns (O, LSE or None)."""
+           lse: Optional[object] = None, want_lse: bool = False, workspace=None, opts=None, stream=None):
+    """Block-sparse attention (seer_bsattn; seer_bsattn_ws with a workspace or
+    launch options -- a dict of seer_attn_opts fields or an AttnOpts).
+    Returns (O, LSE or None)."""
     torch = _torch()
     if out is None:
         out = torch.empty_like(q)
@@ -286,36 +324,38 @@ def bsattn(q, k, v, mask: BlockMask, *, causal: bool = True, sm_scale: float = 0
     d = make_desc(q, k, v, out)
     ms = mask.struct()
     block = mask.block  # 64- or 128-token mask blocks
-    if workspace is None:
+    if workspace is None and opts is None:
         st = lib().seer_bsattn(C.byref(d), block, C.byref(ms), int(bool(causal)), float(sm_scale),
                                _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
         _check(st, "seer_bsattn")
     else:
         wp, wn = _ws_args(workspace)
         st = lib().seer_bsattn_ws(C.byref(d), block, C.byref(ms), int(bool(causal)), float(sm_scale),
-                                  _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), wp, wn, _stream(stream))
+                                  _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), wp, wn,
+                                  _opts_ref(opts, AttnOpts), _stream(stream))
         _check(st, "seer_bsattn_ws")
     return out, lse
 
 
 def dense_attn(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
-               lse: Optional[object] = None, want_lse: bool = False, workspace=None, stream=None):
+               lse: Optional[object] = None, want_lse: bool = False, workspace=None, opts=None, stream=None):
     """Dense attention over every (causal) block (seer_dense_attn; seer_dense_attn_ws
-    with a workspace).  Returns (O, LSE or None)."""
+    with a workspace or launch options).  Returns (O, LSE or None)."""
     torch = _torch()
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:
         lse = torch.empty(q.shape[:3], dtype=torch.float32, device=q.device)
     d = make_desc(q, k, v, out)
-    if workspace is None:
+    if workspace is None and opts is None:
         st = lib().seer_dense_attn(C.byref(d), int(bool(causal)), float(sm_scale), _ptr(q), _ptr(k),
                                    _ptr(v), _ptr(out), _ptr(lse), _stream(stream))
         _check(st, "seer_dense_attn")
     else:
         wp, wn = _ws_args(workspace)
         st = lib().seer_dense_attn_ws(C.byref(d), int(bool(causal)), float(sm_scale), _ptr(q), _ptr(k),
-                                      _ptr(v), _ptr(out), _ptr(lse), wp, wn, _stream(stream))
+                                      _ptr(v), _ptr(out), _ptr(lse), wp, wn, _opts_ref(opts, AttnOpts),
+                                      _stream(stream))
         _check(st, "seer_dense_attn_ws")
     return out, lse
 
@@ -328,7 +368,7 @@ def attn_gt_workspace_bytes(q, k, v=None, kv_groups: int = 0) -> int:
 
 def attn_gt(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
             lse: Optional[object] = None, want_lse: bool = False, gt=None, workspace=None,
-            kv_groups: int = 0, stream=None):
+            kv_groups: int = 0, opts=None, stream=None):
     """Dense attention plus the 2D max-pooled attention map (seer_attn_gt).
     Returns (O, LSE or None, gt [B, Hq, nb, nb] fp32).  Without a workspace,
     one sized for `kv_groups` KV groups per launch (0: all) is allocated."""
@@ -347,20 +387,22 @@ def attn_gt(q, k, v, *, causal: bool = True, sm_scale: float = 0.0, out=None,
         workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=q.device)
     st = lib().seer_attn_gt(C.byref(d), BLOCK, int(bool(causal)), float(sm_scale), _ptr(q), _ptr(k),
                             _ptr(v), _ptr(out), _ptr(lse), _ptr(gt), _ptr(workspace),
-                            workspace.numel() * workspace.element_size(), _stream(stream))
+                            workspace.numel() * workspace.element_size(), _opts_ref(opts, AttnOpts),
+                            _stream(stream))
     _check(st, "seer_attn_gt")
     return out, lse, gt
 
 
-def gate_distill_workspace_bytes(q, k, wq, wk, *, w_per_head: bool = True, rope_theta: float = 0.0) -> int:
-    """Workspace of gate_distill for these shapes."""
+def gate_distill_workspace_bytes(q, k, wq, wk, *, w_per_head: bool = True, rope_theta: float = 0.0,
+                                 opts=None) -> int:
+    """Workspace of gate_distill for these shapes and options."""
     d = make_desc(q, k)
     gd = gate_desc(wq.shape[-1], TOPK_RATIO, topk_ratio=1.0, w_per_head=w_per_head, rope_theta=rope_theta)
-    return lib().seer_gate_distill_workspace_bytes(C.byref(d), C.byref(gd))
+    return lib().seer_gate_distill_workspace_bytes(C.byref(d), C.byref(gd), _opts_ref(opts, DistillOpts))
 
 
 def gate_distill(q, k, wq, wk, gt, *, w_per_head: bool = True, rope_theta: float = 0.0,
-                 dwq=None, dwk=None, loss=None, workspace=None, stream=None):
+                 dwq=None, dwk=None, loss=None, workspace=None, opts=None, stream=None):
     """One gate distillation step (seer_gate_distill): returns (loss [1], dwq, dwk)
     as device fp32 tensors; loss is the mean KL(renormalised gt || gate softmax)."""
     torch = _torch()
@@ -374,11 +416,12 @@ def gate_distill(q, k, wq, wk, gt, *, w_per_head: bool = True, rope_theta: float
     if loss is None:
         loss = torch.empty(1, dtype=torch.float32, device=q.device)
     if workspace is None:
-        n = lib().seer_gate_distill_workspace_bytes(C.byref(d), C.byref(gd))
+        n = lib().seer_gate_distill_workspace_bytes(C.byref(d), C.byref(gd), _opts_ref(opts, DistillOpts))
         workspace = torch.empty(max(n, 1), dtype=torch.uint8, device=q.device)
     st = lib().seer_gate_distill(C.byref(d), C.byref(gd), _ptr(q), _ptr(k), _ptr(wq), _ptr(wk),
                                  _ptr(gt), _ptr(loss), _ptr(dwq), _ptr(dwk), _ptr(workspace),
-                                 workspace.numel() * workspace.element_size(), _stream(stream))
+                                 workspace.numel() * workspace.element_size(), _opts_ref(opts, DistillOpts),
+                                 _stream(stream))
     _check(st, "seer_gate_distill")
     return loss, dwq, dwk
 

@@ -331,17 +331,12 @@ hipError_t launch_kl_rows(const KlArgs& a, hipStream_t s) {
 }
 
 // Parts per output tile: enough workgroups to fill the chip (about 2048) when
-// the tiles alone are fewer, but at least 8 chunks of K per part on the
-// longest tile.  The environment variable SEER_GEMM_MIN_CHUNKS (read on the
-// host at each call and at each workspace query) overrides the 8, so that
-// tests can split small products.
+// the tiles alone are fewer, but at least a.min_chunks chunks of K per part on
+// the longest tile (8 by default; a smaller value lets tests split small
+// products).
 int gemm_splits(const GemmArgs& a) {
   if (a.M <= 0 || a.N <= 0 || a.Z <= 0) return 1;
-  int min_chunks = 8;
-  if (const char* e = getenv("SEER_GEMM_MIN_CHUNKS")) {
-    const int v = atoi(e);
-    if (v >= 1) min_chunks = v;
-  }
+  const int min_chunks = a.min_chunks >= 1 ? a.min_chunks : 8;
   const int64_t tiles = (int64_t)((a.N + kT - 1) / kT) * ((a.M + kT - 1) / kT) * a.Z;
   const int64_t chunks = (int64_t)a.K1 * ((a.K2 + kKc - 1) / kKc);
   int64_t sp = (2048 + tiles - 1) / tiles;

@@ -81,18 +81,22 @@ struct AttnArgs {
   // 2D max-pooled probability map [B][Hq][nb][nb]; both nullptr otherwise
   float* pool_r;
   float* gt;
-  // key-range split (causal, bf16): each row is cut into split_parts key ranges of
-  // split_w blocks, computed as separate tasks into partial slots and merged
-  // afterwards; split_w == 0 disables it
-  int split_parts;              // 8 or 16
+  // key-range split (causal, bf16): each row is cut into ranges of split_w key
+  // blocks, computed as separate tasks into partial slots and merged by each
+  // row's last task; split_w == 0 disables it
+  int split_parts;              // ceil(n_blocks / split_w)
   int split_w;
   int64_t split_slots;          // partial slots per (batch, head)
-  int32_t* split_bounds;        // sparse: [rows][split_parts + 1] list offsets of the ranges
+  int32_t* split_bounds;        // [rows][split_parts + 3]: range list offsets, non-empty
+                                // range count, arrival counter (split_bounds_kernel)
+  int32_t* split_tickets;       // [8] task-queue tickets (zeroed by split_bounds_kernel)
+  // launch options (seer_attn_opts with its defaults resolved)
+  int heads_per_wg;             // cap on query heads per workgroup for shared rows (1, 2, 4)
+  int batch_min_blocks;         // batched launches of sparse rows from this many blocks (0: never)
+  int batch_wgs;                // workgroups per batch (0: the resident capacity)
   float* part_lse;              // [slots][64] log2-domain log-sum-exp of each partial
   uint16_t* part_o;             // [slots][64][D] bf16 partial outputs, normalised
 };
-
-constexpr int kMaxSplitParts = 16;
 
 // Gate distillation (Eq. 2): row-wise KL between the renormalised ground truth
 // and the gate softmax, and the logit gradient written over the logits.
@@ -126,6 +130,7 @@ struct GemmArgs {
   int64_t scm, scz;
   float alpha;
   float* part;
+  int min_chunks;  // K chunks per part at least (seer_distill_opts.gemm_min_chunks; 8 by default)
 };
 int gemm_splits(const GemmArgs& a);
 int64_t gemm_partial_elems(const GemmArgs& a);
@@ -144,10 +149,12 @@ hipError_t launch_rope_inverse(const RopeArgs& a, hipStream_t s);
 hipError_t launch_gate_logits(const GateLogitsArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
 hipError_t launch_mask_from_dense(const MaskFromDenseArgs& a, hipStream_t s);
-hipError_t launch_attn(const AttnArgs& a, hipStream_t s);
-// Split geometry: the number of key ranges for a launch (0 when the shape does
-// not split) and the partial slots per (batch, head) for a range width.
-int split_parts(int n_blocks, int kv_groups, bool causal, bool bf16, bool sparse);
+// With a non-null `count` nothing is launched: the attention-kernel launches
+// the call would make are counted into *count.
+hipError_t launch_attn(const AttnArgs& a, hipStream_t s, int* count = nullptr);
+// Split geometry: the key-range width in blocks for a launch (0 when the shape
+// does not split) and the partial slots per (batch, head) for a range width.
+int split_width(int n_blocks, int head_dim, bool causal, bool bf16, bool want, int width);
 int64_t split_slots_per_head(int n_blocks, int w);
 
 }  // namespace seer

@@ -108,9 +108,9 @@ struct DistillGemms {
   seer::GemmArgs dqg, dkg, dwq, dwk;
 };
 
-DistillGemms distill_gemms(int B, int Hq, int Hkv, int D, int Dg, int nb, bool ph, const float* dl,
-                           const float* qg, const float* kg, const float* qp, const float* kp, float* dqg,
-                           float* dkg, float* dwq, float* dwk, float* part) {
+DistillGemms distill_gemms(int B, int Hq, int Hkv, int D, int Dg, int nb, bool ph, int min_chunks,
+                           const float* dl, const float* qg, const float* kg, const float* qp, const float* kp,
+                           float* dqg, float* dkg, float* dwq, float* dwk, float* part) {
   const int G = Hq / Hkv;
   const int64_t nn = (int64_t)nb * nb;
   const float rsqrt_dg = (float)(1.0 / std::sqrt((double)Dg));
@@ -172,6 +172,7 @@ DistillGemms distill_gemms(int B, int Hq, int Hkv, int D, int Dg, int nb, bool p
     g.sbz = 0; g.sbk1 = (int64_t)nb * Dg;
   }
   r.dwk = g;
+  for (seer::GemmArgs* x : {&r.dqg, &r.dkg, &r.dwq, &r.dwk}) x->min_chunks = min_chunks;
   return r;
 }
 
@@ -182,7 +183,7 @@ struct DistillLayout {
   size_t qg, kg, qp, kp, logits, dqg, dkg, row_loss, part, total;
 };
 
-DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g) {
+DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g, int min_chunks) {
   const size_t nb = (size_t)blocks_of(d->seq_len, g->block);
   const size_t B = d->batch, Hq = d->heads_q, Hkv = d->heads_kv, D = d->head_dim, Dg = g->gate_dim;
   DistillLayout L;
@@ -201,8 +202,8 @@ DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g) {
   L.dkg = take(B * Hkv * nb * Dg * 4);
   L.row_loss = take((B * Hq * nb + seer::kLossParts) * 8);
   const DistillGemms gm = distill_gemms((int)B, (int)Hq, (int)Hkv, (int)D, (int)Dg, (int)nb, g->w_per_head != 0,
-                                        nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                        nullptr, nullptr);
+                                        min_chunks, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                        nullptr, nullptr, nullptr);
   int64_t part = 0;
   for (const seer::GemmArgs* a : {&gm.dqg, &gm.dkg, &gm.dwq, &gm.dwk})
     part = std::max(part, seer::gemm_partial_elems(*a));
@@ -254,37 +255,61 @@ seer::AttnArgs attn_args(const seer_attn_desc* desc, int32_t causal, float sm_sc
   a.split_w = 0;
   a.split_slots = 0;
   a.split_bounds = nullptr;
+  a.split_tickets = nullptr;
+  a.heads_per_wg = 2;
+  a.batch_min_blocks = 2048;
+  a.batch_wgs = 0;
   a.part_lse = nullptr;
   a.part_o = nullptr;
   return a;
 }
 
-// Workspace of the key-range split: list bounds [rows][P + 1] int32, then the
-// partial log-sum-exps [slots][64] fp32 and outputs [slots][64][D] bf16.
+// Workspace of the key-range split: per-row records [rows][P + 3] int32 (range
+// list offsets, non-empty range count, arrival counter), the task-queue tickets
+// [8] int32, then the partial log-sum-exps [slots][64] fp32 and outputs
+// [slots][64][D] bf16.
 struct SplitLayout {
   int parts, w;
   int64_t slots;  // per (batch, head)
-  size_t bounds, lse, o, total;
+  size_t bounds, tickets, lse, o, total;
 };
 
-SplitLayout split_layout(const seer_attn_desc* d, int parts) {
+SplitLayout split_layout(const seer_attn_desc* d, int w) {
   SplitLayout L{};
   const int nb = blocks_of(d->seq_len, SEER_BLOCK);
-  if (parts == 0) return L;
-  L.parts = parts;
-  L.w = nb / parts;
+  if (w <= 0) return L;
+  L.w = w;
+  L.parts = (nb + w - 1) / w;
   L.slots = seer::split_slots_per_head(nb, L.w);
   const size_t bh = (size_t)d->batch * d->heads_q;
   L.bounds = 0;
-  L.lse = round_up(bh * nb * (parts + 1) * sizeof(int32_t));
+  L.tickets = round_up(bh * nb * (L.parts + 3) * sizeof(int32_t));
+  L.lse = L.tickets + round_up(8 * sizeof(int32_t));
   L.o = L.lse + round_up(bh * L.slots * 64 * sizeof(float));
   L.total = L.o + round_up(bh * L.slots * 64 * d->head_dim * sizeof(uint16_t));
   return L;
 }
 
-int split_parts_for(const seer_attn_desc* d, int32_t causal, bool sparse) {
-  return seer::split_parts(blocks_of(d->seq_len, SEER_BLOCK), d->batch * d->heads_kv, causal != 0,
-                           d->dtype == SEER_BF16, sparse);
+int split_width_for(const seer_attn_desc* d, int32_t causal, const seer_attn_opts* o) {
+  return seer::split_width(blocks_of(d->seq_len, SEER_BLOCK), d->head_dim, causal != 0, d->dtype == SEER_BF16,
+                           o && o->split == 1, o ? o->split_width : 0);
+}
+
+// The launch options with their defaults resolved (NULL or zero fields: defaults).
+void apply_opts(seer::AttnArgs& a, const seer_attn_opts* o) {
+  if (!o) return;
+  if (o->heads_per_wg > 0) a.heads_per_wg = o->heads_per_wg;
+  if (o->batch_min_blocks < 0) a.batch_min_blocks = 0;
+  else if (o->batch_min_blocks > 0) a.batch_min_blocks = o->batch_min_blocks;
+  if (o->batch_wgs > 0) a.batch_wgs = o->batch_wgs;
+}
+
+seer_status check_opts(const seer_attn_opts* o) {
+  if (!o) return SEER_OK;
+  if ((o->split != 0 && o->split != 1) || (o->heads_per_wg > 0 && o->heads_per_wg != 1 && o->heads_per_wg != 2 &&
+                                           o->heads_per_wg != 4))
+    return SEER_ERR_INVALID_ARG;
+  return SEER_OK;
 }
 
 // Bytes of row-max workspace per query head: nb key tiles x 64 queries per query block.
@@ -403,9 +428,11 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
 static seer_status attn_common(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
                                int32_t causal, float sm_scale, const void* q, const void* k,
                                const void* v, void* o, float* lse, void* workspace,
-                               size_t workspace_bytes, void* stream) {
+                               size_t workspace_bytes, const seer_attn_opts* opts, void* stream,
+                               int* count = nullptr) {
   seer_status s = check_attn(desc, sm_scale, q, k, v, o);
   if (s != SEER_OK) return s;
+  if ((s = check_opts(opts)) != SEER_OK) return s;
   if (mask) {
     if (block != 64 && block != 128) return SEER_ERR_UNSUPPORTED;
     const int nbm = blocks_of(desc->seq_len, block);
@@ -419,55 +446,78 @@ static seer_status attn_common(const seer_attn_desc* desc, int32_t block, const 
   a.mask_shift = (mask && block == 128) ? 1 : 0;
   a.mask_blocks = mask ? mask->n_blocks : 0;
   a.mask_kv = mask && mask->kv_shared;
+  apply_opts(a, opts);
   if (workspace && a.mask_shift == 0 && !a.mask_kv) {  // the split runs on per-head 64-token masks
     if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
-    const SplitLayout L = split_layout(desc, split_parts_for(desc, causal, mask != nullptr));
+    const SplitLayout L = split_layout(desc, split_width_for(desc, causal, opts));
     if (L.w > 0 && workspace_bytes >= L.total) {  // key-range split
       char* ws = static_cast<char*>(workspace);
       a.split_parts = L.parts;
       a.split_w = L.w;
       a.split_slots = L.slots;
       a.split_bounds = reinterpret_cast<int32_t*>(ws + L.bounds);
+      a.split_tickets = reinterpret_cast<int32_t*>(ws + L.tickets);
       a.part_lse = reinterpret_cast<float*>(ws + L.lse);
       a.part_o = reinterpret_cast<uint16_t*>(ws + L.o);
     }
   }
-  return from_hip(seer::launch_attn(a, static_cast<hipStream_t>(stream)));
+  return from_hip(seer::launch_attn(a, static_cast<hipStream_t>(stream), count));
 }
 
 seer_status seer_bsattn(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
                         int32_t causal, float sm_scale, const void* q, const void* k,
                         const void* v, void* o, float* lse, void* stream) {
   if (!mask || !desc) return SEER_ERR_INVALID_ARG;
-  return attn_common(desc, block, mask, causal, sm_scale, q, k, v, o, lse, nullptr, 0, stream);
+  return attn_common(desc, block, mask, causal, sm_scale, q, k, v, o, lse, nullptr, 0, nullptr, stream);
 }
 
 seer_status seer_dense_attn(const seer_attn_desc* desc, int32_t causal, float sm_scale,
                             const void* q, const void* k, const void* v, void* o, float* lse,
                             void* stream) {
-  return attn_common(desc, SEER_BLOCK, nullptr, causal, sm_scale, q, k, v, o, lse, nullptr, 0, stream);
+  return attn_common(desc, SEER_BLOCK, nullptr, causal, sm_scale, q, k, v, o, lse, nullptr, 0, nullptr, stream);
 }
 
-size_t seer_attn_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t causal) {
-  if (block != SEER_BLOCK || check_desc(desc, 0xF) != SEER_OK) return 0;
-  // enough for the sparse and the dense choice of ranges
-  return std::max(split_layout(desc, split_parts_for(desc, causal, true)).total,
-                  split_layout(desc, split_parts_for(desc, causal, false)).total);
+size_t seer_attn_workspace_bytes(const seer_attn_desc* desc, int32_t block, int32_t causal,
+                                 const seer_attn_opts* opts) {
+  if (block != SEER_BLOCK || check_desc(desc, 0xF) != SEER_OK || check_opts(opts) != SEER_OK) return 0;
+  return split_layout(desc, split_width_for(desc, causal, opts)).total;
 }
 
 seer_status seer_bsattn_ws(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,
                            int32_t causal, float sm_scale, const void* q, const void* k, const void* v,
-                           void* o, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+                           void* o, float* lse, void* workspace, size_t workspace_bytes,
+                           const seer_attn_opts* opts, void* stream) {
   if (!mask || !desc) return SEER_ERR_INVALID_ARG;
-  return attn_common(desc, block, mask, causal, sm_scale, q, k, v, o, lse, workspace, workspace_bytes,
+  return attn_common(desc, block, mask, causal, sm_scale, q, k, v, o, lse, workspace, workspace_bytes, opts,
                      stream);
 }
 
 seer_status seer_dense_attn_ws(const seer_attn_desc* desc, int32_t causal, float sm_scale,
                                const void* q, const void* k, const void* v, void* o, float* lse,
-                               void* workspace, size_t workspace_bytes, void* stream) {
+                               void* workspace, size_t workspace_bytes, const seer_attn_opts* opts,
+                               void* stream) {
   return attn_common(desc, SEER_BLOCK, nullptr, causal, sm_scale, q, k, v, o, lse, workspace,
-                     workspace_bytes, stream);
+                     workspace_bytes, opts, stream);
+}
+
+int32_t seer_attn_launches(const seer_attn_desc* desc, int32_t block, int32_t mask_kind, int32_t causal,
+                           const seer_attn_opts* opts, size_t workspace_bytes) {
+  if (!desc || mask_kind < 0 || mask_kind > 2) return -1;
+  // stand-in pointers: nothing is dereferenced or launched when counting
+  char* fake = reinterpret_cast<char*>(kAlign);
+  seer_block_mask m{};
+  if (mask_kind > 0) {
+    if (block != 64 && block != 128) return -1;
+    m.n_blocks = blocks_of(desc->seq_len, block);
+    m.count = reinterpret_cast<int32_t*>(fake);
+    m.idx = reinterpret_cast<uint16_t*>(fake);
+    m.kv_shared = mask_kind == 2;
+  }
+  int count = 0;
+  const seer_status s = attn_common(desc, mask_kind > 0 ? block : SEER_BLOCK, mask_kind > 0 ? &m : nullptr, causal,
+                                    0.f, fake, fake, fake, fake, nullptr, workspace_bytes ? fake : nullptr,
+                                    workspace_bytes, opts, nullptr, &count);
+  return s == SEER_OK ? count : -1;
 }
 
 seer_status seer_mask_from_dense(const seer_attn_desc* desc, int32_t block, const uint8_t* dense,
@@ -499,10 +549,12 @@ size_t seer_attn_gt_workspace_bytes(const seer_attn_desc* desc, int32_t block, i
 
 seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t causal, float sm_scale,
                          const void* q, const void* k, const void* v, void* o, float* lse,
-                         float* gt, void* workspace, size_t workspace_bytes, void* stream) {
+                         float* gt, void* workspace, size_t workspace_bytes, const seer_attn_opts* opts,
+                         void* stream) {
   if (block != SEER_BLOCK) return desc ? SEER_ERR_UNSUPPORTED : SEER_ERR_INVALID_ARG;
   seer_status s = check_attn(desc, sm_scale, q, k, v, o);
   if (s != SEER_OK) return s;
+  if ((s = check_opts(opts)) != SEER_OK) return s;
   if (!gt) return SEER_ERR_INVALID_ARG;
   const int G = desc->heads_q / desc->heads_kv;
   const size_t group_bytes = (size_t)G * gt_head_bytes(desc);
@@ -512,6 +564,7 @@ seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t caus
   const int64_t nb = blocks_of(desc->seq_len, SEER_BLOCK);
   const int64_t all = (int64_t)desc->batch * desc->heads_kv;
   seer::AttnArgs a = attn_args(desc, causal, sm_scale, q, k, v, o, lse);
+  apply_opts(a, opts);
   a.pool_r = static_cast<float*>(workspace);
   if (workspace_bytes / group_bytes >= (size_t)all) {  // every head in one launch
     a.gt = gt;
@@ -540,21 +593,27 @@ seer_status seer_attn_gt(const seer_attn_desc* desc, int32_t block, int32_t caus
   return SEER_OK;
 }
 
-size_t seer_gate_distill_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate) {
+static int distill_min_chunks(const seer_distill_opts* opts) {
+  return (opts && opts->gemm_min_chunks >= 1) ? opts->gemm_min_chunks : 8;
+}
+
+size_t seer_gate_distill_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate,
+                                         const seer_distill_opts* opts) {
   if (check_gate_common(desc, gate) != SEER_OK) return 0;
-  return distill_layout(desc, gate).total;
+  return distill_layout(desc, gate, distill_min_chunks(opts)).total;
 }
 
 seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* gate, const void* q,
                               const void* k, const float* wq, const float* wk, const float* gt,
                               float* loss, float* dwq, float* dwk, void* workspace,
-                              size_t workspace_bytes, void* stream) {
+                              size_t workspace_bytes, const seer_distill_opts* opts, void* stream) {
   seer_status s = check_gate_common(desc, gate);
   if (s != SEER_OK) return s;
   if (gate->kv_shared) return SEER_ERR_UNSUPPORTED;  // the distillation target is per query head
   if (!q || !k || !wq || !wk || !gt || !loss || !dwq || !dwk) return SEER_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
-  const DistillLayout W = distill_layout(desc, gate);
+  const int min_chunks = distill_min_chunks(opts);
+  const DistillLayout W = distill_layout(desc, gate, min_chunks);
   if (!workspace || workspace_bytes < W.total) return SEER_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
 
@@ -621,8 +680,8 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   ka.loss = loss;
   if ((s = from_hip(seer::launch_kl_rows(ka, st))) != SEER_OK) return s;
 
-  const DistillGemms gm = distill_gemms(B, Hq, Hkv, D, Dg, nb, gate->w_per_head != 0, dl, qg, kg, qp, kp, dqg,
-                                        dkg, dwq, dwk, reinterpret_cast<float*>(ws + W.part));
+  const DistillGemms gm = distill_gemms(B, Hq, Hkv, D, Dg, nb, gate->w_per_head != 0, min_chunks, dl, qg, kg, qp,
+                                        kp, dqg, dkg, dwq, dwk, reinterpret_cast<float*>(ws + W.part));
   if ((s = from_hip(seer::launch_gemm_f32(gm.dqg, st))) != SEER_OK) return s;
   if ((s = from_hip(seer::launch_gemm_f32(gm.dkg, st))) != SEER_OK) return s;
   if (rope_base > 0.0) {  // back through the block-level RoPE
@@ -781,7 +840,7 @@ seer_status seer_bsattn_varlen(const seer_attn_desc* desc, const int32_t* cu_seq
                     at_token(k, desc->k_stride, cu_seqlens_host[b], es),
                     at_token(v, desc->v_stride, cu_seqlens_host[b], es),
                     const_cast<void*>(at_token(o, desc->o_stride, cu_seqlens_host[b], es)), lb, nullptr, 0,
-                    stream);
+                    nullptr, stream);
     if (s != SEER_OK) return s;
   }
   return SEER_OK;

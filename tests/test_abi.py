@@ -24,7 +24,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 19, names
+    assert len(names) == 20, names
     L = C.CDLL(seer.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert seer.abi_version() == 2
+    assert seer.abi_version() == 3
     assert seer.status_str(0) == "SEER_OK"
     assert seer.status_str(3) == "SEER_ERR_WORKSPACE"
     assert seer.status_str(99) == "SEER_ERR_UNKNOWN"
@@ -160,14 +160,14 @@ def test_attn_gt_workspace_and_rejects_bad_args():
     assert L.seer_attn_gt_workspace_bytes(C.byref(d), 64, 9) == 2 * 4 * per_head
     assert L.seer_attn_gt_workspace_bytes(C.byref(d), 128, 0) == 0
     args = (FAKE, FAKE, FAKE, FAKE, None)
-    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, None, FAKE * 16, 1 << 40, None) == \
+    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, None, FAKE * 16, 1 << 40, None, None) == \
         seer.ERR_INVALID_ARG                                                  # no gt
-    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, FAKE, FAKE * 16, 2 * per_head - 1, None) == \
+    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, FAKE, FAKE * 16, 2 * per_head - 1, None, None) == \
         seer.ERR_WORKSPACE
-    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, FAKE, None, 1 << 40, None) == seer.ERR_WORKSPACE
-    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, FAKE, FAKE * 16 + 16, 1 << 40, None) == \
+    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, FAKE, None, 1 << 40, None, None) == seer.ERR_WORKSPACE
+    assert L.seer_attn_gt(C.byref(d), 64, 1, 0.0, *args, FAKE, FAKE * 16 + 16, 1 << 40, None, None) == \
         seer.ERR_INVALID_ARG                                                  # misaligned workspace
-    assert L.seer_attn_gt(C.byref(d), 128, 1, 0.0, *args, FAKE, FAKE * 16, 1 << 40, None) == \
+    assert L.seer_attn_gt(C.byref(d), 128, 1, 0.0, *args, FAKE, FAKE * 16, 1 << 40, None, None) == \
         seer.ERR_UNSUPPORTED
 
 
@@ -178,12 +178,12 @@ def test_gate_distill_workspace_and_rejects_bad_args():
     # Qg, Kg, Qp, Kp, logits, dQg, dKg, row losses + 64 partial sums; no product splits at this size
     want = (up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up(4 * nb * 128 * 4) + up(2 * nb * 384 * 4)
             + up(4 * nb * nb * 4) + up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up((4 * nb + 64) * 8))
-    need = L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g))
+    need = L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g), None)
     assert need == want
     g.mode = 9  # the selection mode is not used by the distillation step
-    assert L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g)) == want
+    assert L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g), None) == want
     call = lambda gt=FAKE, ws=FAKE * 16, n=need, gd=g: L.seer_gate_distill(
-        C.byref(d), C.byref(gd), FAKE, FAKE, FAKE, FAKE, gt, FAKE, FAKE, FAKE, ws, n, None)
+        C.byref(d), C.byref(gd), FAKE, FAKE, FAKE, FAKE, gt, FAKE, FAKE, FAKE, ws, n, None, None)
     assert call(gt=None) == seer.ERR_INVALID_ARG
     assert call(n=need - 1) == seer.ERR_WORKSPACE
     assert call(ws=None) == seer.ERR_WORKSPACE
@@ -202,13 +202,11 @@ def _gemm_splits(M, N, K1, K2, Z, min_chunks=8):
 
 
 @pytest.mark.parametrize("min_chunks", [None, 1])
-def test_gate_distill_workspace_split_products(min_chunks, monkeypatch):
+def test_gate_distill_workspace_split_products(min_chunks):
     """At 32k tokens (32 q / 8 kv heads) the backward products split their K
-    range; the workspace holds the largest product's parts."""
-    if min_chunks is None:
-        monkeypatch.delenv("SEER_GEMM_MIN_CHUNKS", raising=False)
-    else:
-        monkeypatch.setenv("SEER_GEMM_MIN_CHUNKS", str(min_chunks))
+    range; the workspace holds the largest product's parts (gemm_min_chunks
+    option: at least that many K chunks per part)."""
+    opts = None if min_chunks is None else C.byref(seer.DistillOpts(gemm_min_chunks=min_chunks))
     mc = min_chunks or 8
     L = seer.lib()
     B, Hq, Hkv, D, Dg, nb = 1, 32, 8, 128, 128, 512
@@ -223,33 +221,46 @@ def test_gate_distill_workspace_split_products(min_chunks, monkeypatch):
         if sp > 1:
             part = max(part, Z * sp * M * N)
     assert part > 0
-    assert L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g)) == base + up(4 * part)
+    assert L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g), opts) == base + up(4 * part)
 
 
-def test_attn_workspace_bytes_formula(monkeypatch):
+def test_attn_workspace_bytes_formula():
     L = seer.lib()
-    monkeypatch.delenv("SEER_SPLIT_MIN_WIDTH", raising=False)
-    monkeypatch.delenv("SEER_SPLIT_SPARSE", raising=False)
-    monkeypatch.delenv("SEER_SPLIT_DENSE", raising=False)
     up = lambda x: (x + 255) // 256 * 256
+    opt = lambda **kw: C.byref(seer.AttnOpts(**kw))
+
+    def want(Hq, nb, w, D):
+        P = -(-nb // w)
+        slots = sum(i // w + 1 for i in range(nb))
+        return up(Hq * nb * (P + 3) * 4) + up(8 * 4) + up(Hq * slots * 64 * 4) + up(Hq * slots * 64 * D * 2)
+
     d = _desc(B=1, Hq=32, Hkv=8, S=131072, D=128)
-    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == 0      # the split is opt-in
-    monkeypatch.setenv("SEER_SPLIT_DENSE", "1")
-    nb, w = 2048, 128
-    slots = sum(i // w + 1 for i in range(nb))
-    want = up(32 * nb * 17 * 4) + up(32 * slots * 64 * 4) + up(32 * slots * 64 * 128 * 2)
-    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == want
-    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 0) == 0      # non-causal: no split
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, None) == 0            # the split is opt-in
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, opt()) == 0
+    # ranges sized to the L2: 128 blocks (4 MiB of K and V) at head_dim 128
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, opt(split=1)) == want(32, 2048, 128, 128)
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 0, opt(split=1)) == 0    # non-causal: no split
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, opt(split=1, split_width=300)) == \
+        want(32, 2048, 300, 128)                                                # a partial last range
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, opt(split=2)) == 0     # invalid option
     d.dtype = 1
-    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == 0      # fp32: no split
-    d = _desc(B=1, Hq=4, Hkv=2, S=1024, D=128)                       # nb / 16 = 1 < 32
-    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == 0
-    monkeypatch.setenv("SEER_SPLIT_MIN_WIDTH", "1")
-    slots = sum(i + 1 for i in range(16))
-    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == \
-        up(4 * 16 * 17 * 4) + up(4 * slots * 64 * 4) + up(4 * slots * 64 * 128 * 2)
-    d = _desc(B=1, Hq=4, Hkv=2, S=1088, D=128)                       # nb = 17: not a multiple of 16
-    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1) == 0
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, opt(split=1)) == 0    # fp32: no split
+    d = _desc(B=1, Hq=4, Hkv=2, S=8192, D=64)                                  # nb 128 <= 256 at D 64
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, opt(split=1)) == 0
+    assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, opt(split=1, split_width=5)) == want(4, 128, 5, 64)
+
+
+def test_attn_launches_rejects_bad_args():
+    """The launch-count query validates like the calls it mirrors (it needs a GPU
+    only for the occupancy of the batched launches, so its counts are checked in
+    the GPU tests)."""
+    L = seer.lib()
+    d = _desc()
+    assert L.seer_attn_launches(None, 64, 1, 1, None, 0) == -1
+    assert L.seer_attn_launches(C.byref(d), 64, 3, 1, None, 0) == -1      # mask kind 0, 1 or 2
+    assert L.seer_attn_launches(C.byref(d), 96, 1, 1, None, 0) == -1      # 64- or 128-token blocks
+    bad = seer.AttnOpts(split=5)
+    assert L.seer_attn_launches(C.byref(d), 64, 1, 1, C.byref(bad), 0) == -1
 
 
 def test_attention_ws_rejects_bad_args():
@@ -258,10 +269,14 @@ def test_attention_ws_rejects_bad_args():
     m = seer.BlockMaskStruct()
     m.n_blocks, m.count, m.idx, m.dense = 16, FAKE, FAKE, None
     args = (FAKE, FAKE, FAKE, FAKE, None)
-    assert L.seer_bsattn_ws(C.byref(d), 64, None, 1, 0.0, *args, FAKE * 16, 1 << 30, None) == seer.ERR_INVALID_ARG
-    assert L.seer_bsattn_ws(C.byref(d), 64, C.byref(m), 1, 0.0, *args, FAKE * 16 + 8, 1 << 30, None) == \
+    assert L.seer_bsattn_ws(C.byref(d), 64, None, 1, 0.0, *args, FAKE * 16, 1 << 30, None, None) == \
+        seer.ERR_INVALID_ARG
+    bad = seer.AttnOpts(heads_per_wg=3)
+    assert L.seer_bsattn_ws(C.byref(d), 64, C.byref(m), 1, 0.0, *args, None, 0, C.byref(bad), None) == \
+        seer.ERR_INVALID_ARG
+    assert L.seer_bsattn_ws(C.byref(d), 64, C.byref(m), 1, 0.0, *args, FAKE * 16 + 8, 1 << 30, None, None) == \
         seer.ERR_INVALID_ARG                                               # misaligned workspace
-    assert L.seer_dense_attn_ws(C.byref(d), 1, float("inf"), *args, FAKE * 16, 1 << 30, None) == \
+    assert L.seer_dense_attn_ws(C.byref(d), 1, float("inf"), *args, FAKE * 16, 1 << 30, None, None) == \
         seer.ERR_INVALID_ARG
 
 
@@ -311,7 +326,7 @@ def test_kv_shared_flags_are_validated():
     assert L.seer_mask_from_dense(C.byref(d), 64, FAKE, C.byref(m), None) == seer.ERR_INVALID_ARG
     gt = _gate(kv_shared=1)
     assert L.seer_gate_distill(C.byref(d), C.byref(gt), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                               FAKE * 16, 1 << 40, None) == seer.ERR_UNSUPPORTED
+                               FAKE * 16, 1 << 40, None, None) == seer.ERR_UNSUPPORTED
 
 
 def test_varlen_rejects_bad_offsets_and_sizes_the_mask():

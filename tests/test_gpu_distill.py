@@ -55,11 +55,10 @@ def _weights(B, Hq, Hkv, D, Dg, per_head, seed):
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
 @pytest.mark.parametrize("min_chunks", [None, 1], ids=["default", "split"])
-def test_gate_distill_parity(case, min_chunks, monkeypatch):
+def test_gate_distill_parity(case, min_chunks):
     """`split`: every backward product cut into as many K parts as it has
     K chunks (empty parts included), summed by the reduction kernel."""
-    if min_chunks is not None:
-        monkeypatch.setenv("SEER_GEMM_MIN_CHUNKS", str(min_chunks))
+    opts = None if min_chunks is None else {"gemm_min_chunks": min_chunks}
     B, Hq, Hkv, S, D, dt, Dg, per_head, theta = case
     seed = stable_seed(case, "distill")
     _, q, k, _, _, _ = small_inputs(B, Hq, Hkv, S, D, dt, seed=seed, spikes=True)
@@ -69,7 +68,8 @@ def test_gate_distill_parity(case, min_chunks, monkeypatch):
     print(f"[distill] case {case}", flush=True)
     qd, kd = to_device(q), to_device(k)
     loss, dwq, dwk = seer.gate_distill(qd, kd, torch.from_numpy(wq).cuda(), torch.from_numpy(wk).cuda(),
-                                       torch.from_numpy(gt).cuda(), w_per_head=per_head, rope_theta=theta)
+                                       torch.from_numpy(gt).cuda(), w_per_head=per_head, rope_theta=theta,
+                                       opts=opts)
     torch.cuda.synchronize()
     l_ref, dwq_ref, dwk_ref = oracle.distill(q, k, wq, wk, gt, w_per_head=per_head, rope_theta=theta)
     l_gpu = float(loss.item())

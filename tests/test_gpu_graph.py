@@ -45,12 +45,10 @@ def _valid_idx(count, idx):
 
 
 @pytest.mark.parametrize("batched", [False, True], ids=["one_launch", "batched_launches"])
-def test_gate_sparse_and_dense_attention_replay(batched, monkeypatch):
-    monkeypatch.setenv("SEER_SPLIT_MIN_WIDTH", "1")  # the dense call splits its rows at this size
-    monkeypatch.setenv("SEER_SPLIT_DENSE", "1")
-    if batched:  # the sparse call launches its rows in batches of 64 workgroups
-        monkeypatch.setenv("SEER_EPOCH_MIN_BLOCKS", "1")
-        monkeypatch.setenv("SEER_EPOCH_WGS", "64")
+def test_gate_sparse_and_dense_attention_replay(batched):
+    split = {"split": 1, "split_width": 4}  # the dense call splits its rows into ranges of 4 blocks
+    # batched: the sparse call launches its rows in batches of 64 workgroups
+    sparse_opts = {"batch_min_blocks": 1, "batch_wgs": 64} if batched else {"batch_min_blocks": -1}
     B, Hq, Hkv, S, D = 1, 8, 2, 4096, 128
     host = [small_inputs(B, Hq, Hkv, S, D, "bf16", seed=stable_seed("graph", r), spikes=True)
             for r in range(REPLAYS)]
@@ -62,13 +60,13 @@ def test_gate_sparse_and_dense_attention_replay(batched, monkeypatch):
     l_s = torch.empty((B, Hq, S), dtype=torch.float32, device="cuda")
     l_d, l_u = torch.empty_like(l_s), torch.empty_like(l_s)
     gws = torch.empty(seer.gate_workspace_bytes(qd, kd, wq.shape[-1]), dtype=torch.uint8, device="cuda")
-    aws = torch.empty(max(seer.attn_workspace_bytes(qd, kd, vd), 1), dtype=torch.uint8, device="cuda")
+    aws = torch.empty(max(seer.attn_workspace_bytes(qd, kd, vd, opts=split), 1), dtype=torch.uint8, device="cuda")
     assert aws.numel() > 1, "the dense call should take the key-range split here"
 
     def step():
         seer.gate(qd, kd, wqd, wkd, mode=seer.TOPK_RATIO, topk_ratio=0.2, mask=mask, workspace=gws)
-        seer.bsattn(qd, kd, vd, mask, out=o_s, lse=l_s)
-        seer.dense_attn(qd, kd, vd, out=o_d, lse=l_d, workspace=aws)
+        seer.bsattn(qd, kd, vd, mask, out=o_s, lse=l_s, opts=sparse_opts)
+        seer.dense_attn(qd, kd, vd, out=o_d, lse=l_d, workspace=aws, opts=split)
         seer.dense_attn(qd, kd, vd, out=o_u, lse=l_u)  # unsplit: two query heads per workgroup
 
     g = _capture(step)

@@ -94,17 +94,17 @@ def test_kv_gate_mask_parity(case, sel):
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
 @pytest.mark.parametrize("cap", [4, 2, 1])
-def test_kv_attention_parity(case, cap, monkeypatch):
+def test_kv_attention_parity(case, cap):
     """Attention on the oracle's group mask, with at most `cap` query heads per
     workgroup, against the oracle on the mask repeated per head."""
     B, Hq, Hkv, S, D, dt, Dg = case
     G = Hq // Hkv
     print(f"[kv attn] {case} cap {cap}", flush=True)
-    monkeypatch.setenv("SEER_KV_HEADS_PER_WG", str(cap))
     w, q, k, v, wq, wk = small_inputs(B, Hq, Hkv, S, D, dt, seed=stable_seed("kva", case), Dg=Dg)
     orc = _group_select(q, k, wq, wk, Hkv, oracle.TOPK_RATIO, rho=0.35)
     qd, kd, vd = to_device(q), to_device(k), to_device(v)
-    o, lse = seer.bsattn(qd, kd, vd, _upload_kv(orc["count"], orc["idx"]), want_lse=True)
+    o, lse = seer.bsattn(qd, kd, vd, _upload_kv(orc["count"], orc["idx"]), want_lse=True,
+                         opts={"heads_per_wg": cap})
     torch.cuda.synchronize()
     per_head = np.repeat(orc["mask"], G, axis=1)
     O_ref, lse_ref = oracle.attn(q, k, v, mask=per_head)

@@ -231,7 +231,7 @@ def test_strided_views():
 @pytest.mark.parametrize("case", [(1, 8, 2, 4096, 128, 64), (2, 4, 1, 3000, 64, 64), (1, 4, 4, 2048, 128, 64),
                                   (1, 4, 2, 4096, 128, 128)],
                          ids=lambda c: "x".join(map(str, c)))
-def test_batched_launches_equal_single_launch(case, monkeypatch):
+def test_batched_launches_equal_single_launch(case):
     """Long sparse rows launch in batches of the resident workgroups (task ids
     continue across batches); forced here on small shapes with small batches,
     the outputs must equal the single launch's bit for bit."""
@@ -240,13 +240,12 @@ def test_batched_launches_equal_single_launch(case, monkeypatch):
     qd, kd, vd = (to_device(x) for x in (q, k, v))
     mask = seer.gate(qd, kd, torch.from_numpy(wq).cuda(), torch.from_numpy(wk).cuda(), mode=seer.TOPK_RATIO,
                      topk_ratio=0.3, block=blk)
-    monkeypatch.setenv("SEER_EPOCH_WGS", "0")
-    o1, l1 = seer.bsattn(qd, kd, vd, mask, want_lse=True)
-    monkeypatch.setenv("SEER_EPOCH_MIN_BLOCKS", "1")
+    o1, l1 = seer.bsattn(qd, kd, vd, mask, want_lse=True, opts={"batch_min_blocks": -1})
     outs = []
-    for wgs in ("64", "24", "8"):
-        monkeypatch.setenv("SEER_EPOCH_WGS", wgs)
-        outs.append(seer.bsattn(qd, kd, vd, mask, want_lse=True))
+    for wgs in (64, 24, 8):
+        opts = {"batch_min_blocks": 1, "batch_wgs": wgs}
+        assert seer.attn_launches(qd, kd, vd, mask, opts=opts) > 1
+        outs.append(seer.bsattn(qd, kd, vd, mask, want_lse=True, opts=opts))
     torch.cuda.synchronize()
     for o2, l2 in outs:
         assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))

@@ -120,19 +120,19 @@ def test_ragged_bsattn_parity(case, pattern, causal, block):
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
 @pytest.mark.parametrize("causal", [True, False])
-def test_ragged_dense_and_split_parity(case, causal, monkeypatch):
-    monkeypatch.setenv("SEER_SPLIT_MIN_WIDTH", "1")
-    monkeypatch.setenv("SEER_SPLIT_DENSE", "1")
+def test_ragged_dense_and_split_parity(case, causal):
+    split = {"split": 1, "split_width": 3}
     B, Hq, Hkv, S, D, dt, Dg = case
     w, q, k, v, _, _ = _inputs(case, ("dense", causal))
     O_ref, lse_ref = oracle.attn(q, k, v, causal=causal)
     qd, kd, vd = (to_device(x) for x in (q, k, v))
-    n = seer.attn_workspace_bytes(qd, kd, vd, causal=causal)
+    n = seer.attn_workspace_bytes(qd, kd, vd, causal=causal, opts=split)
     ws = torch.empty(max(n, 1), dtype=torch.uint8, device="cuda")
     ref = _rows_valid(O_ref, B, Hq, S, 64, D)
     for workspace in (None, ws):
         buf, o = _guarded_out(qd, S)
-        _, lse = seer.dense_attn(qd, kd, vd, causal=causal, out=o, want_lse=True, workspace=workspace)
+        _, lse = seer.dense_attn(qd, kd, vd, causal=causal, out=o, want_lse=True, workspace=workspace,
+                                 opts=split)
         torch.cuda.synchronize()
         assert _guards_intact(buf, S)
         O = as_f64(from_device(o.contiguous()))

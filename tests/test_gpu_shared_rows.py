@@ -1,8 +1,8 @@
 """Dense attention and the ground-truth kernel with several query heads per
 workgroup.  Dense rows are the same for every query head of a KV group, so a
 workgroup takes 2 (or 4) heads of one group for the same query block and loads
-each K/V tile once for all of them (SEER_KV_HEADS_PER_WG caps the count; 1 is
-one head per workgroup).
+each K/V tile once for all of them (the heads_per_wg option caps the count; 1
+is one head per workgroup).
 
 Bars: O and LSE against the fp64 oracle (2e-2 bf16 max-abs, LSE 1e-3), the
 pooled map within the ground-truth test's relative band, and O, LSE and the
@@ -31,23 +31,23 @@ CASES = [
 ]
 
 
-def _run(qd, kd, vd, causal, cap, monkeypatch):
-    monkeypatch.setenv("SEER_KV_HEADS_PER_WG", str(cap))
-    o, lse = seer.dense_attn(qd, kd, vd, causal=causal, want_lse=True)
-    og, lseg, gt = seer.attn_gt(qd, kd, vd, causal=causal, want_lse=True)
+def _run(qd, kd, vd, causal, cap):
+    opts = {"heads_per_wg": cap}
+    o, lse = seer.dense_attn(qd, kd, vd, causal=causal, want_lse=True, opts=opts)
+    og, lseg, gt = seer.attn_gt(qd, kd, vd, causal=causal, want_lse=True, opts=opts)
     torch.cuda.synchronize()
     return o, lse, og, lseg, gt
 
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
 @pytest.mark.parametrize("causal", [True, False])
-def test_dense_and_ground_truth_with_shared_row_workgroups(case, causal, monkeypatch):
+def test_dense_and_ground_truth_with_shared_row_workgroups(case, causal):
     B, Hq, Hkv, S, D = case
     print(f"[shared rows] {case} causal={causal}", flush=True)
     w, q, k, v, _, _ = small_inputs(B, Hq, Hkv, S, D, "bf16", seed=stable_seed("shared-rows", case, causal),
                                     spikes=True)
     qd, kd, vd = (to_device(x) for x in (q, k, v))
-    runs = {cap: _run(qd, kd, vd, causal, cap, monkeypatch) for cap in (1, 2, 4)}
+    runs = {cap: _run(qd, kd, vd, causal, cap) for cap in (1, 2, 4)}
     for cap in (2, 4):
         for name, a, b in zip(("O", "LSE", "O (gt)", "LSE (gt)", "pooled map"), runs[1], runs[cap]):
             assert torch.equal(a.view(torch.uint8), b.view(torch.uint8)), f"{cap} heads per workgroup: {name}"
