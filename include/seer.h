@@ -162,8 +162,10 @@ int seer_abi_version(void);
 const char* seer_status_str(int status);
 
 /* Bytes of device workspace seer_gate needs for this shape (0 on invalid
- * arguments): the pooled-and-projected Q and K (fp32) and, unless the caller
- * passes logits_out, the fp32 gate logits [batch][heads_q][nb][nb]. */
+ * arguments): the pooled-and-projected Q and K (fp32: (heads_q + heads_kv) nb
+ * gate_dim floats per batch entry, 40 MiB for 32 + 8 heads of 2048 blocks at
+ * gate_dim 128) and, when logits_in_workspace is set (seer_gate called with
+ * logits_out NULL), the fp32 gate logits [batch][heads_q][nb][nb]. */
 size_t seer_gate_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate,
                                  int32_t logits_in_workspace);
 
@@ -188,7 +190,8 @@ size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block);
  * Inputs q, k follow desc (bf16 or fp32); wq, wk are fp32 (layout in
  * seer_gate_desc).  Writes out->count, out->idx and, when non-NULL, out->dense.
  * logits_out (device float [B][Hq][nb][nb], or NULL) receives L for j <= i
- * (entries above the diagonal unspecified); when NULL, L lives in the workspace.
+ * (entries above the diagonal unspecified); when NULL, L lives in the
+ * workspace between the logits kernel and the selection kernel.
  * workspace: device memory of at least seer_gate_workspace_bytes(desc, gate,
  * logits_out == NULL) bytes, 256-byte aligned.
  * Unsupported: gate->block not in {64, 128}, head_dim not in {64, 128},
@@ -198,6 +201,29 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate,
                       const void* q, const void* k, const float* wq, const float* wk,
                       seer_block_mask* out, float* logits_out,
                       void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * seer_gate for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): no
+ * workspace argument and no allocation.  Its scratch (the projected rows Qg,
+ * Kg) is a static device array of seer_gate_noalloc_max_bytes() bytes per
+ * device (64 MiB; each device the library runs on holds it until the process
+ * ends), and the logits are formed and selected in one kernel, never leaving
+ * on-chip memory.  Masks equal seer_gate's except where a logit lies within
+ * rounding of the selection cut (the two form the logits in a different
+ * summation order).  Every call on a device shares that device's scratch:
+ * calls that overlap on one device (concurrent streams, or host threads)
+ * race, so serialise them.
+ * Errors: as seer_gate; SEER_ERR_UNSUPPORTED for a kv_shared gate or rows of
+ * more than 2048 blocks; SEER_ERR_WORKSPACE when the projected rows,
+ * (heads_q + heads_kv) nb gate_dim fp32 per batch entry, exceed the scratch.
+ */
+seer_status seer_gate_noalloc(const seer_attn_desc* desc, const seer_gate_desc* gate,
+                              const void* q, const void* k, const float* wq, const float* wk,
+                              seer_block_mask* out, void* stream);
+
+/* Size of seer_gate_noalloc's static scratch, in bytes. */
+size_t seer_gate_noalloc_max_bytes(void);
 
 /*
  * Block-sparse FlashAttention forward (section 3.3): for each query block i of

@@ -78,6 +78,8 @@ _SIGS = {
     "seer_gate_workspace_bytes": ([_P, _P, C.c_int32], C.c_size_t),
     "seer_mask_idx_elems": ([_P, C.c_int32], C.c_size_t),
     "seer_gate": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, C.c_size_t, _P], C.c_int),
+    "seer_gate_noalloc": ([_P, _P, _P, _P, _P, _P, _P, _P], C.c_int),
+    "seer_gate_noalloc_max_bytes": ([], C.c_size_t),
     "seer_bsattn": ([_P, C.c_int32, _P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P], C.c_int),
     "seer_dense_attn": ([_P, C.c_int32, C.c_float, _P, _P, _P, _P, _P, _P], C.c_int),
     "seer_mask_from_dense": ([_P, C.c_int32, _P, _P, _P], C.c_int),
@@ -282,6 +284,32 @@ def gate(q, k, wq, wk, *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
                          _stream(stream))
     _check(st, "seer_gate")
     return mask
+
+
+def gate_noalloc(q, k, wq, wk, mask: "BlockMask", *, mode: int, topk_ratio: float = 0.0, topk_k: int = 0,
+                 threshold: float = 0.0, head_thresholds=None, keep_first: bool = True,
+                 keep_diag: bool = True, w_per_head: bool = True, rope_theta: float = 0.0,
+                 block: int = BLOCK, stream=None) -> "BlockMask":
+    """seer_gate_noalloc: the gate without a workspace and without any
+    allocation (its scratch is a static device array of
+    gate_noalloc_max_bytes()); the caller passes the output mask.  Calls that
+    overlap on one device share the scratch and race."""
+    if mask is None:
+        raise ValueError("gate_noalloc allocates nothing: pass the output mask")
+    d = make_desc(q, k)
+    gd = gate_desc(wq.shape[-1], mode, topk_ratio, topk_k, threshold, head_thresholds,
+                   keep_first, keep_diag, w_per_head, rope_theta, block, False)
+    mask.block = block
+    ms = mask.struct()
+    st = lib().seer_gate_noalloc(C.byref(d), C.byref(gd), _ptr(q), _ptr(k), _ptr(wq), _ptr(wk), C.byref(ms),
+                                 _stream(stream))
+    _check(st, "seer_gate_noalloc")
+    return mask
+
+
+def gate_noalloc_max_bytes() -> int:
+    """Size of seer_gate_noalloc's static device scratch."""
+    return lib().seer_gate_noalloc_max_bytes()
 
 
 def attn_workspace_bytes(q, k, v=None, causal: bool = True, opts=None) -> int:

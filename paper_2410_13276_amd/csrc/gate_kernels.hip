@@ -17,7 +17,12 @@
 //                       threshold on the row softmax), plus the always-kept first
 //                       and diagonal blocks; one wavefront per query-block row,
 //                       writing the ascending index list by ballot compaction.
+//   gate_fused_kernel   the logits of 16 query-block rows on fp32 MFMA into LDS,
+//                       then select_kernel's selection of each row from LDS; no
+//                       logits buffer, so it serves the no-allocation gate.
 //   mask_from_dense_kernel  the same compaction for caller-made 0/1 masks.
+#include <mutex>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -361,75 +366,17 @@ __device__ __forceinline__ void emit_row(uint64_t sel, int nb, int64_t row, int3
   if (lane == 0) count[row] = base;
 }
 
-// GROUP: rows of a mask shared by a KV group (a separate instantiation, so the
-// per-head kernel keeps its register budget and occupancy).
-template <int MAXM, bool GROUP>
-__global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
-  __shared__ __attribute__((aligned(16))) uint32_t s_hist[4][256];  // per-wavefront digit histogram
+// Block selection of one query-block row i of mask head h from its values v
+// (bit m of a mask stands for block j = 64m + lane): the forced blocks, plus
+// either the strict threshold on the row softmax (Eq. 4) or the TopK of the
+// remaining causal blocks (Eq. 3, ties to the smaller block index).  `hist`:
+// this wavefront's 256-word LDS histogram.  One wavefront; returns the lane's
+// selection bits.
+template <int MAXM>
+__device__ __forceinline__ uint64_t select_row(const SelectArgs& a, const float (&v)[MAXM], uint64_t valid,
+                                               uint64_t forced, int i, int h, uint32_t* hist) {
   const int lane = threadIdx.x % kWave;
-  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
-  const int nb = a.n_blocks;
-  const int G = GROUP ? a.group : 0;  // > 0: rows of a mask shared by the G query heads of a KV group
-  const int mheads = G > 0 ? a.heads_q / G : a.heads_q;  // heads of the mask
-  const int64_t rows = (int64_t)a.batch * mheads * nb;
-  if (row >= rows) return;
-  const int i = (int)(row % nb);
-  const int h = (int)((row / nb) % mheads);  // query head, or KV head when shared
   const int M = i / 64 + 1;  // words holding the causal blocks j <= i (wave-uniform)
-
-  // per-lane bit m describes block j = 64m + lane
-  float v[MAXM];
-  uint64_t valid = 0, forced = 0;
-  if constexpr (!GROUP) {
-    const float* L = a.logits + row * nb;
-#pragma unroll
-    for (int m = 0; m < MAXM; ++m) {
-      v[m] = -INFINITY;
-      if (m < M) {
-        const int j = 64 * m + lane;
-        const bool ok = j <= i;
-        if (ok) v[m] = L[j];
-        valid |= (uint64_t)ok << m;
-        forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
-      }
-    }
-  } else {
-#pragma unroll
-    for (int m = 0; m < MAXM; ++m) {
-      const int j = 64 * m + lane;
-      const bool ok = m < M && j <= i;
-      valid |= (uint64_t)ok << m;
-      forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
-    }
-    // the group's score of block j: the mean over its query heads of their gate
-    // probabilities, held as its logarithm so that TopK (by value) and the
-    // threshold test (against the log of the row sum, 1) below apply unchanged
-    float sc[MAXM];
-#pragma unroll
-    for (int m = 0; m < MAXM; ++m) sc[m] = 0.f;
-    const int64_t b = row / ((int64_t)mheads * nb);
-    for (int hh = 0; hh < G; ++hh) {
-      const float* L = a.logits + (((b * a.heads_q) + (int64_t)h * G + hh) * nb + i) * nb;
-#pragma unroll
-      for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? L[64 * m + lane] : -INFINITY;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int m = 0; m < MAXM; ++m)
-        if (m < M) mx = fmaxf(mx, v[m]);
-      mx = wave_max(mx);
-      float s = 0.f;
-#pragma unroll
-      for (int m = 0; m < MAXM; ++m)
-        if (m < M) s += ((valid >> m) & 1) ? __expf(v[m] - mx) : 0.f;
-      const float lse = mx + __logf(wave_sum(s));
-#pragma unroll
-      for (int m = 0; m < MAXM; ++m)
-        if (m < M) sc[m] += ((valid >> m) & 1) ? __expf(v[m] - lse) : 0.f;
-    }
-    const float inv_g = 1.0f / (float)G;
-#pragma unroll
-    for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? __logf(sc[m] * inv_g) : -INFINITY;
-  }
   uint64_t sel = forced;
 
   if (a.mode == 2) {  // threshold on the softmax probability (Eq. 4, strict)
@@ -493,7 +440,6 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
       auto bucket = [&](float x) -> uint32_t {
         return scale > 0.f ? (uint32_t)min(255, max(0, (int)((x - cmn) * scale))) : 0u;
       };
-      uint32_t* hist = s_hist[threadIdx.x / kWave];
       // one histogram pass: digit(m) of the candidates with in_play(m); returns
       // the target bin and the counts above it and in it
       auto pass = [&](auto in_play, auto digit, int above_in, int& bin, int& abv, int& cb) {
@@ -625,7 +571,221 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
       }
     }
   }
+  return sel;
+}
+
+// GROUP: rows of a mask shared by a KV group (a separate instantiation, so the
+// per-head kernel keeps its register budget and occupancy).
+template <int MAXM, bool GROUP>
+__global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
+  __shared__ __attribute__((aligned(16))) uint32_t s_hist[4][256];  // per-wavefront digit histogram
+  const int lane = threadIdx.x % kWave;
+  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+  const int nb = a.n_blocks;
+  const int G = GROUP ? a.group : 0;  // > 0: rows of a mask shared by the G query heads of a KV group
+  const int mheads = G > 0 ? a.heads_q / G : a.heads_q;  // heads of the mask
+  const int64_t rows = (int64_t)a.batch * mheads * nb;
+  if (row >= rows) return;
+  const int i = (int)(row % nb);
+  const int h = (int)((row / nb) % mheads);  // query head, or KV head when shared
+  const int M = i / 64 + 1;  // words holding the causal blocks j <= i (wave-uniform)
+
+  // per-lane bit m describes block j = 64m + lane
+  float v[MAXM];
+  uint64_t valid = 0, forced = 0;
+  if constexpr (!GROUP) {
+    const float* L = a.logits + row * nb;
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) {
+      v[m] = -INFINITY;
+      if (m < M) {
+        const int j = 64 * m + lane;
+        const bool ok = j <= i;
+        if (ok) v[m] = L[j];
+        valid |= (uint64_t)ok << m;
+        forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) {
+      const int j = 64 * m + lane;
+      const bool ok = m < M && j <= i;
+      valid |= (uint64_t)ok << m;
+      forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
+    }
+    // the group's score of block j: the mean over its query heads of their gate
+    // probabilities, held as its logarithm so that TopK (by value) and the
+    // threshold test (against the log of the row sum, 1) below apply unchanged
+    float sc[MAXM];
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) sc[m] = 0.f;
+    const int64_t b = row / ((int64_t)mheads * nb);
+    for (int hh = 0; hh < G; ++hh) {
+      const float* L = a.logits + (((b * a.heads_q) + (int64_t)h * G + hh) * nb + i) * nb;
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? L[64 * m + lane] : -INFINITY;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m)
+        if (m < M) mx = fmaxf(mx, v[m]);
+      mx = wave_max(mx);
+      float s = 0.f;
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m)
+        if (m < M) s += ((valid >> m) & 1) ? __expf(v[m] - mx) : 0.f;
+      const float lse = mx + __logf(wave_sum(s));
+#pragma unroll
+      for (int m = 0; m < MAXM; ++m)
+        if (m < M) sc[m] += ((valid >> m) & 1) ? __expf(v[m] - lse) : 0.f;
+    }
+    const float inv_g = 1.0f / (float)G;
+#pragma unroll
+    for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? __logf(sc[m] * inv_g) : -INFINITY;
+  }
+  const uint64_t sel = select_row<MAXM>(a, v, valid, forced, i, h, s_hist[threadIdx.x / kWave]);
   emit_row<MAXM>(sel, nb, row, a.count, a.idx, a.dense);
+}
+
+// ---------------------------------------------------------------------------
+// fused gate score + select: the logits never leave LDS
+// ---------------------------------------------------------------------------
+//
+// One workgroup of 16 wavefronts per (batch, head, 16 consecutive query-block
+// rows).  Phase 1 computes the rows' block-causal logits (Eq. 1) on fp32 MFMA
+// (v_mfma_f32_16x16x4_f32) into LDS: wavefront w takes the 16-column tiles
+// w, w + 16, ...; lane l supplies row / column l % 16 and the contiguous run
+// of Dg / 4 gate features starting at (l / 16) Dg / 4, so A and B pair
+// identical features.  Phase 2: wavefront w selects row i0 + w from LDS with
+// the select of select_kernel.  Kg of a KV head (nb Dg fp32, 1 MiB at 2048
+// blocks) stays in L2 for the head's workgroups.  LDS: 16 rows of 64 MAXM + 4
+// floats (the pad puts rows 4 apart on different banks): 128 KiB at 2048
+// blocks, the largest row length served here, 64 KiB at 1024 (two workgroups
+// per CU).  Once every wavefront holds its row in registers the same LDS holds
+// the wavefronts' 1 KiB selection histograms.
+constexpr int kFusedRows = 16;
+constexpr int kFusedMaxBlocks = 2048;
+
+template <int MAXM, int DG>
+__global__ __launch_bounds__(1024) void gate_fused_kernel(GateFusedArgs a) {
+  constexpr int LDL = 64 * MAXM + 4;
+  constexpr int WORDS = kFusedRows * LDL > kFusedRows * 256 ? kFusedRows * LDL : kFusedRows * 256;
+  __shared__ __attribute__((aligned(16))) float sL[WORDS];
+  const int nb = a.sel.n_blocks;
+  const int chunks = (nb + kFusedRows - 1) / kFusedRows;
+  const int chunk = chunks - 1 - (int)blockIdx.x;  // heaviest rows first
+  const int h = blockIdx.y, b = blockIdx.z;
+  const int g = h / (a.sel.heads_q / a.heads_kv);
+  const int i0 = kFusedRows * chunk;
+  const int ncols = min(nb, i0 + kFusedRows);  // block-causal: columns j <= i0 + 15
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int r16 = lane % 16, kq = lane / 16;
+  constexpr int KS = DG / 4;  // MFMA steps: this lane's features kq KS .. kq KS + KS - 1
+
+  // phase 1: logits of rows i0 .. i0 + 15 (rows past nb repeat the last one)
+  float qa[KS];
+  {
+    const float* qrow = a.qg + (((int64_t)b * a.sel.heads_q + h) * nb + min(i0 + r16, nb - 1)) * DG + kq * KS;
+#pragma unroll
+    for (int u = 0; u < KS / 4; ++u) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(qrow + 4 * u);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) qa[4 * u + e] = x[e];
+    }
+  }
+  const float* kbase = a.kg + ((int64_t)b * a.heads_kv + g) * nb * DG + kq * KS;
+  // the next column tile's operands load while the current one multiplies
+  auto load_k = [&](int ct, f32x4 (&kb)[KS / 4]) {
+    const float* krow = kbase + (int64_t)min(16 * ct + r16, nb - 1) * DG;
+#pragma unroll
+    for (int u = 0; u < KS / 4; ++u) kb[u] = *reinterpret_cast<const f32x4*>(krow + 4 * u);
+  };
+  f32x4 kn[KS / 4];
+  if (wave * 16 < ncols) load_k(wave, kn);
+  for (int ct = wave; ct * 16 < ncols; ct += kFusedRows) {
+    f32x4 kb[KS / 4];
+#pragma unroll
+    for (int u = 0; u < KS / 4; ++u) kb[u] = kn[u];
+    if ((ct + kFusedRows) * 16 < ncols) load_k(ct + kFusedRows, kn);
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < KS; ++st) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[st], kb[st / 4][st % 4], acc, 0, 0, 0);
+    // accumulator e of lane l: row 4 (l / 16) + e, column 16 ct + l % 16
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sL[(4 * kq + e) * LDL + 16 * ct + r16] = acc[e] * a.scale;
+  }
+  __syncthreads();
+
+  // phase 2: wavefront w selects row i0 + w (rows past nb take no part)
+  const int i = i0 + wave;
+  const int M = i / 64 + 1;
+  const float* L = sL + wave * LDL;
+  float v[MAXM];
+  uint64_t valid = 0, forced = 0;
+#pragma unroll
+  for (int m = 0; m < MAXM; ++m) {
+    v[m] = -INFINITY;
+    if (m < M && i < nb) {
+      const int j = 64 * m + lane;
+      const bool ok = j <= i;
+      if (ok) v[m] = L[j];
+      valid |= (uint64_t)ok << m;
+      forced |= (uint64_t)(ok && ((a.sel.keep_first && j == 0) || (a.sel.keep_diag && j == i))) << m;
+    }
+  }
+  __syncthreads();  // every row is in registers: the LDS now holds the histograms
+  if (i >= nb) return;
+  const uint64_t sel = select_row<MAXM>(a.sel, v, valid, forced, i, h, reinterpret_cast<uint32_t*>(sL) + 256 * wave);
+  const int64_t row = ((int64_t)b * a.sel.heads_q + h) * nb + i;
+  emit_row<MAXM>(sel, nb, row, a.sel.count, a.sel.idx, a.sel.dense);
+}
+
+// Static scratch of seer_gate_noalloc: the projected rows Qg and Kg (the fused
+// kernel needs no logits buffer).  Every call on a device shares that device's
+// copy.  In host code `scratch` names a host-side stand-in, never the device
+// memory: the device address comes from hipGetSymbolAddress, once per device
+// with that device current.
+static __device__ __align__(256) char scratch[kGateScratchBytes];
+
+void* gate_scratch() {
+  constexpr int kMaxDevices = 64;
+  static std::once_flag once[kMaxDevices];
+  static void* ptr[kMaxDevices];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::call_once(once[dev], [dev]() {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess) ptr[dev] = p;
+  });
+  return ptr[dev];
+}
+
+bool gate_fused_supported(int n_blocks, int gate_dim) {
+  return n_blocks >= 1 && n_blocks <= kFusedMaxBlocks && (gate_dim == 32 || gate_dim == 64 || gate_dim == 128);
+}
+
+template <int MAXM>
+static hipError_t gate_fused_dg(const GateFusedArgs& a, hipStream_t s) {
+  const int chunks = (a.sel.n_blocks + kFusedRows - 1) / kFusedRows;
+  const dim3 grid((unsigned)chunks, a.sel.heads_q, a.sel.batch);
+  switch (a.gate_dim) {
+    case 32: hipLaunchKernelGGL((gate_fused_kernel<MAXM, 32>), grid, dim3(1024), 0, s, a); break;
+    case 64: hipLaunchKernelGGL((gate_fused_kernel<MAXM, 64>), grid, dim3(1024), 0, s, a); break;
+    case 128: hipLaunchKernelGGL((gate_fused_kernel<MAXM, 128>), grid, dim3(1024), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gate_fused(const GateFusedArgs& a, hipStream_t s) {
+  if (!gate_fused_supported(a.sel.n_blocks, a.gate_dim) || a.sel.group > 0) return hipErrorInvalidValue;
+  const int m = (a.sel.n_blocks + 63) / 64;
+  if (m <= 1) return gate_fused_dg<1>(a, s);
+  if (m <= 2) return gate_fused_dg<2>(a, s);
+  if (m <= 4) return gate_fused_dg<4>(a, s);
+  if (m <= 8) return gate_fused_dg<8>(a, s);
+  if (m <= 16) return gate_fused_dg<16>(a, s);
+  return gate_fused_dg<32>(a, s);
 }
 
 template <int MAXM>

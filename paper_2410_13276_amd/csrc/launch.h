@@ -52,6 +52,24 @@ struct SelectArgs {
   uint8_t* dense;  // optional
 };
 
+// Fused gate score and selection (per-query-head masks): the logits of the
+// projected rows qg, kg are formed in LDS and selected there (sel.logits unused).
+struct GateFusedArgs {
+  const float* qg;  // [B][Hq][nb][Dg]
+  const float* kg;  // [B][Hkv][nb][Dg]
+  int heads_kv, gate_dim;
+  float scale;      // 1/sqrt(Dg)
+  SelectArgs sel;
+};
+// Whether the fused path serves this shape (row length and gate width).
+bool gate_fused_supported(int n_blocks, int gate_dim);
+
+// The gate's static device scratch (seer_gate_noalloc): kGateScratchBytes per
+// device, held until the process ends.  gate_scratch() returns this device's
+// copy (its address looked up once per device), or nullptr on a HIP error.
+constexpr size_t kGateScratchBytes = (size_t)64 << 20;
+void* gate_scratch();
+
 struct MaskFromDenseArgs {
   const uint8_t* dense;
   int64_t rows;
@@ -148,6 +166,7 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s);
 hipError_t launch_rope_inverse(const RopeArgs& a, hipStream_t s);
 hipError_t launch_gate_logits(const GateLogitsArgs& a, hipStream_t s);
 hipError_t launch_select(const SelectArgs& a, hipStream_t s);
+hipError_t launch_gate_fused(const GateFusedArgs& a, hipStream_t s);
 hipError_t launch_mask_from_dense(const MaskFromDenseArgs& a, hipStream_t s);
 // With a non-null `count` nothing is launched: the attention-kernel launches
 // the call would make are counted into *count.

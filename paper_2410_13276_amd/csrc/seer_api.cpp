@@ -349,25 +349,21 @@ size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block) {
   return (size_t)desc->batch * desc->heads_q * nb * nb;
 }
 
-seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, const void* q,
-                      const void* k, const float* wq, const float* wk, seer_block_mask* out,
-                      float* logits_out, void* workspace, size_t workspace_bytes, void* stream) {
-  seer_status s = check_gate(desc, gate);
-  if (s != SEER_OK) return s;
-  if (!q || !k || !wq || !wk || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
-  if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
+// The gate after argument checks.  fused: the logits are formed and selected
+// in one kernel (gate_fused_kernel) and never leave on-chip memory, so the
+// workspace holds only the projected rows; otherwise the logits kernel writes
+// them to logits_out or the workspace and the selection kernel reads them.
+static seer_status gate_run(const seer_attn_desc* desc, const seer_gate_desc* gate, const void* q, const void* k,
+                            const float* wq, const float* wk, seer_block_mask* out, float* logits_out,
+                            void* workspace, bool fused, hipStream_t st) {
+  seer_status s;
   const int nb = blocks_of(desc->seq_len, gate->block);
-  if (out->n_blocks != nb || out->kv_shared != gate->kv_shared) return SEER_ERR_INVALID_ARG;
-  const bool logits_in_ws = logits_out == nullptr;
+  const bool logits_in_ws = logits_out == nullptr && !fused;
   const GateLayout L = gate_layout(desc, gate, logits_in_ws);
-  if (!workspace || workspace_bytes < L.total) return SEER_ERR_WORKSPACE;
-  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
-
   char* ws = static_cast<char*>(workspace);
   float* qg = reinterpret_cast<float*>(ws + L.qg);
   float* kg = reinterpret_cast<float*>(ws + L.kg);
   float* logits = logits_in_ws ? reinterpret_cast<float*>(ws + L.logits) : logits_out;
-  hipStream_t st = static_cast<hipStream_t>(stream);
   const int D = desc->head_dim, Dg = gate->gate_dim;
 
   seer::PoolProjArgs pa;
@@ -393,20 +389,23 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   pa.seq_len = desc->seq_len;
   if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
 
-  seer::GateLogitsArgs la;
-  la.qg = qg;
-  la.kg = kg;
-  la.batch = desc->batch;
-  la.heads_q = desc->heads_q;
-  la.heads_kv = desc->heads_kv;
-  la.n_blocks = nb;
-  la.gate_dim = Dg;
-  la.scale = (float)(1.0 / std::sqrt((double)Dg));
-  la.logits = logits;
-  if ((s = from_hip(seer::launch_gate_logits(la, st))) != SEER_OK) return s;
+  const float scale = (float)(1.0 / std::sqrt((double)Dg));
+  if (!fused) {
+    seer::GateLogitsArgs la;
+    la.qg = qg;
+    la.kg = kg;
+    la.batch = desc->batch;
+    la.heads_q = desc->heads_q;
+    la.heads_kv = desc->heads_kv;
+    la.n_blocks = nb;
+    la.gate_dim = Dg;
+    la.scale = scale;
+    la.logits = logits;
+    if ((s = from_hip(seer::launch_gate_logits(la, st))) != SEER_OK) return s;
+  }
 
   seer::SelectArgs sa;
-  sa.logits = logits;
+  sa.logits = fused ? nullptr : logits;
   sa.batch = desc->batch;
   sa.heads_q = desc->heads_q;
   sa.n_blocks = nb;
@@ -421,8 +420,52 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   sa.count = out->count;
   sa.idx = out->idx;
   sa.dense = out->dense;
+  if (fused) {
+    seer::GateFusedArgs fa;
+    fa.qg = qg;
+    fa.kg = kg;
+    fa.heads_kv = desc->heads_kv;
+    fa.gate_dim = Dg;
+    fa.scale = scale;
+    fa.sel = sa;
+    return from_hip(seer::launch_gate_fused(fa, st));
+  }
   return from_hip(seer::launch_select(sa, st));
 }
+
+seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, const void* q,
+                      const void* k, const float* wq, const float* wk, seer_block_mask* out,
+                      float* logits_out, void* workspace, size_t workspace_bytes, void* stream) {
+  seer_status s = check_gate(desc, gate);
+  if (s != SEER_OK) return s;
+  if (!q || !k || !wq || !wk || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
+  const int nb = blocks_of(desc->seq_len, gate->block);
+  if (out->n_blocks != nb || out->kv_shared != gate->kv_shared) return SEER_ERR_INVALID_ARG;
+  const GateLayout L = gate_layout(desc, gate, logits_out == nullptr);
+  if (!workspace || workspace_bytes < L.total) return SEER_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
+  return gate_run(desc, gate, q, k, wq, wk, out, logits_out, workspace, false, static_cast<hipStream_t>(stream));
+}
+
+seer_status seer_gate_noalloc(const seer_attn_desc* desc, const seer_gate_desc* gate, const void* q,
+                              const void* k, const float* wq, const float* wk, seer_block_mask* out,
+                              void* stream) {
+  seer_status s = check_gate(desc, gate);
+  if (s != SEER_OK) return s;
+  if (!q || !k || !wq || !wk || !out || !out->count || !out->idx) return SEER_ERR_INVALID_ARG;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
+  const int nb = blocks_of(desc->seq_len, gate->block);
+  if (out->n_blocks != nb || out->kv_shared != gate->kv_shared) return SEER_ERR_INVALID_ARG;
+  if (gate->kv_shared || !seer::gate_fused_supported(nb, gate->gate_dim)) return SEER_ERR_UNSUPPORTED;
+  const GateLayout L = gate_layout(desc, gate, false);
+  if (L.total > seer::kGateScratchBytes) return SEER_ERR_WORKSPACE;  // beyond the static scratch
+  void* scratch = seer::gate_scratch();
+  if (!scratch) return SEER_ERR_HIP;
+  return gate_run(desc, gate, q, k, wq, wk, out, nullptr, scratch, true, static_cast<hipStream_t>(stream));
+}
+
+size_t seer_gate_noalloc_max_bytes(void) { return seer::kGateScratchBytes; }
 
 // block: tokens per mask block (64 or 128; ignored without a mask).
 static seer_status attn_common(const seer_attn_desc* desc, int32_t block, const seer_block_mask* mask,

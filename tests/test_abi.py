@@ -24,7 +24,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 20, names
+    assert len(names) == 22, names
     L = C.CDLL(seer.LIB_PATH)
     for n in names:
         assert hasattr(L, n), n
@@ -73,6 +73,7 @@ def test_workspace_size_formula():
     want = up(2 * 4 * nb * 128 * 4) + up(2 * 2 * nb * 128 * 4)
     assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 0) == want
     assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 1) == want + up(2 * 4 * nb * nb * 4)
+    assert L.seer_gate_noalloc_max_bytes() == 64 << 20
     assert L.seer_mask_idx_elems(C.byref(d), 64) == 2 * 4 * nb * nb
     assert L.seer_mask_idx_elems(C.byref(d), 128) == 2 * 4 * (nb // 2) ** 2   # 128-token blocks
     assert L.seer_mask_idx_elems(C.byref(d), 96) == 0
@@ -248,6 +249,25 @@ def test_attn_workspace_bytes_formula():
     d = _desc(B=1, Hq=4, Hkv=2, S=8192, D=64)                                  # nb 128 <= 256 at D 64
     assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, opt(split=1)) == 0
     assert L.seer_attn_workspace_bytes(C.byref(d), 64, 1, opt(split=1, split_width=5)) == want(4, 128, 5, 64)
+
+
+def test_gate_noalloc_rejects_unsupported_and_oversized():
+    """The no-allocation gate validates before touching its scratch: the shared
+    mask and rows of more than 2048 blocks are unsupported, and shapes whose
+    projected rows exceed the 64 MiB scratch are refused (SEER_ERR_WORKSPACE)."""
+    L = seer.lib()
+    m = seer.BlockMaskStruct()
+    call = lambda d, g, nb: (setattr(m, "n_blocks", nb), setattr(m, "count", FAKE), setattr(m, "idx", FAKE),
+                             setattr(m, "kv_shared", g.kv_shared),
+                             L.seer_gate_noalloc(C.byref(d), C.byref(g), FAKE, FAKE, FAKE, FAKE, C.byref(m),
+                                                 None))[-1]
+    assert call(_desc(S=64 * 2049), _gate(), 2049) == seer.ERR_UNSUPPORTED          # > 2048 blocks
+    assert call(_desc(), _gate(kv_shared=1), 16) == seer.ERR_UNSUPPORTED            # shared mask
+    # (64 + 8) heads x 2048 blocks x 128 x 4 B = 72 MiB of projected rows > 64 MiB
+    assert call(_desc(Hq=64, Hkv=8, S=131072), _gate(), 2048) == seer.ERR_WORKSPACE
+    assert call(_desc(), _gate(), 15) == seer.ERR_INVALID_ARG                        # mask shape
+    assert L.seer_gate_noalloc(C.byref(_desc()), C.byref(_gate()), None, FAKE, FAKE, FAKE, C.byref(m),
+                               None) == seer.ERR_INVALID_ARG
 
 
 def test_attn_launches_rejects_bad_args():

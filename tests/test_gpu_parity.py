@@ -51,7 +51,10 @@ CASES = [
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
 @pytest.mark.parametrize("sel", ["ratio", "fixed", "thr", "thr_head", "noforce"])
-def test_gate_mask_parity(case, sel):
+@pytest.mark.parametrize("path", ["workspace", "logits"])
+def test_gate_mask_parity(case, sel, path):
+    """path 'workspace': the logits live in the gate's workspace; 'logits': they
+    are written to the caller's buffer and also checked against the oracle's."""
     B, Hq, Hkv, S, D, dt, Dg = case
     w, q, k, v, wq, wk = small_inputs(B, Hq, Hkv, S, D, dt, seed=stable_seed(case, sel), Dg=Dg,
                                       spikes=True)
@@ -75,17 +78,20 @@ def test_gate_mask_parity(case, sel):
         gargs = dict(mode=seer.TOPK_RATIO, topk_ratio=0.25)
         kw = dict(keep_first=0, keep_diag=0)
     orc = oracle_gate(q, k, wq, wk, mode, **args, **kw)
-    logits = torch.empty((B, Hq, S // 64, S // 64), dtype=torch.float32, device="cuda")
+    logits = None
+    if path == "logits":
+        logits = torch.empty((B, Hq, S // 64, S // 64), dtype=torch.float32, device="cuda")
     mask = seer.gate(qd, kd, wqd, wkd, **gargs, **kw, dense_out=True, logits_out=logits)
     torch.cuda.synchronize()
     count, idx, dense = gpu_mask_numpy(mask)
     np.testing.assert_array_equal(dense, mask.dense.cpu().numpy())
-    # the raw gate logits agree with the oracle's on the causal triangle
-    nb = S // 64
-    tri = np.tril(np.ones((nb, nb), bool))
-    gl = logits.cpu().numpy().astype(np.float64)
-    err = np.abs(gl - orc["L"])[..., tri].max()
-    assert err <= 1e-5 * max(1.0, np.abs(orc["L"][..., tri]).max()), err
+    if logits is not None:
+        # the raw gate logits agree with the oracle's on the causal triangle
+        nb = S // 64
+        tri = np.tril(np.ones((nb, nb), bool))
+        gl = logits.cpu().numpy().astype(np.float64)
+        err = np.abs(gl - orc["L"])[..., tri].max()
+        assert err <= 1e-5 * max(1.0, np.abs(orc["L"][..., tri]).max()), err
     check_mask(dense, count, orc, topk=mode != oracle.THRESHOLD)
 
 
