@@ -7,8 +7,10 @@ __graft_entry__.smoke() and the cpu_baseline leg of bench.py use it.
 Every function follows one step of the SeerAttention prefill path
 (arXiv 2410.13276): pooling and gate (section 3.1, Eq. 1), block selection
 (Eq. 3 TopK, Eq. 4 threshold), masked causal attention (section 3.3), and the
-MaxPool2D distillation target (Eq. 2).  The arithmetic itself lives in the C
-file; this module only marshals numpy arrays.
+MaxPool2D distillation target (Eq. 2).  Pooling, gate, selection, attention and
+the pooled target are computed in the C file, this module only marshals numpy
+arrays for them; distill() (the KL loss of Eq. 2 and its weight gradients) is
+written here in numpy fp64 on top of the C gate.
 """
 from __future__ import annotations
 

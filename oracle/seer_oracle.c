@@ -88,9 +88,11 @@ int orc_set_threads(int n) {
 /*
  * Pooling along the sequence (section 3.1).  x is [B][H][S][D] with strides
  * st[0..2]; block is the pooling kernel and stride.  kind selects
- *   ORC_POOL_AVG          -> out [B][H][S/block][D]      (Q side)
- *   ORC_POOL_MAX_MIN_AVG  -> out [B][H][S/block][3*D]    (K side: max | min | avg)
- * Returns 0, or -1 when S is not a multiple of block.
+ *   ORC_POOL_AVG          -> out [B][H][nb][D]      (Q side)
+ *   ORC_POOL_MAX_MIN_AVG  -> out [B][H][nb][3*D]    (K side: max | min | avg)
+ * with nb = ceil(S / block): a partial last block is pooled over the rows it
+ * holds (its mean divides by that count).  Returns 0, or -1 for a non-positive
+ * block or length.
  */
 int orc_pool(const void *x, int dtype, int B, int H, int S, int D,
              const int64_t *st, int block, int kind, double *out) {
