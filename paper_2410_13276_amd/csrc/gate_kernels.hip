@@ -257,7 +257,7 @@ __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
   const int b = blockIdx.z;
   const int g = h / (a.heads_q / a.heads_kv);
 
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int lane = threadIdx.x % kWave;
   const int wi = wave / 2, wj = wave % 2;
   if (I == J && wj > wi) return;  // sub-tile entirely above the diagonal
@@ -366,212 +366,251 @@ __device__ __forceinline__ void emit_row(uint64_t sel, int nb, int64_t row, int3
   if (lane == 0) count[row] = base;
 }
 
+// A copy of a wave-uniform int that the compiler cannot merge with other uses
+// of the same value.  The word loops below each compare it with their
+// constant word index: merged across loops, those per-word conditions would
+// stay live as 64-bit lane masks for the whole selection and spill.
+// A wave-uniform float (equal in every lane) as a scalar.
+__device__ __forceinline__ float uniform_f(float x) {
+  return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
+}
+
+__device__ __forceinline__ int opaque_sgpr(int x) {
+  asm volatile("" : "+s"(x));
+  return x;
+}
+
 // Block selection of one query-block row i of mask head h from its values v
-// (bit m of a mask stands for block j = 64m + lane): the forced blocks, plus
+// (v[m] of a lane: block j = 64 m + lane; -inf for j > i), written straight
+// to the row's index list (and optional 0/1 row): the forced blocks, plus
 // either the strict threshold on the row softmax (Eq. 4) or the TopK of the
 // remaining causal blocks (Eq. 3, ties to the smaller block index).  `hist`:
-// this wavefront's 256-word LDS histogram.  One wavefront; returns the lane's
-// selection bits.
+// this wavefront's 256-word LDS histogram.  One wavefront.
+//
+// TopK finds the cut without sorting.  A first pass counts the candidates in
+// 256 equal-width buckets of their value range (the bucket index never
+// decreases with the value, so the bucket holding the take-th largest value
+// is found from the counts); the candidates of that bucket (usually a few) are
+// gathered one per lane and the cut T is read off their ranks.  A bucket of
+// more than 64 candidates (heavy ties) is resolved by bisection over the keys.
+// Every block then takes one test: above the bucket, or in it and at or above
+// T, with ties at T going to the smaller indices.  State is kept per block in
+// registers (bucket indices, no bit masks), so the passes are straight-line
+// code.
 template <int MAXM>
-__device__ __forceinline__ uint64_t select_row(const SelectArgs& a, const float (&v)[MAXM], uint64_t valid,
-                                               uint64_t forced, int i, int h, uint32_t* hist) {
+__device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v)[MAXM], int i, int h,
+                                            int64_t row, uint32_t* hist) {
   const int lane = threadIdx.x % kWave;
+  const int nb = a.n_blocks;
   const int M = i / 64 + 1;  // words holding the causal blocks j <= i (wave-uniform)
-  uint64_t sel = forced;
+  const uint64_t lt = lanemask_lt();
+  const int f0 = a.keep_first ? 0 : -1;  // forced blocks (-1: none)
+  const int f1 = a.keep_diag ? i : -1;
+  // b[m]: -2 forced, -1 past the diagonal, otherwise a candidate (0; for TopK
+  // its value bucket below).  All later tests read b, so no per-block
+  // condition has to stay live across the passes.
+  int b[MAXM];
+#pragma unroll
+  for (int m = 0; m < MAXM; ++m) {
+    b[m] = -1;
+    if (m < opaque_sgpr(M)) {
+      const int j = 64 * m + lane;
+      b[m] = j > i ? -1 : (((j == f0) | (j == f1)) ? -2 : 0);
+    }
+  }
 
-  if (a.mode == 2) {  // threshold on the softmax probability (Eq. 4, strict)
+  // selection rule, filled in below: a causal block is taken if forced, or
+  // (threshold) v - lse > lthr, or (TopK) its bucket > bstar, or == bstar and
+  // (all_in || key > T || (key == T && tie rank < need))
+  const bool thr_mode = a.mode == 2;
+  float lse = 0.f, lthr = -INFINITY;
+  int bstar = -1;
+  bool all_in = true;
+  uint32_t T = 0u;
+  int need = -1;  // < 0: no tie at T to break
+
+  if (thr_mode) {  // threshold on the softmax probability (Eq. 4, strict)
     float mx = -INFINITY;
 #pragma unroll
     for (int m = 0; m < MAXM; ++m)
-      if (m < M) mx = fmaxf(mx, v[m]);
-    mx = wave_max(mx);
-    float s = 0.f;
+      if (m < opaque_sgpr(M)) mx = fmaxf(mx, v[m]);
+    mx = uniform_f(wave_max(mx));
+    float sum = 0.f;
 #pragma unroll
     for (int m = 0; m < MAXM; ++m)
-      if (m < M) s += ((valid >> m) & 1) ? __expf(v[m] - mx) : 0.f;
-    s = wave_sum(s);
-    const float lse = mx + __logf(s);
+      if (m < opaque_sgpr(M)) sum += __expf(v[m] - mx);  // exp(-inf) = 0 past the diagonal
+    sum = uniform_f(wave_sum(sum));
+    lse = mx + __logf(sum);
     const float t = a.head_thresholds ? a.head_thresholds[h] : a.threshold;
-    if (t <= 0.f) {
-      sel = valid;
-    } else {
-      const float lt = __logf(t);
-#pragma unroll
-      for (int m = 0; m < MAXM; ++m)
-        if (m < M) sel |= (uint64_t)(((valid >> m) & 1) && (v[m] - lse) > lt) << m;
-    }
+    lthr = t <= 0.f ? -INFINITY : __logf(t);
   } else {  // TopK (Eq. 3) over the non-forced causal blocks
     const int nf = (a.keep_first ? 1 : 0) + ((a.keep_diag && !(a.keep_first && i == 0)) ? 1 : 0);
     int kk = (a.mode == 0) ? (int)ceil(a.topk_ratio * (double)(i + 1)) : a.topk_k;
     kk = min(i + 1, max(nf, kk));
     const int take = kk - nf;
     const int ncand = i + 1 - nf;
-    const uint64_t cand = valid & ~forced;
     if (take >= ncand) {
-      sel = valid;
-    } else if (take > 0) {
-      // T: the largest value with #{candidates : value >= T} >= take.  The
-      // first digit is a bucket of 256 equal-width value ranges over the row's
-      // candidate [min, max]; the bucket index is non-decreasing in the value,
-      // so the bucket holding T is found from bucket counts.  Logits spread
-      // over their range, so this pass has few LDS-atomic collisions, where the
-      // top bits of the order-preserving keys are shared by almost every
-      // candidate.  Inside that bucket T is then found exactly, 8 key bits at
-      // a time.  Each pass histograms the candidates still in play in a
-      // per-wavefront LDS histogram; `above` counts candidates already known to
-      // lie above; once exactly `take` candidates lie at or above the current
-      // prefix the selected set is fixed.  When the target bucket holds at most
-      // 64 candidates (the usual case: a few per bucket) their keys are instead
-      // gathered one per lane and T is read off their ranks, which costs one
-      // scan of the row instead of one per digit (gate 0.806 -> 0.777 ms at
-      // 131072 tokens, the same masks); when no tie straddles T the final scan
-      // skips the tie ranking (0.779 -> 0.754 ms).
+      bstar = -1;  // every candidate
+    } else if (take <= 0) {
+      bstar = 256;  // none
+    } else {
       float cmx = -INFINITY, cmn = INFINITY;
 #pragma unroll
       for (int m = 0; m < MAXM; ++m)
-        if (m < M && ((cand >> m) & 1)) {
-          cmx = fmaxf(cmx, v[m]);
-          cmn = fminf(cmn, v[m]);
+        if (m < opaque_sgpr(M)) {
+          cmx = fmaxf(cmx, b[m] == 0 ? v[m] : -INFINITY);
+          cmn = fminf(cmn, b[m] == 0 ? v[m] : INFINITY);
         }
-      cmx = wave_max(cmx);
-      cmn = -wave_max(-cmn);
+      cmx = uniform_f(wave_max(cmx));
+      cmn = uniform_f(-wave_max(-cmn));
       const float span = cmx - cmn;
       const float scale = (span > 0.f && span < INFINITY) ? 256.f / span : 0.f;
-      auto bucket = [&](float x) -> uint32_t {
-        return scale > 0.f ? (uint32_t)min(255, max(0, (int)((x - cmn) * scale))) : 0u;
-      };
-      // one histogram pass: digit(m) of the candidates with in_play(m); returns
-      // the target bin and the counts above it and in it
-      auto pass = [&](auto in_play, auto digit, int above_in, int& bin, int& abv, int& cb) {
-        *reinterpret_cast<u32x4*>(hist + 4 * lane) = u32x4{0u, 0u, 0u, 0u};
-        __builtin_amdgcn_wave_barrier();
+      // bucket pass
+      *reinterpret_cast<u32x4*>(hist + 4 * lane) = u32x4{0u, 0u, 0u, 0u};
+      __builtin_amdgcn_wave_barrier();
 #pragma unroll
-        for (int m = 0; m < MAXM; ++m)
-          if (m < M && ((cand >> m) & 1) && in_play(m)) atomicAdd(hist + digit(m), 1u);
-        __builtin_amdgcn_wave_barrier();
-        const u32x4 c = *reinterpret_cast<const u32x4*>(hist + 4 * lane);  // bins 4 lane .. +3
-        const int local = (int)(c[0] + c[1] + c[2] + c[3]);
-        int incl = local;  // candidates in the bins of this lane and every higher lane
-#pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-          const int t = __shfl_down(incl, off);
-          if (lane + off < kWave) incl += t;
+      for (int m = 0; m < MAXM; ++m) {
+        if (m < opaque_sgpr(M)) {
+          const int bk = min(255, max(0, (int)((v[m] - cmn) * scale)));
+          b[m] = b[m] == 0 ? bk : b[m];
+          if (b[m] >= 0) atomicAdd(hist + b[m], 1u);
         }
-        // the target bin: the highest b with above + #{digit >= b} >= take
-        int run = above_in + (incl - local);
-        int found = -1, ab = 0, cc = 0;
+      }
+      __builtin_amdgcn_wave_barrier();
+      const u32x4 cnt4 = *reinterpret_cast<const u32x4*>(hist + 4 * lane);  // bins 4 lane .. +3
+      const int local = (int)(cnt4[0] + cnt4[1] + cnt4[2] + cnt4[3]);
+      int incl = local;  // candidates in the bins of this lane and every higher lane
 #pragma unroll
-        for (int e = 3; e >= 0; --e) {
-          if (found < 0 && run < take && run + (int)c[e] >= take) {
-            found = e;
-            ab = run;
-            cc = (int)c[e];
-          }
-          run += (int)c[e];
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int t = __shfl_down(incl, off);
+        if (lane + off < kWave) incl += t;
+      }
+      // the target bin: the highest b with #{bucket >= b} >= take
+      int run = incl - local, found = -1, ab = 0, cc = 0;
+#pragma unroll
+      for (int e = 3; e >= 0; --e) {
+        if (found < 0 && run < take && run + (int)cnt4[e] >= take) {
+          found = e;
+          ab = run;
+          cc = (int)cnt4[e];
         }
-        const uint64_t hit = __ballot(found >= 0);  // exactly one lane: bins are monotone
-        const int src = __builtin_ctzll(hit);
-        bin = 4 * src + __shfl(found, src);
-        abv = __shfl(ab, src);
-        cb = __shfl(cc, src);
-      };
-      int bstar, above, cb;
-      pass([&](int) { return true; }, [&](int m) { return bucket(v[m]); }, 0, bstar, above, cb);
-      const bool closed_bucket = above + cb == take;
-      uint32_t prefix = 0;
-      int cntT = take + 1;  // != take until the set closes early
-      int shift = 0;
-      if (!closed_bucket && cb <= kWave) {
-        // few candidates in the target bucket: gather their keys, one per lane,
-        // and find T as the key of rank take - above among them (by value)
-        __builtin_amdgcn_wave_barrier();
-        const uint64_t lt = lanemask_lt();
-        int n = 0;
+        run += (int)cnt4[e];
+      }
+      const uint64_t hit = __ballot(found >= 0);  // exactly one lane: bins are monotone
+      const int src = __builtin_ctzll(hit);
+      bstar = 4 * src + __builtin_amdgcn_readlane(found, src);
+      const int above = __builtin_amdgcn_readlane(ab, src);
+      const int cb = __builtin_amdgcn_readlane(cc, src);
+      const int want = take - above;  // 1 <= want <= cb
+      if (want < cb) {
+        all_in = false;
+        int gt = 0, ge = 0;  // bucket candidates with key > T, >= T
+        if (cb <= kWave) {
+          // gather the bucket's keys one per lane, then T = the key of rank want
+          __builtin_amdgcn_wave_barrier();
+          int n = 0;
 #pragma unroll
-        for (int m = 0; m < MAXM; ++m) {
-          if (m < M) {
-            const bool in_b = ((cand >> m) & 1) && bucket(v[m]) == (uint32_t)bstar;
-            const uint64_t bal = __ballot(in_b);
-            if (bal) {
+          for (int m = 0; m < MAXM; ++m) {
+            if (m < opaque_sgpr(M)) {
+              const bool in_b = b[m] == bstar;
+              const uint64_t bal = __ballot(in_b);
               if (in_b) hist[n + __popcll(bal & lt)] = ordered_key(v[m]);
               n += __popcll(bal);
             }
           }
-        }
-        __builtin_amdgcn_wave_barrier();
-        const uint32_t key = lane < cb ? hist[lane] : 0u;
-        int g = 0, eqc = 0;
-        for (int t = 0; t < cb; ++t) {
-          const uint32_t kt = hist[t];
-          g += kt > key ? 1 : 0;
-          eqc += kt == key ? 1 : 0;
-        }
-        const int want = take - above;  // 1 <= want <= cb - 1
-        const uint64_t hit = __ballot(lane < cb && g < want && g + eqc >= want);
-        const int src = __builtin_ctzll(hit);
-        prefix = __shfl(key, src);
-        const int gs = __shfl(g, src);
-        if (gs + __shfl(eqc, src) == want) cntT = take;  // no tie to break at T: every key >= T is taken
-        above += gs;
-      } else if (!closed_bucket) {
-        for (int d = 3; d >= 0; --d) {
-          const int sh = 8 * d;
-          int b;
-          pass([&](int m) {
-                 return bucket(v[m]) == (uint32_t)bstar &&
-                        (d == 3 || (ordered_key(v[m]) >> (sh + 8)) == prefix);
-               },
-               [&](int m) { return (ordered_key(v[m]) >> sh) & 255u; }, above, b, above, cb);
-          prefix = (d == 3) ? (uint32_t)b : ((prefix << 8) | (uint32_t)b);
-          if (above + cb == take) {
-            cntT = take;
-            shift = sh;
-            break;
+          __builtin_amdgcn_wave_barrier();
+          const uint32_t key = lane < cb ? hist[lane] : 0u;
+          int g = 0, eqc = 0;
+          for (int t = 0; t < cb; ++t) {
+            const uint32_t kt = hist[t];
+            g += kt > key ? 1 : 0;
+            eqc += kt == key ? 1 : 0;
           }
-        }
-      }
-      const uint32_t T = (cntT == take) ? (prefix << shift) : prefix;
-      const int gt = above;  // candidates with value > T (when the set did not close early)
-      // candidates in higher buckets are taken; in the target bucket, everything
-      // when the bucket closed the set, everything >= T when the key digits
-      // closed it, otherwise everything > T plus the (take - gt)
-      // smallest-index candidates tied at T
-      const int need = (closed_bucket || cntT == take) ? 0 : take - gt;
-      const uint32_t strict_from = (cntT == take) ? T : T + 1;  // in-bucket key >= strict_from is taken
-      if (need == 0) {  // no tie to break: a plain test per block
+          const uint64_t hit2 = __ballot(lane < cb && g < want && g + eqc >= want);
+          const int s2 = __builtin_ctzll(hit2);
+          T = (uint32_t)__builtin_amdgcn_readlane((int)key, s2);
+          gt = __builtin_amdgcn_readlane(g, s2);
+          ge = gt + __builtin_amdgcn_readlane(eqc, s2);
+        } else {
+          // heavy ties: bisection over the keys of the bucket,
+          // count(key >= lo) >= want > count(key >= hi + 1)
+          auto count_ge = [&](uint32_t x) -> int {
+            int c = 0;
 #pragma unroll
-        for (int m = 0; m < MAXM; ++m) {
-          if (m < M) {
-            const bool c = (cand >> m) & 1;
-            const uint32_t bk = bucket(v[m]);
-            const bool take_it = c && (bk > (uint32_t)bstar ||
-                                       (bk == (uint32_t)bstar && (closed_bucket || ordered_key(v[m]) >= strict_from)));
-            sel |= (uint64_t)take_it << m;
-          }
-        }
-      } else {  // everything > T, then the smallest-index candidates tied at T
-        const uint64_t lt = lanemask_lt();
-        int before = 0;
+            for (int m = 0; m < MAXM; ++m)
+              if (m < opaque_sgpr(M)) c += __popcll(__ballot(b[m] == bstar && ordered_key(v[m]) >= x));
+            return c;
+          };
+          uint32_t klo = 0xFFFFFFFFu, khi = 0u;
 #pragma unroll
-        for (int m = 0; m < MAXM; ++m) {
-          if (m < M) {
-            const bool c = (cand >> m) & 1;
-            const uint32_t bk = bucket(v[m]);
-            const uint32_t key = ordered_key(v[m]);
-            const bool in_b = c && bk == (uint32_t)bstar;
-            const bool take_it = (c && bk > (uint32_t)bstar) ||
-                                 (in_b && (closed_bucket || (key >= strict_from && (cntT == take || key != T))));
-            const bool eq = in_b && !closed_bucket && cntT != take && key == T;
-            const uint64_t bal = __ballot(eq);
-            const int rank = before + __popcll(bal & lt);
-            sel |= (uint64_t)(take_it || (eq && rank < need)) << m;
-            before += __popcll(bal);
+          for (int m = 0; m < MAXM; ++m)
+            if (m < opaque_sgpr(M)) {
+              const uint32_t k = ordered_key(v[m]);
+              klo = min(klo, b[m] == bstar ? k : 0xFFFFFFFFu);
+              khi = max(khi, b[m] == bstar ? k : 0u);
+            }
+          klo = (uint32_t)__builtin_amdgcn_readfirstlane((int)wave_min_u32(klo));
+          khi = (uint32_t)__builtin_amdgcn_readfirstlane((int)wave_max_u32(khi));
+          uint32_t lo = klo, hi = khi;
+          while (lo < hi) {
+            const uint32_t mid = lo + ((hi - lo) >> 1) + 1;  // in (lo, hi]
+            if (count_ge(mid) >= want) lo = mid;
+            else hi = mid - 1;
           }
+          T = lo;
+          ge = count_ge(T);
+          gt = T < khi ? count_ge(T + 1) : 0;
         }
+        need = (ge == want) ? -1 : want - gt;  // ties at T straddle the cut: take the first `need`
       }
     }
   }
-  return sel;
+
+  // emit: ascending index list by ballot compaction.  The rule reduces to
+  // compares against scalars: taken if forced, or bucket > bstar, or bucket ==
+  // bstar and (the whole bucket is in, or key >= kcut, or tied at T with rank
+  // < need).
+  const bool in_rule = !thr_mode && bstar >= 0 && bstar < 256;  // bucket bstar is split by keys
+  const bool by_key = in_rule && !all_in;
+  const bool tie = by_key && need >= 0;
+  const uint32_t kcut = tie ? T + 1u : T;
+  const bool key_in = !(tie && T == 0xFFFFFFFFu);  // (no key lies above the largest)
+  uint16_t* const idx_row = a.idx + row * nb;
+  uint8_t* const dense_row = a.dense ? a.dense + row * nb : nullptr;
+  int base = 0, before = 0;
+#pragma unroll
+  for (int m = 0; m < MAXM; ++m) {
+    const int j = 64 * m + lane;
+    if (m < opaque_sgpr(M)) {
+      const int bm = b[m];
+      bool s = bm == -2;
+      if (thr_mode) {
+        s = s | ((bm == 0) & (v[m] - lse > lthr));
+      } else {
+        s = s | (bm > bstar);
+        if (by_key) {
+          const uint32_t key = ordered_key(v[m]);
+          const bool in_b = bm == bstar;
+          s = s | (in_b & (key >= kcut) & key_in);
+          if (tie) {  // the smallest-index candidates tied at T
+            const bool eq = in_b & (key == T);
+            const uint64_t bal_eq = __ballot(eq);
+            s = s | (eq & (before + (int)__popcll(bal_eq & lt) < need));
+            before += __popcll(bal_eq);
+          }
+        } else if (in_rule) {
+          s = s | (bm == bstar);
+        }
+      }
+      const uint64_t bal = __ballot(s);
+      if (s) idx_row[base + (int)__popcll(bal & lt)] = (uint16_t)j;
+      base += __popcll(bal);
+      if (dense_row && j < nb) dense_row[j] = s ? 1 : 0;
+    } else if (dense_row && j < nb) {
+      dense_row[j] = 0;
+    }
+  }
+  if (lane == 0) a.count[row] = base;
 }
 
 // GROUP: rows of a mask shared by a KV group (a separate instantiation, so the
@@ -580,51 +619,40 @@ template <int MAXM, bool GROUP>
 __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_hist[4][256];  // per-wavefront digit histogram
   const int lane = threadIdx.x % kWave;
-  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+  // the wavefront index is uniform: readfirstlane makes row, i and the word
+  // count M scalars, so the per-word guards below are scalar branches
+  // grid: (query-block rows / 4, mask heads, batch), heaviest rows first
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int nb = a.n_blocks;
   const int G = GROUP ? a.group : 0;  // > 0: rows of a mask shared by the G query heads of a KV group
   const int mheads = G > 0 ? a.heads_q / G : a.heads_q;  // heads of the mask
-  const int64_t rows = (int64_t)a.batch * mheads * nb;
-  if (row >= rows) return;
-  const int i = (int)(row % nb);
-  const int h = (int)((row / nb) % mheads);  // query head, or KV head when shared
+  const int i = nb - 1 - ((int)blockIdx.x * 4 + wv);
+  if (i < 0) return;
+  const int h = blockIdx.y;  // query head, or KV head when shared
+  const int64_t row = ((int64_t)blockIdx.z * mheads + h) * nb + i;
   const int M = i / 64 + 1;  // words holding the causal blocks j <= i (wave-uniform)
 
-  // per-lane bit m describes block j = 64m + lane
+  // v[m]: block j = 64 m + lane, -inf past the diagonal
   float v[MAXM];
-  uint64_t valid = 0, forced = 0;
   if constexpr (!GROUP) {
     const float* L = a.logits + row * nb;
 #pragma unroll
     for (int m = 0; m < MAXM; ++m) {
       v[m] = -INFINITY;
-      if (m < M) {
-        const int j = 64 * m + lane;
-        const bool ok = j <= i;
-        if (ok) v[m] = L[j];
-        valid |= (uint64_t)ok << m;
-        forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
-      }
+      if (m < M && 64 * m + lane <= i) v[m] = L[64 * m + lane];
     }
   } else {
-#pragma unroll
-    for (int m = 0; m < MAXM; ++m) {
-      const int j = 64 * m + lane;
-      const bool ok = m < M && j <= i;
-      valid |= (uint64_t)ok << m;
-      forced |= (uint64_t)(ok && ((a.keep_first && j == 0) || (a.keep_diag && j == i))) << m;
-    }
     // the group's score of block j: the mean over its query heads of their gate
     // probabilities, held as its logarithm so that TopK (by value) and the
     // threshold test (against the log of the row sum, 1) below apply unchanged
     float sc[MAXM];
 #pragma unroll
     for (int m = 0; m < MAXM; ++m) sc[m] = 0.f;
-    const int64_t b = row / ((int64_t)mheads * nb);
+    const int64_t b = blockIdx.z;
     for (int hh = 0; hh < G; ++hh) {
       const float* L = a.logits + (((b * a.heads_q) + (int64_t)h * G + hh) * nb + i) * nb;
 #pragma unroll
-      for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? L[64 * m + lane] : -INFINITY;
+      for (int m = 0; m < MAXM; ++m) v[m] = (m < M && 64 * m + lane <= i) ? L[64 * m + lane] : -INFINITY;
       float mx = -INFINITY;
 #pragma unroll
       for (int m = 0; m < MAXM; ++m)
@@ -633,18 +661,17 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
       float s = 0.f;
 #pragma unroll
       for (int m = 0; m < MAXM; ++m)
-        if (m < M) s += ((valid >> m) & 1) ? __expf(v[m] - mx) : 0.f;
+        if (m < M) s += __expf(v[m] - mx);
       const float lse = mx + __logf(wave_sum(s));
 #pragma unroll
       for (int m = 0; m < MAXM; ++m)
-        if (m < M) sc[m] += ((valid >> m) & 1) ? __expf(v[m] - lse) : 0.f;
+        if (m < M) sc[m] += __expf(v[m] - lse);
     }
     const float inv_g = 1.0f / (float)G;
 #pragma unroll
-    for (int m = 0; m < MAXM; ++m) v[m] = ((valid >> m) & 1) ? __logf(sc[m] * inv_g) : -INFINITY;
+    for (int m = 0; m < MAXM; ++m) v[m] = (m < M && 64 * m + lane <= i) ? __logf(sc[m] * inv_g) : -INFINITY;
   }
-  const uint64_t sel = select_row<MAXM>(a, v, valid, forced, i, h, s_hist[threadIdx.x / kWave]);
-  emit_row<MAXM>(sel, nb, row, a.count, a.idx, a.dense);
+  select_emit<MAXM>(a, v, i, h, row, s_hist[wv]);
 }
 
 // ---------------------------------------------------------------------------
@@ -678,7 +705,7 @@ __global__ __launch_bounds__(1024) void gate_fused_kernel(GateFusedArgs a) {
   const int g = h / (a.sel.heads_q / a.heads_kv);
   const int i0 = kFusedRows * chunk;
   const int ncols = min(nb, i0 + kFusedRows);  // block-causal: columns j <= i0 + 15
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
   const int r16 = lane % 16, kq = lane / 16;
   constexpr int KS = DG / 4;  // MFMA steps: this lane's features kq KS .. kq KS + KS - 1
 
@@ -721,23 +748,15 @@ __global__ __launch_bounds__(1024) void gate_fused_kernel(GateFusedArgs a) {
   const int M = i / 64 + 1;
   const float* L = sL + wave * LDL;
   float v[MAXM];
-  uint64_t valid = 0, forced = 0;
 #pragma unroll
   for (int m = 0; m < MAXM; ++m) {
     v[m] = -INFINITY;
-    if (m < M && i < nb) {
-      const int j = 64 * m + lane;
-      const bool ok = j <= i;
-      if (ok) v[m] = L[j];
-      valid |= (uint64_t)ok << m;
-      forced |= (uint64_t)(ok && ((a.sel.keep_first && j == 0) || (a.sel.keep_diag && j == i))) << m;
-    }
+    if (m < M && i < nb && 64 * m + lane <= i) v[m] = L[64 * m + lane];
   }
   __syncthreads();  // every row is in registers: the LDS now holds the histograms
   if (i >= nb) return;
-  const uint64_t sel = select_row<MAXM>(a.sel, v, valid, forced, i, h, reinterpret_cast<uint32_t*>(sL) + 256 * wave);
   const int64_t row = ((int64_t)b * a.sel.heads_q + h) * nb + i;
-  emit_row<MAXM>(sel, nb, row, a.sel.count, a.sel.idx, a.sel.dense);
+  select_emit<MAXM>(a.sel, v, i, h, row, reinterpret_cast<uint32_t*>(sL) + 256 * wave);
 }
 
 // Static scratch of seer_gate_noalloc: the projected rows Qg and Kg (the fused
@@ -790,8 +809,8 @@ hipError_t launch_gate_fused(const GateFusedArgs& a, hipStream_t s) {
 
 template <int MAXM>
 static hipError_t select_launch(const SelectArgs& a, hipStream_t s) {
-  const int64_t rows = (int64_t)a.batch * (a.group > 0 ? a.heads_q / a.group : a.heads_q) * a.n_blocks;
-  dim3 grid((unsigned)((rows + 3) / 4));
+  const dim3 grid((unsigned)((a.n_blocks + 3) / 4), (unsigned)(a.group > 0 ? a.heads_q / a.group : a.heads_q),
+                  (unsigned)a.batch);
   if (a.group > 0) hipLaunchKernelGGL((select_kernel<MAXM, true>), grid, dim3(256), 0, s, a);
   else hipLaunchKernelGGL((select_kernel<MAXM, false>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
@@ -816,7 +835,7 @@ hipError_t launch_select(const SelectArgs& a, hipStream_t s) {
 template <int MAXM>
 __global__ __launch_bounds__(256) void mask_from_dense_kernel(MaskFromDenseArgs a) {
   const int lane = threadIdx.x % kWave;
-  const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+  const int64_t row = (int64_t)blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   if (row >= a.rows) return;
   uint64_t sel = 0;
 #pragma unroll
