@@ -191,7 +191,10 @@ size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block);
  * seer_gate_desc).  Writes out->count, out->idx and, when non-NULL, out->dense.
  * logits_out (device float [B][Hq][nb][nb], or NULL) receives L for j <= i
  * (entries above the diagonal unspecified); when NULL, L lives in the
- * workspace between the logits kernel and the selection kernel.
+ * workspace between the logits kernel and the selection kernel, except for
+ * per-query-head masks of at most 128 blocks, where one kernel forms and
+ * selects the logits in on-chip memory (that part of the workspace then stays
+ * unused).
  * workspace: device memory of at least seer_gate_workspace_bytes(desc, gate,
  * logits_out == NULL) bytes, 256-byte aligned.
  * Unsupported: gate->block not in {64, 128}, head_dim not in {64, 128},

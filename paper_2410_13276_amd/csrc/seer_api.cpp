@@ -349,6 +349,9 @@ size_t seer_mask_idx_elems(const seer_attn_desc* desc, int32_t block) {
   return (size_t)desc->batch * desc->heads_q * nb * nb;
 }
 
+// Longest gate rows (in blocks) that seer_gate selects with the fused kernel.
+constexpr int kFusedGateMaxBlocks = 128;
+
 // The gate after argument checks.  fused: the logits are formed and selected
 // in one kernel (gate_fused_kernel) and never leave on-chip memory, so the
 // workspace holds only the projected rows; otherwise the logits kernel writes
@@ -445,7 +448,15 @@ seer_status seer_gate(const seer_attn_desc* desc, const seer_gate_desc* gate, co
   const GateLayout L = gate_layout(desc, gate, logits_out == nullptr);
   if (!workspace || workspace_bytes < L.total) return SEER_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
-  return gate_run(desc, gate, q, k, wq, wk, out, logits_out, workspace, false, static_cast<hipStream_t>(stream));
+  // Short rows take the fused score + select kernel, whose logits never leave
+  // LDS (16 rows per workgroup; at up to 128 blocks several workgroups share a
+  // CU).  Longer rows fill 64-128 KiB of LDS per workgroup, which leaves one
+  // workgroup per CU and no overlap of its MFMA and selection phases: measured
+  // gate 0.059 against 0.067 ms at 8192 tokens (32 query / 8 KV heads), but
+  // 0.173 against 0.143 ms at 32768 and 0.92 against 0.76 ms at 131072.
+  const bool fused = logits_out == nullptr && !gate->kv_shared && nb <= kFusedGateMaxBlocks &&
+                     seer::gate_fused_supported(nb, gate->gate_dim);
+  return gate_run(desc, gate, q, k, wq, wk, out, logits_out, workspace, fused, static_cast<hipStream_t>(stream));
 }
 
 seer_status seer_gate_noalloc(const seer_attn_desc* desc, const seer_gate_desc* gate, const void* q,
