@@ -22,7 +22,7 @@ pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 torch = pytest.importorskip("torch")
 seer = pytest.importorskip("paper_2410_13276_amd")
 
-ROWS = 48  # sampled query-block rows per workload
+ROWS = 256  # sampled query-block rows per workload (row-stratified)
 
 
 def _gate_kwargs(w):
