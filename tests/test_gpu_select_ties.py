@@ -10,8 +10,10 @@ drives the select kernel through its exact paths: rows whose cut falls inside a
 run of equal logits, all-equal rows (zero query weights), and buckets holding a
 single value; cut buckets of at most 64 candidates (resolved from the ranks of
 their gathered keys: hundreds of rows per case from 65 blocks up) and of more
-(resolved digit by digit: over a thousand rows in the 700- and 1100-block
-cases)."""
+(resolved by bisection over the keys: over a thousand rows in the 700- and
+1100-block cases).  Rows of up to 128 blocks are selected by the fused score +
+select kernel unless the caller asks for the logits; the `logits_out` runs
+take the logits and selection kernels on every case."""
 import numpy as np
 import pytest
 
@@ -53,9 +55,10 @@ CASES = [
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c[:6])))
 @pytest.mark.parametrize("sel", ["ratio", "fixed", "ratio_noforce", "zero_q"])
-def test_topk_with_exact_ties_matches_oracle(case, sel):
+@pytest.mark.parametrize("path", ["default", "logits_out"])
+def test_topk_with_exact_ties_matches_oracle(case, sel, path):
     B, Hq, Hkv, nb, D, Dg, (lo, hi) = case
-    print(f"[ties] {case} {sel}", flush=True)
+    print(f"[ties] {case} {sel} {path}", flush=True)
     rng = np.random.default_rng(stable_seed("ties", case, sel))
     q = _blockwise_integers(rng, B, Hq, nb, D, lo, hi)
     k = _blockwise_integers(rng, B, Hkv, nb, D, lo, hi)
@@ -67,8 +70,9 @@ def test_topk_with_exact_ties_matches_oracle(case, sel):
         mode, oargs, gargs = oracle.TOPK_RATIO, dict(rho=0.3), dict(mode=seer.TOPK_RATIO, topk_ratio=0.3)
     _, ell = oracle.gate(q, k, wq, wk, 64, True)
     orc = oracle.select(ell, mode, **oargs, keep_first=keep, keep_diag=keep)
+    logits = torch.empty((B, Hq, nb, nb), dtype=torch.float32, device="cuda") if path == "logits_out" else None
     mask = seer.gate(to_device(q), to_device(k), torch.from_numpy(wq).cuda(), torch.from_numpy(wk).cuda(),
-                     **gargs, keep_first=keep, keep_diag=keep, dense_out=True)
+                     **gargs, keep_first=keep, keep_diag=keep, dense_out=True, logits_out=logits)
     torch.cuda.synchronize()
     count, idx, dense = gpu_mask_numpy(mask)
     np.testing.assert_array_equal(count, orc["count"])
