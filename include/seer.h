@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SEER_ABI_VERSION 3
+#define SEER_ABI_VERSION 4
 #define SEER_BLOCK 64 /* the attention tile edge and the default gate block (section 4); gate
                         blocks and masks of 128 tokens are the other size the paper names */
 
@@ -147,6 +147,12 @@ typedef struct {
                                0: 2048; < 0: never */
   int32_t batch_wgs;        /* workgroups per such batch (rounded down to a multiple of 8);
                                0: as many as the GPU holds at once */
+  int32_t walk_classes;     /* sparse rows of 64-token masks (unsplit, at most 2048 entries)
+                               visit their blocks j = S q + c in the order (c, q): one column
+                               order common to every row, which keeps the rows running at once
+                               on K/V tiles near each other even where a mask selects runs of
+                               adjacent blocks.  S = walk_classes: 1 (ascending), 2, 4, 8 or 16;
+                               0: 4.  Changes only the order in which a row's tiles are summed */
 } seer_attn_opts;
 
 /* Options of seer_gate_distill (NULL or zero fields: defaults). */

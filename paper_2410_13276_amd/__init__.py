@@ -46,7 +46,7 @@ class GateDesc(C.Structure):
 class AttnOpts(C.Structure):
     """seer_attn_opts: launch options of the attention calls (zero fields: defaults)."""
     _fields_ = [("split", C.c_int32), ("split_width", C.c_int32), ("heads_per_wg", C.c_int32),
-                ("batch_min_blocks", C.c_int32), ("batch_wgs", C.c_int32)]
+                ("batch_min_blocks", C.c_int32), ("batch_wgs", C.c_int32), ("walk_classes", C.c_int32)]
 
 
 class DistillOpts(C.Structure):

@@ -489,6 +489,9 @@ __device__ __forceinline__ void load_tile_lds_clamped(uint32_t lds, const uint16
 // loop issues no vector-memory loads of its own (whose waits would also drain
 // the tile loads in flight).
 constexpr int kListChunk = 256;
+// Unsplit sparse rows hold up to this many list entries in LDS at once (a whole
+// row of a 131072-token mask), so that a row can be walked in another order.
+constexpr int kListWhole = 2048;
 
 // Two workgroups' worth of wavefronts per SIMD (<= 256 registers per lane) so
 // that one wavefront's softmax overlaps another's MFMA work.
@@ -534,7 +537,9 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   __shared__ __attribute__((aligned(16))) uint16_t sKV[2 * Lay::TILE];
   uint16_t* const sK = sKV;
   uint16_t* const sV = sKV + Lay::TILE;
-  __shared__ uint16_t sList[SPARSE ? kListChunk : 1];
+  constexpr int kWin = SPLIT ? kListChunk : kListWhole;  // entries of the LDS list window
+  __shared__ uint16_t sList[SPARSE ? kWin : 1];
+  __shared__ int sListN;  // entries of a row walked by residue classes
   __shared__ __attribute__((aligned(16))) float sL2[SPARSE ? 1 : 64 * NH];
   __shared__ int sLast;    // SPLIT: this task completed its row
   __shared__ int sTicket;  // SPLIT: the workgroup's next ticket of its queue
@@ -647,24 +652,77 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   const bool pool = !SPARSE && !SPLIT && a.gt != nullptr;  // ground-truth mode
   const int64_t trow = ((int64_t)t.b * a.heads_q + hq) * a.n_blocks + t.i;  // this wavefront's head
   float* const rrow = pool ? a.pool_r + trow * a.n_blocks * 64 : nullptr;
-  auto fetch_chunk = [&](int base) {  // mask entries [base, base + kListChunk) of the row
+  auto fetch_chunk = [&](int base) {  // mask entries [base, base + kWin) of the row, ascending
     if (SPARSE) {
       const int ne = list.n >> list.sh;
-      for (int p = tid; p < kListChunk; p += 128 * NH)
+#pragma unroll
+      for (int p = tid; p < kWin; p += 128 * NH)
         if (base + p < ne) sList[p] = list.idx[base + p];
     }
   };
   // last valid key block: j <= i when causal, j < nb always (i < nb); a dense
   // list is valid by construction
   const int jmax = a.causal ? t.i : a.n_blocks - 1;
+  // Walk by residue classes (a.walk_classes = S > 1; unsplit rows of 64-token
+  // masks held whole in LDS): the row visits its blocks j = S q + c in the order
+  // (c, q), i.e. every row follows one common column order, in which runs of
+  // adjacent blocks are spread apart.  Wavefront 0 partitions the ascending
+  // list into the S classes, stable within each class (ballot ranks: the order,
+  // and so every result, is deterministic); entries past jmax, the ascending
+  // list's tail, are dropped.
+  const int wcls = (SPARSE && !SPLIT && list.sh == 0 && list.n <= kWin && a.walk_classes > 1) ? a.walk_classes : 1;
+  auto fetch_classes = [&]() {
+    if (wave_all == 0) {
+      const uint64_t lt = lanemask_lt();
+      const int msk = wcls - 1;
+      int cnt[16];
+#pragma unroll
+      for (int c = 0; c < 16; ++c) cnt[c] = 0;
+      for (int k0 = 0; k0 < list.n; k0 += 64) {
+        const int e = k0 + lane;
+        const int v = e < list.n ? (int)list.idx[e] : 0;
+        const bool ok = e < list.n && v <= jmax;
+        const int cl = v & msk;
+#pragma unroll
+        for (int c = 0; c < 16; ++c)
+          if (c < wcls) cnt[c] += __popcll(__ballot(ok && cl == c));
+      }
+      int run = 0;
+#pragma unroll
+      for (int c = 0; c < 16; ++c) {
+        const int t0 = cnt[c];
+        cnt[c] = run;  // first walk position of class c
+        if (c < wcls) run += t0;
+      }
+      for (int k0 = 0; k0 < list.n; k0 += 64) {
+        const int e = k0 + lane;
+        const int v = e < list.n ? (int)list.idx[e] : 0;
+        const bool ok = e < list.n && v <= jmax;
+        const int cl = v & msk;
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+          if (c < wcls) {
+            const uint64_t bal = __ballot(ok && cl == c);
+            if (ok && cl == c) sList[cnt[c] + __popcll(bal & lt)] = (uint16_t)v;
+            cnt[c] += __popcll(bal);
+          }
+        }
+      }
+      if (lane == 0) sListN = run;
+    }
+  };
+  if (!pre) {
+    if (wcls > 1) fetch_classes();
+    else fetch_chunk(0);
+  }
+  __syncthreads();
+  const int list_n = wcls > 1 ? sListN : list.n;  // tiles this row walks
   auto entry = [&](int p) -> int {  // p must lie in the current LDS window
-    if (p >= list.n) return -1;
+    if (p >= list_n) return -1;
     if (!SPARSE) return list.lo + p;
-    const int jj = ((int)sList[(p >> list.sh) % kListChunk] << list.sh) + (p & list.sh);
+    const int jj = ((int)sList[(p >> list.sh) % kWin] << list.sh) + (p & list.sh);
     return jj <= jmax ? jj : -1;
   };
-  if (!pre) fetch_chunk(0);
-  __syncthreads();
   int j = entry(0);
   int jn = (j >= 0) ? entry(1) : -1;
   int n = 0;
@@ -766,7 +824,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
   auto tile = [&](f32x16 (&sc)[2], f32x16 (&sn)[2]) {
     int jnn = -1;
     if (jn >= 0) {
-      if (SPARSE && ((n + 2) & ((kListChunk << list.sh) - 1)) == 0 && n + 2 < list.n) {
+      if (SPARSE && ((n + 2) & ((kWin << list.sh) - 1)) == 0 && n + 2 < list_n) {
         fetch_chunk((n + 2) >> list.sh);  // every thread has read entry n + 1 already
         wait_loads();
         __syncthreads();

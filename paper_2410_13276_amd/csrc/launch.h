@@ -112,6 +112,8 @@ struct AttnArgs {
   int heads_per_wg;             // cap on query heads per workgroup for shared rows (1, 2, 4)
   int batch_min_blocks;         // batched launches of sparse rows from this many blocks (0: never)
   int batch_wgs;                // workgroups per batch (0: the resident capacity)
+  int walk_classes;             // unsplit sparse rows walk their blocks by residue classes
+                                // mod this (a power of two up to 16; 1: ascending)
   float* part_lse;              // [slots][64] log2-domain log-sum-exp of each partial
   uint16_t* part_o;             // [slots][64][D] bf16 partial outputs, normalised
 };

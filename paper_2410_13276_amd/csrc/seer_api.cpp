@@ -259,6 +259,7 @@ seer::AttnArgs attn_args(const seer_attn_desc* desc, int32_t causal, float sm_sc
   a.heads_per_wg = 2;
   a.batch_min_blocks = 2048;
   a.batch_wgs = 0;
+  a.walk_classes = 4;  // measured: 131072 tokens 17.1 -> 14.4-14.7 ms, 65536 (GQA 7:1) 7.56 -> 7.25 ms
   a.part_lse = nullptr;
   a.part_o = nullptr;
   return a;
@@ -302,12 +303,14 @@ void apply_opts(seer::AttnArgs& a, const seer_attn_opts* o) {
   if (o->batch_min_blocks < 0) a.batch_min_blocks = 0;
   else if (o->batch_min_blocks > 0) a.batch_min_blocks = o->batch_min_blocks;
   if (o->batch_wgs > 0) a.batch_wgs = o->batch_wgs;
+  if (o->walk_classes > 0) a.walk_classes = o->walk_classes;
 }
 
 seer_status check_opts(const seer_attn_opts* o) {
   if (!o) return SEER_OK;
   if ((o->split != 0 && o->split != 1) || (o->heads_per_wg > 0 && o->heads_per_wg != 1 && o->heads_per_wg != 2 &&
-                                           o->heads_per_wg != 4))
+                                           o->heads_per_wg != 4) ||
+      o->walk_classes < 0 || o->walk_classes > 16 || (o->walk_classes & (o->walk_classes - 1)) != 0)
     return SEER_ERR_INVALID_ARG;
   return SEER_OK;
 }

@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert seer.abi_version() == 3
+    assert seer.abi_version() == 4
     assert seer.status_str(0) == "SEER_OK"
     assert seer.status_str(3) == "SEER_ERR_WORKSPACE"
     assert seer.status_str(99) == "SEER_ERR_UNKNOWN"
@@ -291,9 +291,10 @@ def test_attention_ws_rejects_bad_args():
     args = (FAKE, FAKE, FAKE, FAKE, None)
     assert L.seer_bsattn_ws(C.byref(d), 64, None, 1, 0.0, *args, FAKE * 16, 1 << 30, None, None) == \
         seer.ERR_INVALID_ARG
-    bad = seer.AttnOpts(heads_per_wg=3)
-    assert L.seer_bsattn_ws(C.byref(d), 64, C.byref(m), 1, 0.0, *args, None, 0, C.byref(bad), None) == \
-        seer.ERR_INVALID_ARG
+    for bad in (seer.AttnOpts(heads_per_wg=3), seer.AttnOpts(walk_classes=3), seer.AttnOpts(walk_classes=32),
+                seer.AttnOpts(walk_classes=-1)):
+        assert L.seer_bsattn_ws(C.byref(d), 64, C.byref(m), 1, 0.0, *args, None, 0, C.byref(bad), None) == \
+            seer.ERR_INVALID_ARG
     assert L.seer_bsattn_ws(C.byref(d), 64, C.byref(m), 1, 0.0, *args, FAKE * 16 + 8, 1 << 30, None, None) == \
         seer.ERR_INVALID_ARG                                               # misaligned workspace
     assert L.seer_dense_attn_ws(C.byref(d), 1, float("inf"), *args, FAKE * 16, 1 << 30, None, None) == \

@@ -102,7 +102,8 @@ def test_bsattn_block128_parity(case, pattern):
 
 def test_block128_equals_expanded_64_mask():
     """A 128-token mask and its expansion to 64-token blocks give the same tiles,
-    hence bit-identical outputs."""
+    hence bit-identical outputs when both rows walk their tiles in ascending
+    order (128-token rows always do; 64-token rows are asked to)."""
     B, Hq, Hkv, S, D = 1, 4, 2, 2048, 128
     nb = S // BLK
     w, q, k, v, _, _ = small_inputs(B, Hq, Hkv, S, D, "bf16", seed=stable_seed("b128exp"))
@@ -111,16 +112,17 @@ def test_block128_equals_expanded_64_mask():
     om64 = np.kron(om, np.ones((2, 2), np.uint8)) & np.tril(np.ones((2 * nb, 2 * nb), np.uint8))
     qd, kd, vd = (to_device(x) for x in (q, k, v))
     o128, l128 = seer.bsattn(qd, kd, vd, upload_mask(*lists_from_dense(om), block=BLK), want_lse=True)
-    o64, l64 = seer.bsattn(qd, kd, vd, upload_mask(*lists_from_dense(om64)), want_lse=True)
+    o64, l64 = seer.bsattn(qd, kd, vd, upload_mask(*lists_from_dense(om64)), want_lse=True,
+                           opts={"walk_classes": 1})
     torch.cuda.synchronize()
     assert torch.equal(o128.view(torch.int16), o64.view(torch.int16))
     assert torch.equal(l128, l64)
 
 
 def test_block128_long_rows_refill_the_list_window():
-    """Rows with more than 256 mask entries (512 tiles) cross the kernel's list
-    window: 33024 tokens (258 blocks of 128), every causal block active,
-    against the dense kernel in full and the oracle on sampled rows."""
+    """Long rows of a 128-token mask: 33024 tokens (258 blocks of 128, 516
+    tiles per row), every causal block active, against the dense kernel in full
+    (bit for bit: both walk ascending) and the oracle on sampled rows."""
     B, Hq, Hkv, S, D = 1, 1, 1, 33024, 64
     nb = S // BLK
     w, q, k, v, _, _ = small_inputs(B, Hq, Hkv, S, D, "bf16", seed=stable_seed("b128long"))
