@@ -146,8 +146,8 @@ __global__ __launch_bounds__(256) void loss_mean_kernel(const double* __restrict
 // next 16 MFMAs with four 16-byte reads: MFMA step s contracts k = s (lanes
 // 0-31) and k = 16 + s (lanes 32-63).  Operand tiles are read from global
 // memory along whichever index has unit stride, so that loads coalesce for
-// every layout used here.  blockIdx.z = z * splits + s: part s of the tile's
-// (k1, k2) chunks; with splits > 1 the part's product goes to g.part.
+// every layout used here.  A workgroup computes part s of its tile's (k1, k2)
+// chunks; with splits > 1 the part's product goes to g.part.
 constexpr int kT = 64;
 constexpr int kKc = 32;
 constexpr int kKp = kKc + 4;              // LDS row stride (floats)
@@ -155,12 +155,24 @@ constexpr int kLoads = kT * kKc / 256;  // elements of each operand per thread a
 static_assert(kT == kKlTile, "the logit gradient is written up to the end of each row's GEMM tile");
 static_assert(kT == 64 && kKc == 32 && kLoads == 8, "the element mapping of fetch and stash");
 
+// Tiles are dispatched heaviest first over the whole launch (a 1-D grid):
+// the row-tile index outermost, in the order of decreasing work for the
+// triangular products (tri 1: rows near the end contract the longest k range;
+// tri 2: rows near the start), then the batch index and split part, then the
+// column tile.  Launched batch by batch instead, each batch's heavy tiles
+// would come last and the final batches' would run alone at the end.
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
   __shared__ __attribute__((aligned(16))) float sA[2][kT][kKp];
   __shared__ __attribute__((aligned(16))) float sB[2][kT][kKp];
   const int t = threadIdx.x;
-  const int m0 = blockIdx.y * kT, n0 = blockIdx.x * kT;
-  const int z = blockIdx.z / splits, sp = blockIdx.z % splits;
+  const int ntn = (g.N + kT - 1) / kT, ntm = (g.M + kT - 1) / kT, nzs = g.Z * splits;
+  const int lin = blockIdx.x;
+  const int tn = lin % ntn;
+  const int zs = (lin / ntn) % nzs;
+  const int tq = lin / ntn / nzs;  // position in the row-tile order
+  const int tm = g.tri == 1 ? ntm - 1 - tq : tq;
+  const int m0 = tm * kT, n0 = tn * kT;
+  const int z = zs / splits, sp = zs % splits;
   const float* A = g.A + (int64_t)z * g.saz;
   const float* B = g.B + (int64_t)(z / g.bdiv) * g.sbz;
   const int wave = t / kWave, lane = t % kWave;
@@ -354,8 +366,9 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.Z <= 0) return hipSuccess;
   const int sp = gemm_splits(a);
   if (sp > 1 && a.part == nullptr) return hipErrorInvalidValue;
-  dim3 grid((a.N + kT - 1) / kT, (a.M + kT - 1) / kT, a.Z * sp);
-  hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, a, sp);
+  const int64_t tiles = (int64_t)((a.N + kT - 1) / kT) * ((a.M + kT - 1) / kT) * a.Z * sp;
+  if (tiles > INT32_MAX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gemm_f32_kernel, dim3((unsigned)tiles), dim3(256), 0, s, a, sp);
   if (sp > 1) {
     const int64_t n = (int64_t)a.Z * a.M * a.N;
     hipLaunchKernelGGL(gemm_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a, sp);
