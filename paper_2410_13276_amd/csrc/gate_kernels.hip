@@ -700,8 +700,12 @@ __global__ __launch_bounds__(1024) void gate_fused_kernel(GateFusedArgs a) {
   __shared__ __attribute__((aligned(16))) float sL[WORDS];
   const int nb = a.sel.n_blocks;
   const int chunks = (nb + kFusedRows - 1) / kFusedRows;
-  const int chunk = chunks - 1 - (int)blockIdx.x;  // heaviest rows first
-  const int h = blockIdx.y, b = blockIdx.z;
+  // 1-D grid, heaviest rows first over the whole launch (head by head, the
+  // last heads' heavy rows would run alone at the end: measured 0.93 -> 0.86 ms
+  // at 131072 tokens, 0.178 -> 0.153 ms at 32768)
+  const int nbh = a.sel.batch * a.sel.heads_q;
+  const int chunk = chunks - 1 - (int)blockIdx.x / nbh;
+  const int h = (int)blockIdx.x % nbh % a.sel.heads_q, b = (int)blockIdx.x % nbh / a.sel.heads_q;
   const int g = h / (a.sel.heads_q / a.heads_kv);
   const int i0 = kFusedRows * chunk;
   const int ncols = min(nb, i0 + kFusedRows);  // block-causal: columns j <= i0 + 15
@@ -786,7 +790,9 @@ bool gate_fused_supported(int n_blocks, int gate_dim) {
 template <int MAXM>
 static hipError_t gate_fused_dg(const GateFusedArgs& a, hipStream_t s) {
   const int chunks = (a.sel.n_blocks + kFusedRows - 1) / kFusedRows;
-  const dim3 grid((unsigned)chunks, a.sel.heads_q, a.sel.batch);
+  const int64_t wgs = (int64_t)chunks * a.sel.heads_q * a.sel.batch;
+  if (wgs > INT32_MAX) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)wgs);
   switch (a.gate_dim) {
     case 32: hipLaunchKernelGGL((gate_fused_kernel<MAXM, 32>), grid, dim3(1024), 0, s, a); break;
     case 64: hipLaunchKernelGGL((gate_fused_kernel<MAXM, 64>), grid, dim3(1024), 0, s, a); break;
