@@ -616,7 +616,7 @@ __device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v
 // GROUP: rows of a mask shared by a KV group (a separate instantiation, so the
 // per-head kernel keeps its register budget and occupancy).
 template <int MAXM, bool GROUP>
-__global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
+__device__ __forceinline__ void select_rows(const SelectArgs& a) {
   __shared__ __attribute__((aligned(16))) uint32_t s_hist[4][256];  // per-wavefront digit histogram
   const int lane = threadIdx.x % kWave;
   // the wavefront index is uniform: readfirstlane makes row, i and the word
@@ -672,6 +672,20 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
     for (int m = 0; m < MAXM; ++m) v[m] = (m < M && 64 * m + lane <= i) ? __logf(sc[m] * inv_g) : -INFINITY;
   }
   select_emit<MAXM>(a, v, i, h, row, s_hist[wv]);
+}
+
+template <int MAXM, bool GROUP>
+__global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
+  select_rows<MAXM, GROUP>(a);
+}
+
+// Rows of 1025 to 2048 blocks: the compiler's choice (132 VGPRs, three
+// wavefronts per SIMD) is held to 128 VGPRs for a fourth, at a spill of four
+// words per lane; measured at 131072 tokens: gate 0.80 -> 0.75-0.76 ms.  (The
+// shorter-row instantiations keep five wavefronts per SIMD without a hint.)
+template <bool GROUP>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void select_kernel_m32(SelectArgs a) {
+  select_rows<32, GROUP>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -817,8 +831,13 @@ template <int MAXM>
 static hipError_t select_launch(const SelectArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)((a.n_blocks + 3) / 4), (unsigned)(a.group > 0 ? a.heads_q / a.group : a.heads_q),
                   (unsigned)a.batch);
-  if (a.group > 0) hipLaunchKernelGGL((select_kernel<MAXM, true>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((select_kernel<MAXM, false>), grid, dim3(256), 0, s, a);
+  if constexpr (MAXM == 32) {
+    if (a.group > 0) hipLaunchKernelGGL((select_kernel_m32<true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((select_kernel_m32<false>), grid, dim3(256), 0, s, a);
+  } else {
+    if (a.group > 0) hipLaunchKernelGGL((select_kernel<MAXM, true>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((select_kernel<MAXM, false>), grid, dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
