@@ -670,9 +670,9 @@ def main() -> int:
                              "peak_at_measured_clock = 256 CUs x 4096 bf16 flop/clk x the median gfx clock "
                              "under load. traffic = bytes past L2 per launch (scaled rocprofv3 FETCH_SIZE + "
                              "WRITE_SIZE); traffic_tb_per_s = traffic / launch_avg_ms, against "
-                             "algorithmic_bytes_per_launch (Q, K, V read once, O written once): tiles of "
-                             "near-random masks are reused little in a 4 MB L2, so the launch streams K/V "
-                             "from the Infinity Cache"},
+                             "algorithmic_bytes_per_launch (Q, K, V read once, O written once): the "
+                             "active tiles request far more K/V than that (32 KiB each), and what the XCD "
+                             "L2s do not reuse comes from the Infinity Cache or HBM"},
     }
     log(f"[bench] step {ms_step:.3f} ms (gate {gate_ms:.3f} + attn {attn_ms:.3f}); "
         f"attn {attn_tflops:.1f} TF/s; dense {dense_ms:.2f} ms; speedup {speedup:.2f}x "
