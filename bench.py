@@ -185,7 +185,8 @@ def _timed(fn, runs, stream):
 def _gate_kernel_split(fn, runs):
     """Per-call device time of the gate's kernels by stage (torch.profiler): pool
     + linear (pool_proj_kernel) and score + select (the logits and selection
-    kernels).  None under rocprofv3 (one tracer at a time)."""
+    kernels, also given apart; the fused kernel counts as both).  None under
+    rocprofv3 (one tracer at a time)."""
     if _under_profiler():
         return None
     import torch
@@ -196,19 +197,31 @@ def _gate_kernel_split(fn, runs):
         for _ in range(runs):
             fn()
         torch.cuda.synchronize()
-    pool = score = 0.0
+    pool = logits = select = fused = 0.0
     for e in prof.key_averages():
         t = getattr(e, "device_time_total", None)
         if t is None:
             t = getattr(e, "cuda_time_total", 0.0)
         if "pool_proj_kernel" in e.key:
             pool += t
-        elif "gate_logits_kernel" in e.key or "select_kernel" in e.key or "gate_fused_kernel" in e.key:
-            score += t
+        elif "gate_logits_kernel" in e.key:
+            logits += t
+        elif "select_kernel" in e.key:
+            select += t
+        elif "gate_fused_kernel" in e.key:
+            fused += t
+    score = logits + select + fused
     if pool <= 0 and score <= 0:
         return None
-    return {"pool_linear_ms": round(pool / runs / 1e3, 4), "score_select_ms": round(score / runs / 1e3, 4),
-            "source": "torch.profiler kernel device times, per call"}
+    ms = lambda t: round(t / runs / 1e3, 4)
+    out = {"pool_linear_ms": ms(pool), "score_select_ms": ms(score)}
+    if fused > 0:
+        out["fused_score_select_ms"] = ms(fused)
+    else:
+        out["logits_ms"] = ms(logits)
+        out["select_ms"] = ms(select)
+    out["source"] = "torch.profiler kernel device times, per call"
+    return out
 
 
 def _gate_kwargs(w, seer):

@@ -168,10 +168,13 @@ int seer_abi_version(void);
 const char* seer_status_str(int status);
 
 /* Bytes of device workspace seer_gate needs for this shape (0 on invalid
- * arguments): the pooled-and-projected Q and K (fp32: (heads_q + heads_kv) nb
- * gate_dim floats per batch entry, 40 MiB for 32 + 8 heads of 2048 blocks at
- * gate_dim 128) and, when logits_in_workspace is set (seer_gate called with
- * logits_out NULL), the fp32 gate logits [batch][heads_q][nb][nb]. */
+ * arguments): the pooled-and-projected Q and K, (heads_q + heads_kv) nb
+ * gate_dim values per batch entry, held as three bf16 parts each for the
+ * logits kernel (6 bytes per value with nb rounded up to a multiple of 32;
+ * 60 MiB for 32 + 8 heads of 2048 blocks at gate_dim 128; the fused kernel of
+ * short rows keeps them as fp32 in the same region) and, when
+ * logits_in_workspace is set (seer_gate called with logits_out NULL), the fp32
+ * gate logits [batch][heads_q][nb][nb]. */
 size_t seer_gate_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate,
                                  int32_t logits_in_workspace);
 

@@ -7,7 +7,9 @@
 //                       GEMV reuses each weight element for every block of the
 //                       workgroup.
 //   gate_logits_kernel  Eq. 1: Qg Kg^T / sqrt(Dg) on the block-causal lower
-//                       triangle, fp32 MFMA (v_mfma_f32_32x32x2_f32), 128x128 tiles.
+//                       triangle, 128x128 tiles on bf16 MFMA
+//                       (v_mfma_f32_32x32x16_bf16) from Qg, Kg split in three
+//                       bf16 parts each (fp32-accurate products).
 //   select_kernel       Eq. 3 (TopK by an exact select: one pass over 256
 //                       equal-width value buckets, then, inside the target
 //                       bucket, ranks of its gathered keys (at most 64) or
@@ -56,6 +58,32 @@ struct Load16<uint16_t> {
   }
 };
 
+// x as the sum of three bf16 values hi + mid + lo (each rounded to nearest
+// even from what the previous parts leave; both differences are exact in fp32
+// because each part is within a factor of two of the remainder it rounds).
+// hi + mid + lo reproduces x to about 2^-27 relative, so products of the parts
+// summed in fp32 (the bf16 logits kernel) stay as accurate as an fp32 product.
+//
+// The parts are stored in the order the logits kernel's MFMA operands consume
+// them: per 32-row group rb, 16-feature step c and part p, one 1 KiB run of 64
+// lanes x 8 features, lane hf 32 + rl holding features 16c + 8hf .. +7 of row
+// 32 rb + rl, so that every operand load of a wavefront reads 1 KiB of
+// contiguous memory.  A head holds ceil(nb / 32) groups (split_rows(nb) rows).
+__host__ __device__ __forceinline__ int64_t split_index(int r, int f, int part, int dg) {
+  const int rb = r / 32, rl = r % 32, c = f / 16, hf = (f / 8) % 2, e = f % 8;
+  return ((((int64_t)rb * (dg / 16) + c) * 3 + part) * 64 + (hf * 32 + rl)) * 8 + e;
+}
+
+__device__ __forceinline__ void store_split(uint16_t* head, int r, int f, int dg, float x) {
+  const __bf16 hi = (__bf16)x;
+  const float r1 = x - (float)hi;
+  const __bf16 mid = (__bf16)r1;
+  const __bf16 lo = (__bf16)(r1 - (float)mid);
+  head[split_index(r, f, 0, dg)] = __builtin_bit_cast(uint16_t, hi);
+  head[split_index(r, f, 1, dg)] = __builtin_bit_cast(uint16_t, mid);
+  head[split_index(r, f, 2, dg)] = __builtin_bit_cast(uint16_t, lo);
+}
+
 // One workgroup of 256 threads pools R consecutive 64-token blocks of one head
 // (each thread owns one 16-byte column chunk of one block and walks its 64 rows)
 // and then projects the R pooled rows through the head's gate weights.
@@ -64,7 +92,7 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
                                                const float* __restrict__ W,
                                                float* __restrict__ out, float* smem,
                                                float* srot, double rope_base,
-                                               float* __restrict__ pooled_out) {
+                                               float* __restrict__ pooled_out, uint16_t* __restrict__ split) {
   constexpr int EPL = Load16<T>::N;  // elements per 16-byte load
   constexpr int TPR = D / EPL;       // threads per block row
   constexpr int R = 256 / TPR;       // blocks per workgroup
@@ -147,31 +175,32 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
       acc[q] = fmaf(p[3], w[3], acc[q]);
     }
   }
-  if (rope_base <= 0.0) {
+  if (rope_base > 0.0) {
+    // Block-level RoPE (section 3.1): rotate plane (d, d + DG/2) of the row of
+    // block bb by angle bb * base^(-2d/DG); the angle is formed in double.
+#pragma unroll
+    for (int q = 0; q < RPT; ++q) srot[(r0 + q * RSTEP) * DG + j] = acc[q];
+    __syncthreads();
+    constexpr int HALF = DG / 2;
+    const int d = j % HALF;
+    const double w = pow(rope_base, -2.0 * d / DG);
 #pragma unroll
     for (int q = 0; q < RPT; ++q) {
-      const int bb = blockIdx.x * R + r0 + q * RSTEP;
-      if (bb < nb) out[(int64_t)bb * DG + j] = acc[q];
+      const int rr = r0 + q * RSTEP;
+      const int bb = blockIdx.x * R + rr;
+      const double ang = (double)bb * w;
+      const float cs = (float)cos(ang), sn = (float)sin(ang);
+      const float a = srot[rr * DG + d], b = srot[rr * DG + d + HALF];
+      acc[q] = (j < HALF) ? (a * cs - b * sn) : (a * sn + b * cs);
     }
-    return;
   }
-  // Block-level RoPE (section 3.1): rotate plane (d, d + DG/2) of the row of
-  // block bb by angle bb * base^(-2d/DG); the angle is formed in double.
-#pragma unroll
-  for (int q = 0; q < RPT; ++q) srot[(r0 + q * RSTEP) * DG + j] = acc[q];
-  __syncthreads();
-  constexpr int HALF = DG / 2;
-  const int d = j % HALF;
-  const double w = pow(rope_base, -2.0 * d / DG);
 #pragma unroll
   for (int q = 0; q < RPT; ++q) {
-    const int rr = r0 + q * RSTEP;
-    const int bb = blockIdx.x * R + rr;
-    const double ang = (double)bb * w;
-    const float cs = (float)cos(ang), sn = (float)sin(ang);
-    const float a = srot[rr * DG + d], b = srot[rr * DG + d + HALF];
-    const float y = (j < HALF) ? (a * cs - b * sn) : (a * sn + b * cs);
-    if (bb < nb) out[(int64_t)bb * DG + j] = y;
+    const int bb = blockIdx.x * R + r0 + q * RSTEP;
+    if (bb < nb) {
+      if (out) out[(int64_t)bb * DG + j] = acc[q];
+      if (split) store_split(split, bb, j, DG, acc[q]);
+    }
   }
 }
 
@@ -186,17 +215,19 @@ __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
   if (slot < a.heads_q) {
     const int h = slot;
     const T* x = static_cast<const T*>(a.q.ptr) + b * a.q.sb + h * a.q.sh;
-    float* out = a.qg + ((int64_t)b * a.heads_q + h) * a.n_blocks * DG;
+    float* out = a.qg ? a.qg + ((int64_t)b * a.heads_q + h) * a.n_blocks * DG : nullptr;
     float* po = a.qp ? a.qp + ((int64_t)b * a.heads_q + h) * a.n_blocks * D : nullptr;
+    uint16_t* sp = a.qs ? a.qs + ((int64_t)b * a.heads_q + h) * split_rows(a.n_blocks) * 3 * DG : nullptr;
     pool_proj_head<T, D, DG, false, BLK>(x, a.q.ss, a.n_blocks, a.seq_len, a.wq + h * a.wq_head_stride, out, smem, srot,
-                                    a.rope_base, po);
+                                    a.rope_base, po, sp);
   } else {
     const int g = slot - a.heads_q;
     const T* x = static_cast<const T*>(a.k.ptr) + b * a.k.sb + g * a.k.sh;
-    float* out = a.kg + ((int64_t)b * a.heads_kv + g) * a.n_blocks * DG;
+    float* out = a.kg ? a.kg + ((int64_t)b * a.heads_kv + g) * a.n_blocks * DG : nullptr;
     float* po = a.kp ? a.kp + ((int64_t)b * a.heads_kv + g) * a.n_blocks * 3 * D : nullptr;
+    uint16_t* sp = a.ks ? a.ks + ((int64_t)b * a.heads_kv + g) * split_rows(a.n_blocks) * 3 * DG : nullptr;
     pool_proj_head<T, D, DG, true, BLK>(x, a.k.ss, a.n_blocks, a.seq_len, a.wk + g * a.wk_head_stride, out, smem, srot,
-                                   a.rope_base, po);
+                                   a.rope_base, po, sp);
   }
 }
 
@@ -236,14 +267,20 @@ hipError_t launch_pool_proj(const PoolProjArgs& a, hipStream_t s) {
 // ---------------------------------------------------------------------------
 
 // Each of the 4 wavefronts computes a 64x64 sub-tile of a 128x128 tile as 2x2
-// blocks of 32x32 with v_mfma_f32_32x32x2_f32 (each operand row read from L2
-// serves two blocks).  Operand lanes: A (rows i of Qg) and B (rows j of Kg)
-// both hold, in lane half hf = lane/32 and MFMA step v of group u, the gate
-// feature 8u + 4hf + v, so the contraction pairs identical features.  Output
-// lane holds column j = lane%32 and rows 8*(e/4) + 4*hf + e%4 of a 32x32 block
-// (e = accumulator index).  Blocks entirely above the diagonal are skipped.
-// Loading one feature group ahead took the gate from 0.837 to 0.808 ms at
-// 131072 tokens (32 heads, Dg 128).
+// blocks of 32x32 on bf16 MFMA (v_mfma_f32_32x32x16_bf16), from Qg and Kg held
+// as three bf16 parts each (store_split): of the nine part products the six
+// down to 2^-18 of the leading one (hi.hi, hi.mid, mid.hi, hi.lo, lo.hi,
+// mid.mid) are summed in fp32, which keeps the logits as accurate as fp32
+// products (the dropped ones and the split's remainder lie near 2^-26 of it) at 6 bf16 MFMAs (192
+// cycles) per 32x32x16 step instead of 8 fp32 MFMAs (512 cycles).  Operand
+// lanes: A (rows i of Qg) and B (rows j of Kg) both hold, in lane half hf =
+// lane/32 and feature step c, the gate features 16c + 8hf .. +7, so the
+// contraction pairs identical features (the parts are stored in exactly this
+// lane order, split_index).  Output lane holds column j = lane%32 and rows
+// 8*(e/4) + 4*hf + e%4 of a 32x32 block (e = accumulator index).  Blocks
+// entirely above the diagonal are skipped.  The next feature step's operands
+// load while the current one multiplies (two steps in flight measured no
+// faster).
 template <int DG>
 __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
   const int nb = a.n_blocks;
@@ -266,14 +303,18 @@ __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
   if (i0 >= nb || j0 >= nb) return;
   const bool diag = I == J && wi == wj;  // block (0, 1) of this sub-tile lies above the diagonal
   const int hf = lane / 32;
-  const float* qbase = a.qg + ((int64_t)b * a.heads_q + h) * nb * DG + 4 * hf;
-  const float* kbase = a.kg + ((int64_t)b * a.heads_kv + g) * nb * DG + 4 * hf;
-  const float* qrow[2];
-  const float* krow[2];
+  // operand runs (split_index): row group rb, step c, part p at
+  // ((rb DG/16 + c) 3 + p) 512 elements; groups past the last hold only rows
+  // past nb, whose logits are never stored, so a clamped group serves them
+  const int nrb = split_rows(nb) / 32;
+  const uint16_t* qhead = a.qs + ((int64_t)b * a.heads_q + h) * split_rows(nb) * 3 * DG + 8 * lane;
+  const uint16_t* khead = a.ks + ((int64_t)b * a.heads_kv + g) * split_rows(nb) * 3 * DG + 8 * lane;
+  const uint16_t* qrow[2];
+  const uint16_t* krow[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
-    qrow[s] = qbase + (int64_t)min(i0 + 32 * s + lane % 32, nb - 1) * DG;
-    krow[s] = kbase + (int64_t)min(j0 + 32 * s + lane % 32, nb - 1) * DG;
+    qrow[s] = qhead + (int64_t)min(i0 / 32 + s, nrb - 1) * (DG / 16) * 3 * 512;
+    krow[s] = khead + (int64_t)min(j0 / 32 + s, nrb - 1) * (DG / 16) * 3 * 512;
   }
 
   f32x16 acc[2][2];
@@ -283,36 +324,40 @@ __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
     for (int c = 0; c < 2; ++c)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[r][c][e] = 0.f;
-  // operands of the next feature group load while the current one multiplies
-  f32x4 qn[2], kn[2];
+  // operands of feature step c: part p of row block s
+  bf16x8 qn[2][3], kn[2][3];
+  auto load = [&](int c, bf16x8 (&qo)[2][3], bf16x8 (&ko)[2][3]) {
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    qn[s] = *reinterpret_cast<const f32x4*>(qrow[s]);
-    kn[s] = *reinterpret_cast<const f32x4*>(krow[s]);
-  }
-#pragma unroll 2
-  for (int u = 0; u < DG / 8; ++u) {
-    f32x4 qa[2], kb[2];
+    for (int s = 0; s < 2; ++s)
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      qa[s] = qn[s];
-      kb[s] = kn[s];
-    }
-    if (u + 1 < DG / 8) {
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        qn[s] = *reinterpret_cast<const f32x4*>(qrow[s] + 8 * (u + 1));
-        kn[s] = *reinterpret_cast<const f32x4*>(krow[s] + 8 * (u + 1));
+      for (int p = 0; p < 3; ++p) {
+        qo[s][p] = *reinterpret_cast<const bf16x8*>(qrow[s] + (3 * c + p) * 512);
+        ko[s][p] = *reinterpret_cast<const bf16x8*>(krow[s] + (3 * c + p) * 512);
       }
-    }
+  };
+  load(0, qn, kn);
+  // part pairs (Q part, K part) in the order they are summed
+  constexpr int PQ[6] = {0, 0, 1, 0, 2, 1};
+  constexpr int PK[6] = {0, 1, 0, 2, 0, 1};
 #pragma unroll
-    for (int v = 0; v < 4; ++v)
+  for (int c = 0; c < DG / 16; ++c) {
+    bf16x8 qa[2][3], kb[2][3];
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int p = 0; p < 3; ++p) {
+        qa[s][p] = qn[s][p];
+        kb[s][p] = kn[s][p];
+      }
+    if (c + 1 < DG / 16) load(c + 1, qn, kn);
+#pragma unroll
+    for (int t = 0; t < 6; ++t)
 #pragma unroll
       for (int r = 0; r < 2; ++r)
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
-          if (!(diag && c > r))
-            acc[r][c] = __builtin_amdgcn_mfma_f32_32x32x2f32(qa[r][v], kb[c][v], acc[r][c], 0, 0, 0);
+        for (int cc = 0; cc < 2; ++cc)
+          if (!(diag && cc > r))
+            acc[r][cc] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[r][PQ[t]], kb[cc][PK[t]], acc[r][cc], 0, 0, 0);
   }
   float* out = a.logits + ((int64_t)b * a.heads_q + h) * nb * nb;
 #pragma unroll
@@ -366,15 +411,15 @@ __device__ __forceinline__ void emit_row(uint64_t sel, int nb, int64_t row, int3
   if (lane == 0) count[row] = base;
 }
 
-// A copy of a wave-uniform int that the compiler cannot merge with other uses
-// of the same value.  The word loops below each compare it with their
-// constant word index: merged across loops, those per-word conditions would
-// stay live as 64-bit lane masks for the whole selection and spill.
 // A wave-uniform float (equal in every lane) as a scalar.
 __device__ __forceinline__ float uniform_f(float x) {
   return __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(x)));
 }
 
+// A copy of a wave-uniform int that the compiler cannot merge with other uses
+// of the same value.  The word loops below each compare it with their
+// constant word index: merged across loops, those per-word conditions would
+// stay live as 64-bit lane masks for the whole selection and spill.
 __device__ __forceinline__ int opaque_sgpr(int x) {
   asm volatile("" : "+s"(x));
   return x;
@@ -406,6 +451,10 @@ __device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v
   const uint64_t lt = lanemask_lt();
   const int f0 = a.keep_first ? 0 : -1;  // forced blocks (-1: none)
   const int f1 = a.keep_diag ? i : -1;
+  // Words 1 .. M-2 are full: every block in them is a causal candidate (the
+  // forced blocks lie in words 0 and M-1, blocks past the diagonal only in
+  // M-1), so they take no per-block state tests; the two edge words do.
+  auto edge = [&](int m) { return m == 0 || m == opaque_sgpr(M) - 1; };
   // b[m]: -2 forced, -1 past the diagonal, otherwise a candidate (0; for TopK
   // its value bucket below).  All later tests read b, so no per-block
   // condition has to stay live across the passes.
@@ -414,8 +463,11 @@ __device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v
   for (int m = 0; m < MAXM; ++m) {
     b[m] = -1;
     if (m < opaque_sgpr(M)) {
-      const int j = 64 * m + lane;
-      b[m] = j > i ? -1 : (((j == f0) | (j == f1)) ? -2 : 0);
+      b[m] = 0;
+      if (edge(m)) {
+        const int j = 64 * m + lane;
+        b[m] = j > i ? -1 : (((j == f0) | (j == f1)) ? -2 : 0);
+      }
     }
   }
 
@@ -454,12 +506,16 @@ __device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v
     } else if (take <= 0) {
       bstar = 256;  // none
     } else {
+      // value range of the causal blocks (the forced ones included: a range
+      // that covers every candidate keeps the bucket index monotone); v is -inf
+      // past the diagonal, which only word M-1 holds
       float cmx = -INFINITY, cmn = INFINITY;
 #pragma unroll
       for (int m = 0; m < MAXM; ++m)
         if (m < opaque_sgpr(M)) {
-          cmx = fmaxf(cmx, b[m] == 0 ? v[m] : -INFINITY);
-          cmn = fminf(cmn, b[m] == 0 ? v[m] : INFINITY);
+          cmx = fmaxf(cmx, v[m]);
+          if (m == opaque_sgpr(M) - 1) cmn = fminf(cmn, 64 * m + lane <= i ? v[m] : INFINITY);
+          else cmn = fminf(cmn, v[m]);
         }
       cmx = uniform_f(wave_max(cmx));
       cmn = uniform_f(-wave_max(-cmn));
@@ -472,8 +528,13 @@ __device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v
       for (int m = 0; m < MAXM; ++m) {
         if (m < opaque_sgpr(M)) {
           const int bk = min(255, max(0, (int)((v[m] - cmn) * scale)));
-          b[m] = b[m] == 0 ? bk : b[m];
-          if (b[m] >= 0) atomicAdd(hist + b[m], 1u);
+          if (edge(m)) {
+            b[m] = b[m] == 0 ? bk : b[m];
+            if (b[m] >= 0) atomicAdd(hist + b[m], 1u);
+          } else {
+            b[m] = bk;
+            atomicAdd(hist + bk, 1u);
+          }
         }
       }
       __builtin_amdgcn_wave_barrier();
@@ -506,7 +567,8 @@ __device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v
         all_in = false;
         int gt = 0, ge = 0;  // bucket candidates with key > T, >= T
         if (cb <= kWave) {
-          // gather the bucket's keys one per lane, then T = the key of rank want
+          // gather the bucket's keys one per lane (words without one are
+          // skipped on their ballot), then T = the key of rank want
           __builtin_amdgcn_wave_barrier();
           int n = 0;
 #pragma unroll
@@ -514,8 +576,10 @@ __device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v
             if (m < opaque_sgpr(M)) {
               const bool in_b = b[m] == bstar;
               const uint64_t bal = __ballot(in_b);
-              if (in_b) hist[n + __popcll(bal & lt)] = ordered_key(v[m]);
-              n += __popcll(bal);
+              if (bal != 0) {
+                if (in_b) hist[n + __popcll(bal & lt)] = ordered_key(v[m]);
+                n += __popcll(bal);
+              }
             }
           }
           __builtin_amdgcn_wave_barrier();
@@ -569,12 +633,13 @@ __device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v
   // emit: ascending index list by ballot compaction.  The rule reduces to
   // compares against scalars: taken if forced, or bucket > bstar, or bucket ==
   // bstar and (the whole bucket is in, or key >= kcut, or tied at T with rank
-  // < need).
+  // < need).  The key tests run only in words that hold the cut bucket.
   const bool in_rule = !thr_mode && bstar >= 0 && bstar < 256;  // bucket bstar is split by keys
   const bool by_key = in_rule && !all_in;
   const bool tie = by_key && need >= 0;
   const uint32_t kcut = tie ? T + 1u : T;
   const bool key_in = !(tie && T == 0xFFFFFFFFu);  // (no key lies above the largest)
+  const int bmin = (in_rule && !by_key) ? bstar : bstar + 1;  // buckets taken whole
   uint16_t* const idx_row = a.idx + row * nb;
   uint8_t* const dense_row = a.dense ? a.dense + row * nb : nullptr;
   int base = 0, before = 0;
@@ -583,23 +648,23 @@ __device__ __forceinline__ void select_emit(const SelectArgs& a, const float (&v
     const int j = 64 * m + lane;
     if (m < opaque_sgpr(M)) {
       const int bm = b[m];
-      bool s = bm == -2;
+      bool s;
       if (thr_mode) {
-        s = s | ((bm == 0) & (v[m] - lse > lthr));
+        s = (bm == -2) | ((bm == 0) & (v[m] - lse > lthr));
       } else {
-        s = s | (bm > bstar);
+        s = (bm == -2) | (bm >= bmin);
         if (by_key) {
-          const uint32_t key = ordered_key(v[m]);
           const bool in_b = bm == bstar;
-          s = s | (in_b & (key >= kcut) & key_in);
-          if (tie) {  // the smallest-index candidates tied at T
-            const bool eq = in_b & (key == T);
-            const uint64_t bal_eq = __ballot(eq);
-            s = s | (eq & (before + (int)__popcll(bal_eq & lt) < need));
-            before += __popcll(bal_eq);
+          if (__ballot(in_b) != 0) {
+            const uint32_t key = ordered_key(v[m]);
+            s = s | (in_b & (key >= kcut) & key_in);
+            if (tie) {  // the smallest-index candidates tied at T
+              const bool eq = in_b & (key == T);
+              const uint64_t bal_eq = __ballot(eq);
+              s = s | (eq & (before + (int)__popcll(bal_eq & lt) < need));
+              before += __popcll(bal_eq);
+            }
           }
-        } else if (in_rule) {
-          s = s | (bm == bstar);
         }
       }
       const uint64_t bal = __ballot(s);

@@ -12,6 +12,9 @@ struct TensorView {  // [batch][heads][seq][dim], element strides of (batch, hea
   int64_t sb, sh, ss;
 };
 
+// Rows of one head's split gate rows: nb rounded up to whole 32-row groups.
+__host__ __device__ __forceinline__ int split_rows(int nb) { return (nb + 31) / 32 * 32; }
+
 struct PoolProjArgs {
   TensorView q, k;
   int batch, heads_q, heads_kv, n_blocks, head_dim, gate_dim;
@@ -19,18 +22,23 @@ struct PoolProjArgs {
   const float* wq;
   const float* wk;
   int64_t wq_head_stride, wk_head_stride;  // 0 when one matrix is shared by all heads
-  float* qg;  // [B][Hq][nb][Dg]
-  float* kg;  // [B][Hkv][nb][Dg]
+  float* qg;  // [B][Hq][nb][Dg] (nullptr: not stored)
+  float* kg;  // [B][Hkv][nb][Dg] (nullptr: not stored)
   double rope_base;  // > 0: block-level RoPE with this base (model base / block)
   float* qp;  // optional pooled Q [B][Hq][nb][D] (nullptr: not stored)
   float* kp;  // optional pooled K [B][Hkv][nb][3D]
+  // optional split rows for the bf16 logits kernel: Qg, Kg as three bf16 parts
+  // (hi, mid, lo) per element, [B][H][split_rows(nb)][3][Dg] elements in the
+  // lane order of the kernel's MFMA operands (nullptr: not stored)
+  uint16_t* qs;
+  uint16_t* ks;
   int block;  // tokens per gate block: 64 or 128
   int seq_len;  // tokens; the last block holds seq_len - (n_blocks - 1) block of them
 };
 
 struct GateLogitsArgs {
-  const float* qg;
-  const float* kg;
+  const uint16_t* qs;  // Qg split in three bf16 parts (PoolProjArgs::qs)
+  const uint16_t* ks;  // Kg split in three bf16 parts (PoolProjArgs::ks)
   int batch, heads_q, heads_kv, n_blocks, gate_dim;
   float scale;   // 1/sqrt(Dg)
   float* logits; // [B][Hq][nb][nb]

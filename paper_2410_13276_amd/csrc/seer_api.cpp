@@ -84,16 +84,26 @@ seer_status check_gate(const seer_attn_desc* d, const seer_gate_desc* g) {
   return SEER_OK;
 }
 
+// Gate workspace: the projected rows Qg, Kg, then the logits when they live in
+// the workspace.  The rows are fp32 for the fused kernel, or three bf16 parts
+// per element for the logits kernel; one call uses one of the two forms, so
+// they share the region (split = false: the fp32 form only).
 struct GateLayout {
-  size_t qg, kg, logits, total;
+  size_t qg, kg, qs, ks, logits, total;
 };
 
-GateLayout gate_layout(const seer_attn_desc* d, const seer_gate_desc* g, bool logits_in_ws) {
+GateLayout gate_layout(const seer_attn_desc* d, const seer_gate_desc* g, bool logits_in_ws, bool split = true) {
   const size_t nb = (size_t)blocks_of(d->seq_len, g->block);
+  const size_t Dg = g->gate_dim;
+  const size_t ns = (size_t)seer::split_rows((int)nb);
   GateLayout L;
   L.qg = 0;
-  L.kg = round_up((size_t)d->batch * d->heads_q * nb * g->gate_dim * 4);
-  L.logits = L.kg + round_up((size_t)d->batch * d->heads_kv * nb * g->gate_dim * 4);
+  L.kg = round_up((size_t)d->batch * d->heads_q * nb * Dg * 4);
+  size_t rows_end = L.kg + round_up((size_t)d->batch * d->heads_kv * nb * Dg * 4);
+  L.qs = 0;
+  L.ks = round_up((size_t)d->batch * d->heads_q * ns * 3 * Dg * 2);
+  if (split) rows_end = std::max(rows_end, L.ks + round_up((size_t)d->batch * d->heads_kv * ns * 3 * Dg * 2));
+  L.logits = rows_end;
   L.total = L.logits + (logits_in_ws ? round_up((size_t)d->batch * d->heads_q * nb * nb * 4) : 0);
   return L;
 }
@@ -180,7 +190,7 @@ DistillGemms distill_gemms(int B, int Hq, int Hkv, int D, int Dg, int nb, bool p
 // their gradient), projected-row gradients, per-row losses, and the split
 // products of the backward GEMMs (run one after another, so one buffer).
 struct DistillLayout {
-  size_t qg, kg, qp, kp, logits, dqg, dkg, row_loss, part, total;
+  size_t qg, kg, qs, ks, qp, kp, logits, dqg, dkg, row_loss, part, total;
 };
 
 DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g, int min_chunks) {
@@ -195,6 +205,8 @@ DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g, i
   };
   L.qg = take(B * Hq * nb * Dg * 4);
   L.kg = take(B * Hkv * nb * Dg * 4);
+  L.qs = take(B * Hq * seer::split_rows((int)nb) * 3 * Dg * 2);
+  L.ks = take(B * Hkv * seer::split_rows((int)nb) * 3 * Dg * 2);
   L.qp = take(B * Hq * nb * D * 4);
   L.kp = take(B * Hkv * nb * 3 * D * 4);
   L.logits = take(B * Hq * nb * nb * 4);
@@ -365,10 +377,12 @@ static seer_status gate_run(const seer_attn_desc* desc, const seer_gate_desc* ga
   seer_status s;
   const int nb = blocks_of(desc->seq_len, gate->block);
   const bool logits_in_ws = logits_out == nullptr && !fused;
-  const GateLayout L = gate_layout(desc, gate, logits_in_ws);
+  const GateLayout L = gate_layout(desc, gate, logits_in_ws, !fused);
   char* ws = static_cast<char*>(workspace);
   float* qg = reinterpret_cast<float*>(ws + L.qg);
   float* kg = reinterpret_cast<float*>(ws + L.kg);
+  uint16_t* qs = fused ? nullptr : reinterpret_cast<uint16_t*>(ws + L.qs);
+  uint16_t* ks = fused ? nullptr : reinterpret_cast<uint16_t*>(ws + L.ks);
   float* logits = logits_in_ws ? reinterpret_cast<float*>(ws + L.logits) : logits_out;
   const int D = desc->head_dim, Dg = gate->gate_dim;
 
@@ -386,11 +400,14 @@ static seer_status gate_run(const seer_attn_desc* desc, const seer_gate_desc* ga
   pa.wk = wk;
   pa.wq_head_stride = gate->w_per_head ? (int64_t)D * Dg : 0;
   pa.wk_head_stride = gate->w_per_head ? (int64_t)3 * D * Dg : 0;
-  pa.qg = qg;
-  pa.kg = kg;
+  // the fused kernel reads the fp32 rows, the logits kernel only their parts
+  pa.qg = fused ? qg : nullptr;
+  pa.kg = fused ? kg : nullptr;
   pa.rope_base = gate->rope_theta > 0.0 ? gate->rope_theta / gate->block : 0.0;
   pa.qp = nullptr;
   pa.kp = nullptr;
+  pa.qs = qs;
+  pa.ks = ks;
   pa.block = gate->block;
   pa.seq_len = desc->seq_len;
   if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
@@ -398,8 +415,8 @@ static seer_status gate_run(const seer_attn_desc* desc, const seer_gate_desc* ga
   const float scale = (float)(1.0 / std::sqrt((double)Dg));
   if (!fused) {
     seer::GateLogitsArgs la;
-    la.qg = qg;
-    la.kg = kg;
+    la.qs = qs;
+    la.ks = ks;
     la.batch = desc->batch;
     la.heads_q = desc->heads_q;
     la.heads_kv = desc->heads_kv;
@@ -472,7 +489,7 @@ seer_status seer_gate_noalloc(const seer_attn_desc* desc, const seer_gate_desc* 
   const int nb = blocks_of(desc->seq_len, gate->block);
   if (out->n_blocks != nb || out->kv_shared != gate->kv_shared) return SEER_ERR_INVALID_ARG;
   if (gate->kv_shared || !seer::gate_fused_supported(nb, gate->gate_dim)) return SEER_ERR_UNSUPPORTED;
-  const GateLayout L = gate_layout(desc, gate, false);
+  const GateLayout L = gate_layout(desc, gate, false, false);
   if (L.total > seer::kGateScratchBytes) return SEER_ERR_WORKSPACE;  // beyond the static scratch
   void* scratch = seer::gate_scratch();
   if (!scratch) return SEER_ERR_HIP;
@@ -677,6 +694,8 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   char* ws = static_cast<char*>(workspace);
   float* qg = reinterpret_cast<float*>(ws + W.qg);
   float* kg = reinterpret_cast<float*>(ws + W.kg);
+  uint16_t* qs = reinterpret_cast<uint16_t*>(ws + W.qs);
+  uint16_t* ks = reinterpret_cast<uint16_t*>(ws + W.ks);
   float* qp = reinterpret_cast<float*>(ws + W.qp);
   float* kp = reinterpret_cast<float*>(ws + W.kp);
   float* dl = reinterpret_cast<float*>(ws + W.logits);
@@ -710,13 +729,15 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   pa.rope_base = rope_base;
   pa.qp = qp;
   pa.kp = kp;
+  pa.qs = qs;
+  pa.ks = ks;
   pa.block = gate->block;
   pa.seq_len = desc->seq_len;
   if ((s = from_hip(seer::launch_pool_proj(pa, st))) != SEER_OK) return s;
 
   seer::GateLogitsArgs la;
-  la.qg = qg;
-  la.kg = kg;
+  la.qs = qs;
+  la.ks = ks;
   la.batch = B;
   la.heads_q = Hq;
   la.heads_kv = Hkv;

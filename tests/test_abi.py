@@ -65,12 +65,19 @@ def _call_gate(d, g, ws_bytes=1 << 40, mask_nb=None, q=FAKE, ws=FAKE * 16):
     return L.seer_gate(C.byref(d), C.byref(g), q, FAKE, FAKE, FAKE, C.byref(m), None, ws, ws_bytes, None)
 
 
+def _sr(nb):
+    """Rows of one head's split gate rows (whole 32-row groups)."""
+    return -(-nb // 32) * 32
+
+
 def test_workspace_size_formula():
     d, g = _desc(B=2, Hq=4, Hkv=2, S=1024), _gate()
     L = seer.lib()
     nb = 16
     up = lambda x: (x + 255) // 256 * 256
-    want = up(2 * 4 * nb * 128 * 4) + up(2 * 2 * nb * 128 * 4)
+    # Qg, Kg as three bf16 parts per element (the logits kernel; the fp32 rows
+    # of the fused kernel share that region)
+    want = up(2 * 4 * _sr(nb) * 3 * 128 * 2) + up(2 * 2 * _sr(nb) * 3 * 128 * 2)
     assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 0) == want
     assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 1) == want + up(2 * 4 * nb * nb * 4)
     assert L.seer_gate_noalloc_max_bytes() == 64 << 20
@@ -176,8 +183,10 @@ def test_gate_distill_workspace_and_rejects_bad_args():
     L = seer.lib()
     d, g = _desc(B=1, Hq=4, Hkv=2, S=1024, D=128), _gate()
     nb, up = 16, (lambda x: (x + 255) // 256 * 256)
-    # Qg, Kg, Qp, Kp, logits, dQg, dKg, row losses + 64 partial sums; no product splits at this size
-    want = (up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up(4 * nb * 128 * 4) + up(2 * nb * 384 * 4)
+    # Qg, Kg, their bf16 parts, Qp, Kp, logits, dQg, dKg, row losses + 64 partial sums; no
+    # product splits at this size
+    want = (up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up(4 * _sr(nb) * 3 * 128 * 2) + up(2 * _sr(nb) * 3 * 128 * 2)
+            + up(4 * nb * 128 * 4) + up(2 * nb * 384 * 4)
             + up(4 * nb * nb * 4) + up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4) + up((4 * nb + 64) * 8))
     need = L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g), None)
     assert need == want
@@ -213,7 +222,8 @@ def test_gate_distill_workspace_split_products(min_chunks):
     B, Hq, Hkv, D, Dg, nb = 1, 32, 8, 128, 128, 512
     d, g = _desc(B=B, Hq=Hq, Hkv=Hkv, S=64 * nb, D=D), _gate()
     up = lambda x: (x + 255) // 256 * 256
-    base = (up(Hq * nb * Dg * 4) + up(Hkv * nb * Dg * 4) + up(Hq * nb * D * 4) + up(Hkv * nb * 3 * D * 4)
+    base = (up(Hq * nb * Dg * 4) + up(Hkv * nb * Dg * 4) + up(Hq * _sr(nb) * 3 * Dg * 2) + up(Hkv * _sr(nb) * 3 * Dg * 2)
+            + up(Hq * nb * D * 4) + up(Hkv * nb * 3 * D * 4)
             + up(Hq * nb * nb * 4) + up(Hq * nb * Dg * 4) + up(Hkv * nb * Dg * 4) + up((Hq * nb + 64) * 8))
     products = [(nb, Dg, 1, nb, Hq), (nb, Dg, Hq // Hkv, nb, Hkv), (D, Dg, 1, nb, Hq), (3 * D, Dg, 1, nb, Hkv)]
     part = 0
@@ -311,7 +321,7 @@ def test_block_128_gate_and_mask_validation():
     g = _gate(block=128)
     need = L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 1)
     up = lambda x: (x + 255) // 256 * 256
-    assert need == up(4 * 8 * 128 * 4) + up(2 * 8 * 128 * 4) + up(4 * 8 * 8 * 4)
+    assert need == up(4 * _sr(8) * 3 * 128 * 2) + up(2 * _sr(8) * 3 * 128 * 2) + up(4 * 8 * 8 * 4)
     m = seer.BlockMaskStruct()
     m.n_blocks, m.count, m.idx, m.dense = 16, FAKE, FAKE, None
     assert L.seer_mask_from_dense(C.byref(d), 128, FAKE, C.byref(m), None) == seer.ERR_INVALID_ARG
@@ -324,7 +334,8 @@ def test_partial_last_block_sizes():
     up = lambda x: (x + 255) // 256 * 256
     nb = 16  # ceil(1000 / 64)
     assert L.seer_mask_idx_elems(C.byref(d), 64) == 4 * nb * nb
-    assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 0) == up(4 * nb * 128 * 4) + up(2 * nb * 128 * 4)
+    assert L.seer_gate_workspace_bytes(C.byref(d), C.byref(g), 0) == (
+        up(4 * _sr(nb) * 3 * 128 * 2) + up(2 * _sr(nb) * 3 * 128 * 2))
     assert L.seer_attn_gt_workspace_bytes(C.byref(d), 64, 0) == 4 * nb * nb * 64 * 4
     assert _call_gate(d, g, mask_nb=15) == seer.ERR_INVALID_ARG
 
