@@ -744,12 +744,14 @@ __global__ __launch_bounds__(256) void select_kernel(SelectArgs a) {
   select_rows<MAXM, GROUP>(a);
 }
 
-// Rows of 1025 to 2048 blocks: the compiler's choice (132 VGPRs, three
-// wavefronts per SIMD) is held to 128 VGPRs for a fourth, at a spill of four
-// words per lane; measured at 131072 tokens: gate 0.80 -> 0.75-0.76 ms.  (The
-// shorter-row instantiations keep five wavefronts per SIMD without a hint.)
+// Rows of 1025 to 2048 blocks: the selection is latency bound (one wavefront
+// walks a row through dependent passes), so occupancy pays: held to 96 VGPRs
+// for a fifth wavefront per SIMD (the compiler's choice is 103, four), at a
+// spill of 11 words per lane.  Measured at 131072 tokens: selection 0.215-0.221
+// -> 0.190-0.193 ms; six wavefronts (80 VGPRs, 40 spilled) 0.189-0.190 ms.
+// (The shorter-row instantiations keep five wavefronts per SIMD without a hint.)
 template <bool GROUP>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void select_kernel_m32(SelectArgs a) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void select_kernel_m32(SelectArgs a) {
   select_rows<32, GROUP>(a);
 }
 
