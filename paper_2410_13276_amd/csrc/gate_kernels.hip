@@ -284,14 +284,30 @@ hipError_t launch_pool_proj(const PoolProjArgs& a, hipStream_t s) {
 template <int DG>
 __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
   const int nb = a.n_blocks;
+  // Workgroup -> (batch x head, tile): workgroups are dealt to the 8 XCDs in
+  // turn, so with a multiple of 8 (batch, head) pairs, pair p's tiles all go
+  // to XCD p % 8, which then holds one head's rows and its KV head's in its
+  // L2 at a time; otherwise the pairs follow each other.
+  const int T = (nb + 127) / 128;
+  const int tiles = T * (T + 1) / 2;
+  const int pairs = a.batch * a.heads_q;
+  const int wg = blockIdx.x;
+  int pair, x;
+  if (pairs % 8 == 0) {
+    const int k = wg / 8;
+    pair = (k / tiles) * 8 + wg % 8;
+    x = k % tiles;
+  } else {
+    pair = wg / tiles;
+    x = wg % tiles;
+  }
+  const int h = pair % a.heads_q;
+  const int b = pair / a.heads_q;
   // decode the linear lower-triangular tile index
-  const int x = blockIdx.x;
   int I = (int)((sqrtf(8.0f * x + 1.0f) - 1.0f) * 0.5f);
   while ((I + 1) * (I + 2) / 2 <= x) ++I;
   while (I * (I + 1) / 2 > x) --I;
   const int J = x - I * (I + 1) / 2;
-  const int h = blockIdx.y;
-  const int b = blockIdx.z;
   const int g = h / (a.heads_q / a.heads_kv);
 
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -377,7 +393,9 @@ __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
 
 hipError_t launch_gate_logits(const GateLogitsArgs& a, hipStream_t s) {
   const int T = (a.n_blocks + 127) / 128;
-  dim3 grid(T * (T + 1) / 2, a.heads_q, a.batch);
+  const int64_t wgs = (int64_t)T * (T + 1) / 2 * a.heads_q * a.batch;
+  if (wgs > INT32_MAX) return hipErrorInvalidValue;
+  dim3 grid((unsigned)wgs);
   switch (a.gate_dim) {
     case 32: hipLaunchKernelGGL(gate_logits_kernel<32>, grid, dim3(256), 0, s, a); break;
     case 64: hipLaunchKernelGGL(gate_logits_kernel<64>, grid, dim3(256), 0, s, a); break;
