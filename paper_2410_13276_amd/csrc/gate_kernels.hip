@@ -278,7 +278,8 @@ hipError_t launch_pool_proj(const PoolProjArgs& a, hipStream_t s) {
 // contraction pairs identical features (the parts are stored in exactly this
 // lane order, split_index).  Output lane holds column j = lane%32 and rows
 // 8*(e/4) + 4*hf + e%4 of a 32x32 block (e = accumulator index).  Blocks
-// entirely above the diagonal are skipped.  The next feature step's operands
+// entirely above the diagonal are computed (a per-MFMA branch broke the
+// MFMA stream into small blocks) but not stored.  The next feature step's operands
 // load while the current one multiplies (two steps in flight measured no
 // faster).
 template <int DG>
@@ -371,9 +372,8 @@ __global__ __launch_bounds__(256) void gate_logits_kernel(GateLogitsArgs a) {
 #pragma unroll
       for (int r = 0; r < 2; ++r)
 #pragma unroll
-        for (int cc = 0; cc < 2; ++cc)
-          if (!(diag && cc > r))
-            acc[r][cc] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[r][PQ[t]], kb[cc][PK[t]], acc[r][cc], 0, 0, 0);
+        for (int cc = 0; cc < 2; ++cc)  // (diagonal sub-tiles compute their upper block too: no branch here)
+          acc[r][cc] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa[r][PQ[t]], kb[cc][PK[t]], acc[r][cc], 0, 0, 0);
   }
   float* out = a.logits + ((int64_t)b * a.heads_q + h) * nb * nb;
 #pragma unroll
