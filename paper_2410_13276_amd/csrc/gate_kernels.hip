@@ -211,7 +211,9 @@ __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
   __shared__ __attribute__((aligned(16))) float smem[R * 3 * D];
   __shared__ float srot[R * DG];
   const int b = blockIdx.z;
-  const int slot = blockIdx.y;
+  // the K heads' workgroups (max | min | avg pooling, a GEMV three times as
+  // wide) are dispatched first, so that the lighter Q heads' fill the end
+  const int slot = (blockIdx.y + a.heads_q) % (a.heads_q + a.heads_kv);
   if (slot < a.heads_q) {
     const int h = slot;
     const T* x = static_cast<const T*>(a.q.ptr) + b * a.q.sb + h * a.q.sh;
