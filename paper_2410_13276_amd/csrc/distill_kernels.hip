@@ -11,7 +11,8 @@
 //                       identical).
 //   gemm_f32_kernel     fp32 strided batched products for the backward pass
 //                       (dQg = dL Kg, dKg = dL^T Qg, dW = pooled^T dG), 64x64
-//                       LDS tiles on fp32 MFMA, triangular skipping of the
+//                       LDS tiles of the operands split in three bf16 parts on
+//                       bf16 MFMA (fp32-accurate), triangular skipping of the
 //                       causal zeros, K split over several workgroups when
 //                       the output tiles are few.
 //   gemm_reduce_kernel  sums the split parts in a fixed order.
@@ -137,23 +138,41 @@ __global__ __launch_bounds__(256) void loss_mean_kernel(const double* __restrict
   if (threadIdx.x == 0) loss[0] = (float)(s / (double)rows);
 }
 
-// 64x64 output tile per 256-thread workgroup (a 32x32 fp32-MFMA block per
-// wavefront, v_mfma_f32_32x32x2_f32), K in chunks of 32 staged through two LDS
-// buffers: the next chunk's global loads are in flight in registers while the
-// current chunk's MFMAs run, one barrier per chunk.  The LDS tiles are
-// [row][k] with k contiguous (rows padded to 36 floats, 16-byte aligned and
-// conflict-free for 16-byte reads), so a lane reads the 16 k values of its
-// next 16 MFMAs with four 16-byte reads: MFMA step s contracts k = s (lanes
-// 0-31) and k = 16 + s (lanes 32-63).  Operand tiles are read from global
-// memory along whichever index has unit stride, so that loads coalesce for
-// every layout used here.  A workgroup computes part s of its tile's (k1, k2)
-// chunks; with splits > 1 the part's product goes to g.part.
+// 64x64 output tile per 256-thread workgroup (a 32x32 block per wavefront), K in
+// chunks of 32 staged through two LDS buffers: the next chunk's global loads
+// are in flight in registers while the current chunk's MFMAs run, one barrier
+// per chunk.  Each fp32 operand value is written to LDS as three bf16 parts
+// (hi = RNE(x), mid = RNE(x - hi), lo = RNE(x - hi - mid); both differences
+// are exact), and the products of the parts down to 2^-18 of the leading one
+// (hi.hi, hi.mid, mid.hi, hi.lo, lo.hi, mid.mid) are summed in fp32 by
+// v_mfma_f32_32x32x16_bf16: fp32-accurate products at 6 MFMAs of 32 cycles
+// per 32x32x16 step instead of 8 fp32 MFMAs (v_mfma_f32_32x32x2_f32) of 64.
+// The LDS tiles are [part][row][k] bf16 with k contiguous in rows of 64 bytes,
+// their four 16-byte chunks XOR-swizzled by (row / 4) % 4 so that 16 lanes
+// reading 16 rows hit 16 distinct bank groups (48 KiB for the two buffers:
+// three workgroups per CU), and a lane reads the 8 k values of one MFMA
+// operand (k = 16 s + 8 hf .. +7 of its row or column at step s) with one
+// 16-byte read per part.  Operand tiles are read from global memory along
+// whichever index has unit stride, so that loads coalesce for every layout
+// used here.  A workgroup computes part s of its tile's (k1, k2) chunks; with
+// splits > 1 the part's product goes to g.part.
 constexpr int kT = 64;
 constexpr int kKc = 32;
-constexpr int kKp = kKc + 4;              // LDS row stride (floats)
+constexpr int kKb = kKc;                // LDS row stride (bf16 elements)
 constexpr int kLoads = kT * kKc / 256;  // elements of each operand per thread and chunk
 static_assert(kT == kKlTile, "the logit gradient is written up to the end of each row's GEMM tile");
 static_assert(kT == 64 && kKc == 32 && kLoads == 8, "the element mapping of fetch and stash");
+
+// Element offset within an LDS row of k (a multiple of 8: one 16-byte chunk).
+__device__ __forceinline__ int swz(int row, int k) { return (((k >> 3) ^ ((row >> 2) & 3)) << 3) | (k & 7); }
+
+// The three bf16 parts of x.
+__device__ __forceinline__ void split3(float x, __bf16& hi, __bf16& mid, __bf16& lo) {
+  hi = (__bf16)x;
+  const float r = x - (float)hi;
+  mid = (__bf16)r;
+  lo = (__bf16)(r - (float)mid);
+}
 
 // Tiles are dispatched heaviest first over the whole launch (a 1-D grid):
 // the row-tile index outermost, in the order of decreasing work for the
@@ -162,8 +181,8 @@ static_assert(kT == 64 && kKc == 32 && kLoads == 8, "the element mapping of fetc
 // column tile.  Launched batch by batch instead, each batch's heavy tiles
 // would come last and the final batches' would run alone at the end.
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
-  __shared__ __attribute__((aligned(16))) float sA[2][kT][kKp];
-  __shared__ __attribute__((aligned(16))) float sB[2][kT][kKp];
+  __shared__ __attribute__((aligned(16))) __bf16 sA[2][3][kT][kKb];
+  __shared__ __attribute__((aligned(16))) __bf16 sB[2][3][kT][kKb];
   const int t = threadIdx.x;
   const int ntn = (g.N + kT - 1) / kT, ntm = (g.M + kT - 1) / kT, nzs = g.Z * splits;
   const int lin = blockIdx.x;
@@ -194,9 +213,9 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
 
   // Element u of this thread's share of a chunk.  Row index fast in memory:
   // row = t % 64, k = 8 (t / 64) + u (the thread's 8 values are contiguous in
-  // the LDS row: two 16-byte writes).  k fast: row = t / 32 + 8u, k = t % 32.
-  // Either way one offset per operand plus u times a uniform stride addresses
-  // every element.
+  // the LDS row: one 16-byte write per part).  k fast: row = t / 32 + 8u,
+  // k = t % 32.  Either way one offset per operand plus u times a uniform
+  // stride addresses every element.
   const int ar = a_mfast ? t % 64 : t / 32, ak = a_mfast ? 8 * (t / 64) : t % 32;
   const int br = b_nfast ? t % 64 : t / 32, bk = b_nfast ? 8 * (t / 64) : t % 32;
   const int64_t a_off = (int64_t)(m0 + ar) * g.sam + (int64_t)ak * g.sak2;
@@ -236,43 +255,60 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
       ++k1;
     }
   };
+  // the 8 values of one operand into its LDS tile, split in three parts
+  auto stash_one = [&](__bf16 (&s)[3][kT][kKb], const float (&r)[kLoads], bool fast, int row, int k) {
+    if (fast) {  // one row, k .. k + 7
+      bf16x8 h, m, l;
+#pragma unroll
+      for (int u = 0; u < kLoads; ++u) {
+        __bf16 a, b, c;
+        split3(r[u], a, b, c);
+        h[u] = a;
+        m[u] = b;
+        l[u] = c;
+      }
+      const int kw = swz(row, k);
+      *reinterpret_cast<bf16x8*>(&s[0][row][kw]) = h;
+      *reinterpret_cast<bf16x8*>(&s[1][row][kw]) = m;
+      *reinterpret_cast<bf16x8*>(&s[2][row][kw]) = l;
+    } else {  // rows row + 8u, one k
+#pragma unroll
+      for (int u = 0; u < kLoads; ++u) {
+        const int rw = row + 8 * u, kw = swz(rw, k);
+        split3(r[u], s[0][rw][kw], s[1][rw][kw], s[2][rw][kw]);
+      }
+    }
+  };
   auto stash = [&](int buf) {
-    if (a_mfast) {
-      *reinterpret_cast<f32x4*>(&sA[buf][ar][ak]) = f32x4{ra[0], ra[1], ra[2], ra[3]};
-      *reinterpret_cast<f32x4*>(&sA[buf][ar][ak + 4]) = f32x4{ra[4], ra[5], ra[6], ra[7]};
-    } else {
-#pragma unroll
-      for (int u = 0; u < kLoads; ++u) sA[buf][ar + 8 * u][ak] = ra[u];
-    }
-    if (b_nfast) {
-      *reinterpret_cast<f32x4*>(&sB[buf][br][bk]) = f32x4{rb[0], rb[1], rb[2], rb[3]};
-      *reinterpret_cast<f32x4*>(&sB[buf][br][bk + 4]) = f32x4{rb[4], rb[5], rb[6], rb[7]};
-    } else {
-#pragma unroll
-      for (int u = 0; u < kLoads; ++u) sB[buf][br + 8 * u][bk] = rb[u];
-    }
+    stash_one(sA[buf], ra, a_mfast, ar, ak);
+    stash_one(sB[buf], rb, b_nfast, br, bk);
   };
   if (c0 < c1) {
     fetch();
     stash(0);
   }
   __syncthreads();
+  // part pairs (A part, B part) in the order they are summed
+  constexpr int PA[6] = {0, 0, 1, 0, 2, 1};
+  constexpr int PB[6] = {0, 1, 0, 2, 0, 1};
   int buf = 0;
   for (int64_t c = c0; c < c1; ++c) {
     const bool more = c + 1 < c1;
     if (more) fetch();
     // wavefront (wm, wn) accumulates the 32x32 block at rows 32 wm, columns 32
-    // wn of the tile; lane (hf, col) supplies k = 16 hf + s of its row (A) and
-    // column (B) to MFMA step s
-    f32x4 av[4], bv[4];
+    // wn of the tile; lane (hf, col) supplies k = 16 st + 8 hf .. +7 of its row
+    // (A) and column (B) to MFMA step st
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      av[q] = *reinterpret_cast<const f32x4*>(&sA[buf][32 * wm + col][16 * hf + 4 * q]);
-      bv[q] = *reinterpret_cast<const f32x4*>(&sB[buf][32 * wn + col][16 * hf + 4 * q]);
+    for (int st = 0; st < kKc / 16; ++st) {
+      bf16x8 av[3], bv[3];
+#pragma unroll
+      for (int p = 0; p < 3; ++p) {
+        av[p] = *reinterpret_cast<const bf16x8*>(&sA[buf][p][32 * wm + col][swz(32 * wm + col, 16 * st + 8 * hf)]);
+        bv[p] = *reinterpret_cast<const bf16x8*>(&sB[buf][p][32 * wn + col][swz(32 * wn + col, 16 * st + 8 * hf)]);
+      }
+#pragma unroll
+      for (int q = 0; q < 6; ++q) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[PA[q]], bv[PB[q]], acc, 0, 0, 0);
     }
-#pragma unroll
-    for (int st = 0; st < kKc / 2; ++st)
-      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(av[st / 4][st % 4], bv[st / 4][st % 4], acc, 0, 0, 0);
     if (more) stash(buf ^ 1);
     __syncthreads();
     buf ^= 1;
