@@ -143,7 +143,7 @@ typedef struct {
                                KV group share their rows (dense attention, the ground truth, a
                                kv_shared mask): 1, 2 or 4; 0: 2 */
   int32_t batch_min_blocks; /* per-head sparse rows of at least this many 64-token blocks launch
-                               the heavier half of their tasks in batches of resident workgroups;
+                               the heaviest quarter of their tasks in batches of resident workgroups;
                                0: 2048; < 0: never */
   int32_t batch_wgs;        /* workgroups per such batch (rounded down to a multiple of 8);
                                0: as many as the GPU holds at once */

@@ -1483,10 +1483,13 @@ static void launch_nh_d(const KernelArgs& ka, int nh, bool sparse, bool ragged, 
 // walk their ascending lists roughly in step: concurrent rows then share more
 // of their K/V tiles in L2.  Within a batch the order is the usual one (task
 // ids continue across batches), so every output is unchanged.  Only the
-// heavier half of the tasks is batched: the later batches' short rows leave too
-// much idle time at their ends.  Measured at 131072 tokens (32 q / 8 KV heads,
-// TopK 0.1): 17.29 ms unbatched, 16.92 ms with every task batched, 16.65 ms
-// with the heavier half batched; 48.9 -> 48.2 ms (all batched) with per-head
+// heaviest quarter of the tasks is batched: the later batches' shorter rows
+// leave too much idle time at their ends.  Measured at 131072 tokens (32 q / 8
+// KV heads, TopK 0.1), walking ascending: 17.29 ms unbatched, 16.92 ms with
+// every task batched, 16.65 ms with the heavier half batched; with the walk by
+// residue classes (same box, batched fraction none / 1/8 / 1/4 / 3/8 / 1/2 /
+// 3/4 / all): 14.47-14.53, 14.33-14.36, 14.24-14.33, 14.30-14.35, 14.41-14.51,
+// 14.67, 14.83 ms; 48.9 -> 48.2 ms (all batched) with per-head
 // densities spread over 5-40%; at 32768 tokens the batch ends' idle time
 // outweighed the gain (1.84 -> 2.06 ms; at 65536 tokens with 7 heads of 5-40%
 // density 7.6 -> 10.6 ms), hence the size threshold (a.batch_min_blocks, 2048
@@ -1560,9 +1563,9 @@ static hipError_t launch_attn_one(const AttnArgs& a, hipStream_t s, int* count) 
   if (a.bf16 && sparse && !pool && a.batch_min_blocks > 0 && a.n_blocks >= a.batch_min_blocks) {
     const int E = batch_size(a, ragged);
     if (E > 0 && total > E) {
-      // the heavier half of the tasks (the longest rows) in batches, the rest
-      // (whose short rows would leave batch ends idle) in one launch
-      const int64_t batched = (total / 2 + E - 1) / E * E;
+      // the heaviest quarter of the tasks (the longest rows) in batches, the
+      // rest (whose shorter rows would leave batch ends idle) in one launch
+      const int64_t batched = (total / 4 + E - 1) / E * E;
       for (int64_t b0 = 0, cnt = 0; b0 < total; b0 += cnt) {
         cnt = b0 < batched ? std::min<int64_t>(E, total - b0) : total - b0;
         ka.task_base = (int)b0;
