@@ -85,24 +85,38 @@ __device__ __forceinline__ void store_split(uint16_t* head, int r, int f, int dg
 }
 
 // One workgroup of 256 threads pools R consecutive 64-token blocks of one head
-// (each thread owns one 16-byte column chunk of one block and walks its 64 rows)
-// and then projects the R pooled rows through the head's gate weights.
-template <typename T, int D, int DG, bool IS_K, int BLK>
+// and then projects the R pooled rows through the head's gate weights.  Each
+// thread owns one 16-byte column chunk of one block and walks its rows: all
+// of them (RS = 1), or one of RS equal row ranges (short sequences, whose
+// RS = 1 grid would hold too few workgroups to keep enough loads in flight),
+// the ranges' partial sums, maxima and minima then combined through LDS.
+template <typename T, int D, int DG, int RS>
+struct PoolTiling {
+  static constexpr int EPL = Load16<T>::N;  // elements per 16-byte load
+  static constexpr int TPR = D / EPL;       // threads per block row
+  static constexpr int R = 256 / (TPR * RS);  // blocks per workgroup
+  static constexpr bool ok = R >= 1 && R * TPR * RS == 256 && R * DG >= 256 && (R * DG) % 256 == 0;
+};
+
+template <typename T, int D, int DG, bool IS_K, int BLK, int RS>
 __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t ss, int nb, int seq_len,
                                                const float* __restrict__ W,
                                                float* __restrict__ out, float* smem,
                                                float* srot, double rope_base,
                                                float* __restrict__ pooled_out, uint16_t* __restrict__ split) {
-  constexpr int EPL = Load16<T>::N;  // elements per 16-byte load
-  constexpr int TPR = D / EPL;       // threads per block row
-  constexpr int R = 256 / TPR;       // blocks per workgroup
+  using Til = PoolTiling<T, D, DG, RS>;
+  constexpr int EPL = Til::EPL;
+  constexpr int TPR = Til::TPR;
+  constexpr int R = Til::R;
   constexpr int WIDTH = IS_K ? 3 * D : D;
   constexpr int RPT = R * DG / 256;  // output rows per thread in the GEMV
-  static_assert(R * TPR == 256 && RPT >= 1 && (R * DG) % 256 == 0, "bad tiling");
+  constexpr int PSTR = RS * WIDTH;   // LDS floats between pooled rows
+  static_assert(Til::ok, "bad tiling");
 
   const int t = threadIdx.x;
-  const int r = t / TPR;
   const int c = t % TPR;
+  const int rs = (t / TPR) % RS;  // this thread's row range
+  const int r = t / (TPR * RS);
   const int blk = blockIdx.x * R + r;
 
   if (blk < nb) {
@@ -115,8 +129,9 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
     }
     const T* base = x + (int64_t)blk * BLK * ss + c * EPL;
     const int nrow = min(BLK, seq_len - blk * BLK);  // the last block may be partial
+    const int row_end = min(nrow, (rs + 1) * (BLK / RS));
 #pragma unroll 8
-    for (int row = 0; row < nrow; ++row) {
+    for (int row = rs * (BLK / RS); row < row_end; ++row) {
       float v[EPL];
       Load16<T>::get(base + row * ss, v);
 #pragma unroll
@@ -128,10 +143,11 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
         }
       }
     }
-    float* prow = smem + r * WIDTH + c * EPL;
+    // RS = 1: the pooled row; otherwise the range's raw sum, maximum, minimum
+    float* prow = smem + (r * RS + rs) * WIDTH + c * EPL;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) {
-      const float avg = sum[e] / (float)nrow;
+      const float avg = RS == 1 ? sum[e] / (float)nrow : sum[e];
       if (IS_K) {
         prow[e] = mx[e];
         prow[D + e] = mn[e];
@@ -140,7 +156,7 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
         prow[e] = avg;
       }
     }
-    if (pooled_out) {  // the pooled row itself (kept for the gate's weight gradients)
+    if (RS == 1 && pooled_out) {  // the pooled row itself (kept for the gate's weight gradients)
       float* po = pooled_out + (int64_t)blk * WIDTH + c * EPL;
 #pragma unroll
       for (int e = 0; e < EPL; ++e) {
@@ -153,6 +169,27 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
     }
   }
   __syncthreads();
+  if constexpr (RS > 1) {
+    // combine the ranges in range order into the first range's slot: maxima,
+    // minima, and the sums divided by the block's row count
+    for (int idx = t; idx < R * WIDTH; idx += 256) {
+      const int rr = idx / WIDTH, col = idx % WIDTH;
+      const int bb = blockIdx.x * R + rr;
+      if (bb >= nb) continue;
+      float* p = smem + rr * PSTR + col;
+      float v = p[0];
+      const int kind = IS_K ? col / D : 2;  // 0 max, 1 min, 2 mean
+#pragma unroll
+      for (int q = 1; q < RS; ++q) {
+        const float u = p[q * WIDTH];
+        v = kind == 0 ? fmaxf(v, u) : (kind == 1 ? fminf(v, u) : v + u);
+      }
+      if (kind == 2) v /= (float)min(BLK, seq_len - bb * BLK);
+      p[0] = v;
+      if (pooled_out) pooled_out[(int64_t)bb * WIDTH + col] = v;
+    }
+    __syncthreads();
+  }
 
   // GEMV: out[r][j] = sum_c pooled[r][c] * W[c][j]
   const int j = t % DG;
@@ -168,7 +205,7 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
     for (int e = 0; e < 4; ++e) w[e] = W[(int64_t)(cc + e) * DG + j];
 #pragma unroll
     for (int q = 0; q < RPT; ++q) {
-      const f32x4 p = *reinterpret_cast<const f32x4*>(smem + (r0 + q * RSTEP) * WIDTH + cc);
+      const f32x4 p = *reinterpret_cast<const f32x4*>(smem + (r0 + q * RSTEP) * PSTR + cc);
       acc[q] = fmaf(p[0], w[0], acc[q]);
       acc[q] = fmaf(p[1], w[1], acc[q]);
       acc[q] = fmaf(p[2], w[2], acc[q]);
@@ -204,11 +241,10 @@ __device__ __forceinline__ void pool_proj_head(const T* __restrict__ x, int64_t 
   }
 }
 
-template <typename T, int D, int DG, int BLK>
+template <typename T, int D, int DG, int BLK, int RS>
 __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
-  constexpr int EPL = Load16<T>::N;
-  constexpr int R = 256 / (D / EPL);
-  __shared__ __attribute__((aligned(16))) float smem[R * 3 * D];
+  constexpr int R = PoolTiling<T, D, DG, RS>::R;
+  __shared__ __attribute__((aligned(16))) float smem[R * RS * 3 * D];
   __shared__ float srot[R * DG];
   const int b = blockIdx.z;
   // the K heads' workgroups (max | min | avg pooling, a GEMV three times as
@@ -220,7 +256,7 @@ __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
     float* out = a.qg ? a.qg + ((int64_t)b * a.heads_q + h) * a.n_blocks * DG : nullptr;
     float* po = a.qp ? a.qp + ((int64_t)b * a.heads_q + h) * a.n_blocks * D : nullptr;
     uint16_t* sp = a.qs ? a.qs + ((int64_t)b * a.heads_q + h) * split_rows(a.n_blocks) * 3 * DG : nullptr;
-    pool_proj_head<T, D, DG, false, BLK>(x, a.q.ss, a.n_blocks, a.seq_len, a.wq + h * a.wq_head_stride, out, smem, srot,
+    pool_proj_head<T, D, DG, false, BLK, RS>(x, a.q.ss, a.n_blocks, a.seq_len, a.wq + h * a.wq_head_stride, out, smem, srot,
                                     a.rope_base, po, sp);
   } else {
     const int g = slot - a.heads_q;
@@ -228,19 +264,33 @@ __global__ __launch_bounds__(256) void pool_proj_kernel(PoolProjArgs a) {
     float* out = a.kg ? a.kg + ((int64_t)b * a.heads_kv + g) * a.n_blocks * DG : nullptr;
     float* po = a.kp ? a.kp + ((int64_t)b * a.heads_kv + g) * a.n_blocks * 3 * D : nullptr;
     uint16_t* sp = a.ks ? a.ks + ((int64_t)b * a.heads_kv + g) * split_rows(a.n_blocks) * 3 * DG : nullptr;
-    pool_proj_head<T, D, DG, true, BLK>(x, a.k.ss, a.n_blocks, a.seq_len, a.wk + g * a.wk_head_stride, out, smem, srot,
+    pool_proj_head<T, D, DG, true, BLK, RS>(x, a.k.ss, a.n_blocks, a.seq_len, a.wk + g * a.wk_head_stride, out, smem, srot,
                                    a.rope_base, po, sp);
   }
 }
 
-template <typename T, int D, int DG>
-static hipError_t pool_proj_launch(const PoolProjArgs& a, hipStream_t s) {
-  constexpr int R = 256 / (D / Load16<T>::N);
+// Row ranges per block: 4 when the grid of whole-block threads would hold fewer
+// than kPoolSplitWgs workgroups (and the tiling allows it), else 1.
+constexpr int kPoolSplitWgs = 512;
+
+template <typename T, int D, int DG, int RS>
+static hipError_t pool_proj_launch_rs(const PoolProjArgs& a, hipStream_t s) {
+  constexpr int R = PoolTiling<T, D, DG, RS>::R;
   dim3 grid((a.n_blocks + R - 1) / R, a.heads_q + a.heads_kv, a.batch);
-  if (a.block == 64) hipLaunchKernelGGL((pool_proj_kernel<T, D, DG, 64>), grid, dim3(256), 0, s, a);
-  else if (a.block == 128) hipLaunchKernelGGL((pool_proj_kernel<T, D, DG, 128>), grid, dim3(256), 0, s, a);
+  if (a.block == 64) hipLaunchKernelGGL((pool_proj_kernel<T, D, DG, 64, RS>), grid, dim3(256), 0, s, a);
+  else if (a.block == 128) hipLaunchKernelGGL((pool_proj_kernel<T, D, DG, 128, RS>), grid, dim3(256), 0, s, a);
   else return hipErrorInvalidValue;
   return hipGetLastError();
+}
+
+template <typename T, int D, int DG>
+static hipError_t pool_proj_launch(const PoolProjArgs& a, hipStream_t s) {
+  constexpr int R1 = PoolTiling<T, D, DG, 1>::R;
+  const int64_t wgs = (int64_t)((a.n_blocks + R1 - 1) / R1) * (a.heads_q + a.heads_kv) * a.batch;
+  if constexpr (PoolTiling<T, D, DG, 4>::ok) {
+    if (wgs < kPoolSplitWgs) return pool_proj_launch_rs<T, D, DG, 4>(a, s);
+  }
+  return pool_proj_launch_rs<T, D, DG, 1>(a, s);
 }
 
 template <typename T, int D>
