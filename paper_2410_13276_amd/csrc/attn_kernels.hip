@@ -850,13 +850,14 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
     // P^T operand of k-step kt: accumulators 8(kt%2)..+7 of half kt/2, i.e. keys
     // 32(kt/2) + 16(kt%2) + {4hf + 0..3, 8 + 4hf + 0..3}
     bf16x8 pb[4];
-    float ps[4] = {0.f, 0.f, 0.f, 0.f};  // four independent partial sums
+    float ps[4];  // four independent partial sums, each started with its first term (the
+                  // compiler keeps 0 + p as an add: p might be -0, which exp2 never returns)
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float p = __builtin_amdgcn_exp2f(fmaf(sc[kt / 2][8 * (kt % 2) + e], c, -mc));
-        ps[kt] += p;
+        ps[kt] = e == 0 ? p : ps[kt] + p;
         pb[kt][e] = (__bf16)p;
       }
     l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
