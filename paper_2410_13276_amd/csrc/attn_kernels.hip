@@ -629,6 +629,7 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
 #pragma unroll
     for (int e = 0; e < 16; ++e) acc[dt][e] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
+  float mc = 0.f;  // m_run * c, 0 while m_run is -inf (formed when m_run moves)
   const float c = ka.scale_log2;
 
   // Per-lane LDS element offsets of the operand reads.  K: row 32mt + col, chunk
@@ -837,13 +838,13 @@ void attn_fwd_bf16_kernel(KernelArgs ka) {
       const float m_new = fmaxf(m_run, mloc);
       const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c);
       m_run = m_new;
+      mc = (m_run == -INFINITY) ? 0.f : m_run * c;
       l_run *= alpha;
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[dt][e] *= alpha;
     }
-    const float mc = (m_run == -INFINITY) ? 0.f : m_run * c;
 
     // S for the next tile (harmless junk when there is none)
     s_product(sn);
