@@ -2,7 +2,8 @@
 // section 3.2, Eq. 2): KL(ground truth || gate score) and its gradients with
 // respect to the gate weights.
 //
-//   kl_rows_kernel      one wavefront per query-block row: the row's softmax of
+//   kl_rows_kernel      one wavefront per query-block row (kl_rows_staged_kernel:
+//                       the row held in registers): the row's softmax of
 //                       the gate logits, the ground-truth row renormalised to a
 //                       distribution T, the row's KL(T || P) and the logit
 //                       gradient (P sum(T) - T) / rows written over the logits.
@@ -101,6 +102,81 @@ __global__ __launch_bounds__(256) void kl_rows_kernel(KlArgs a) {
     } else {
       Lr[j0] = d[0];
     }
+  }
+  double dl = (double)loss;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) dl += __shfl_xor(dl, off);
+  if (lane == 0) a.row_loss[r] = dl;
+}
+
+// The same row computation with the row held in registers (16-byte chunks u =
+// 0 .. NW-1 of a lane: entries 4 (lane + 64 u) .. +3), every load issued before
+// any is used: the streaming loop above waits for each chunk in turn (its
+// online maximum depends on the previous one).  Needs nb % 4 == 0, 16-byte
+// aligned rows and nb <= 256 NW.
+template <int NW>
+__global__ __launch_bounds__(256) void kl_rows_staged_kernel(KlArgs a) {
+  const int wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const int64_t r = (int64_t)blockIdx.x * kRowsPerBlock + wave;
+  if (r >= a.rows) return;
+  const int nb = a.n_blocks;
+  const int i = (int)(r % nb);
+  const int M = i + 1;                                  // causal entries j <= i
+  const int Mz = min(nb, (i / kKlTile + 1) * kKlTile);  // entries the gradient covers
+  float* Lr = a.logits + r * nb;
+  const float* gr = a.gt + r * nb;
+  // entries past the diagonal (and chunks past the row) read as logit -inf and
+  // target 0, which takes them out of every sum below
+  f32x4 l[NW], g[NW];
+#pragma unroll
+  for (int u = 0; u < NW; ++u) {
+    const int j0 = 4 * (lane + 64 * u);
+    f32x4 lu = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, gu = {0.f, 0.f, 0.f, 0.f};
+    if (j0 < M) {
+      lu = *reinterpret_cast<const f32x4*>(Lr + j0);
+      gu = *reinterpret_cast<const f32x4*>(gr + j0);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool ok = j0 + e < M;
+      l[u][e] = ok ? lu[e] : -INFINITY;
+      g[u][e] = ok ? gu[e] : 0.f;
+    }
+  }
+  float mx = -INFINITY, gs = 0.f;
+#pragma unroll
+  for (int u = 0; u < NW; ++u)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      mx = fmaxf(mx, l[u][e]);
+      gs += g[u][e];
+    }
+  const float mw = wave_max(mx);
+  float es = 0.f;
+#pragma unroll
+  for (int u = 0; u < NW; ++u)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) es += __expf(l[u][e] - mw);  // exp(-inf) = 0
+  es = wave_sum(es);
+  gs = wave_sum(gs);
+  const float lse = mw + __logf(es);
+  const float inv_gs = gs > 0.f ? 1.0f / gs : 0.f;
+  const float tsum = gs > 0.f ? 1.0f : 0.f;  // sum of T
+  const float log_gs = gs > 0.f ? __logf(gs) : 0.f;
+  float loss = 0.f;
+#pragma unroll
+  for (int u = 0; u < NW; ++u) {
+    const int j0 = 4 * (lane + 64 * u);
+    f32x4 d;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float logp = l[u][e] - lse;
+      const float t = g[u][e] * inv_gs;
+      if (t > 0.f) loss += t * ((__logf(g[u][e]) - log_gs) - logp);
+      d[e] = (__expf(logp) * tsum - t) * a.inv_rows;  // 0 past the diagonal
+    }
+    if (j0 < Mz) *reinterpret_cast<f32x4*>(Lr + j0) = d;
   }
   double dl = (double)loss;
 #pragma unroll
@@ -370,8 +446,13 @@ hipError_t launch_kl_rows(const KlArgs& a, hipStream_t s) {
   const int64_t blocks = (a.rows + kRowsPerBlock - 1) / kRowsPerBlock;
   const bool vec = a.n_blocks % 4 == 0 && reinterpret_cast<uintptr_t>(a.logits) % 16 == 0 &&
                    reinterpret_cast<uintptr_t>(a.gt) % 16 == 0;
-  if (vec) hipLaunchKernelGGL(kl_rows_kernel<4>, dim3((unsigned)blocks), dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(kl_rows_kernel<1>, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  const dim3 grid((unsigned)blocks);
+  if (vec && a.n_blocks <= 256) hipLaunchKernelGGL(kl_rows_staged_kernel<1>, grid, dim3(256), 0, s, a);
+  else if (vec && a.n_blocks <= 512) hipLaunchKernelGGL(kl_rows_staged_kernel<2>, grid, dim3(256), 0, s, a);
+  else if (vec && a.n_blocks <= 1024) hipLaunchKernelGGL(kl_rows_staged_kernel<4>, grid, dim3(256), 0, s, a);
+  else if (vec && a.n_blocks <= 2048) hipLaunchKernelGGL(kl_rows_staged_kernel<8>, grid, dim3(256), 0, s, a);
+  else if (vec) hipLaunchKernelGGL(kl_rows_kernel<4>, grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL(kl_rows_kernel<1>, grid, dim3(256), 0, s, a);
   double* parts = a.row_loss + a.rows;
   hipLaunchKernelGGL(loss_part_kernel, dim3(kLossParts), dim3(256), 0, s, a.row_loss, a.rows, parts);
   hipLaunchKernelGGL(loss_mean_kernel, dim3(1), dim3(256), 0, s, parts, a.rows, a.loss);

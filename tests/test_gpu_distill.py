@@ -30,7 +30,7 @@ ELEM_FLOOR = 1e-2
 ELEM_RTOL = 1e-3
 
 
-def _check_grad_elementwise(g, ref):
+def _check_grad_elementwise(g, ref, rtol=ELEM_RTOL):
     top = float(np.abs(ref).max())
     if top == 0.0:  # (a single block: every gradient is exactly zero, checked above)
         return
@@ -38,7 +38,7 @@ def _check_grad_elementwise(g, ref):
     rel = np.abs(g[big] - ref[big]) / np.abs(ref[big])
     print(f"[distill] element-wise relative error {float(rel.max()):.3e} over {int(big.sum())} entries",
           flush=True)
-    assert float(rel.max()) <= ELEM_RTOL, float(rel.max())
+    assert float(rel.max()) <= rtol, float(rel.max())
 
 
 CASES = [
@@ -102,6 +102,39 @@ def test_gate_distill_parity(case, min_chunks):
         print(f"[distill] grad err {err:.3e} of max {float(np.abs(ref).max()):.3e}", flush=True)
         assert err <= GRAD_RTOL * float(np.abs(ref).max()) + 1e-12, (err, float(np.abs(ref).max()))
         _check_grad_elementwise(g, ref)
+
+
+# Long rows (one query head): nb = 1100 and 2048 hold the whole row in registers
+# (eight 16-byte chunks per lane), nb = 2052 streams it in two passes.  The
+# element-wise bar is looser here: the fp32 row softmax of a long row carries a
+# larger absolute error (its log-sum-exp and logits round at a larger scale), and
+# the small gradient entries are sums with heavy cancellation of P - T.
+# Measured: 1.6e-3 at nb = 1024, 2.3e-3 at nb = 1100 (both KL row kernels give
+# the same within 10%), while the max-scaled error stays at 1-4e-5 of the
+# largest entry.
+LONG_ROWS = [1100, 2048, 2052]
+ELEM_RTOL_LONG = 5e-3
+
+
+@pytest.mark.parametrize("nb", LONG_ROWS)
+def test_gate_distill_long_rows(nb):
+    B, Hq, Hkv, S, D, Dg = 1, 1, 1, 64 * nb, 64, 32
+    seed = stable_seed("distlong", nb)
+    _, q, k, _, _, _ = small_inputs(B, Hq, Hkv, S, D, "bf16", seed=seed, spikes=True)
+    wq, wk = _weights(B, Hq, Hkv, D, Dg, True, seed + 1)
+    gt = synthetic_gt(B, Hq, nb, seed + 2)
+    print(f"[distill] long rows nb = {nb}", flush=True)
+    loss, dwq, dwk = seer.gate_distill(to_device(q), to_device(k), torch.from_numpy(wq).cuda(),
+                                       torch.from_numpy(wk).cuda(), torch.from_numpy(gt).cuda())
+    torch.cuda.synchronize()
+    l_ref, dwq_ref, dwk_ref = oracle.distill(q, k, wq, wk, gt)
+    assert abs(float(loss.item()) - l_ref) <= DIST_RTOL * abs(l_ref), (float(loss.item()), l_ref)
+    for got, ref in ((dwq, dwq_ref), (dwk, dwk_ref)):
+        g = got.cpu().numpy().astype(np.float64)
+        err = float(np.abs(g - ref).max())
+        print(f"[distill] grad err {err:.3e} of max {float(np.abs(ref).max()):.3e}", flush=True)
+        assert err <= GRAD_RTOL * float(np.abs(ref).max()), err
+        _check_grad_elementwise(g, ref, ELEM_RTOL_LONG)
 
 
 def test_gate_distill_deterministic_and_workspace_reuse():
