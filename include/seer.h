@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define SEER_ABI_VERSION 4
+#define SEER_ABI_VERSION 5
 #define SEER_BLOCK 64 /* the attention tile edge and the default gate block (section 4); gate
                         blocks and masks of 128 tokens are the other size the paper names */
 
@@ -159,6 +159,10 @@ typedef struct {
 typedef struct {
   int32_t gemm_min_chunks;  /* the backward products split their reduction into parts of at
                                least this many 32-wide chunks; 0: 8 */
+  int32_t gemm_tile_n;      /* output tile width of the backward products, 64 or 128 columns
+                               (any other value: SEER_ERR_INVALID_ARG); 0: 128 when gate_dim
+                               is 128 and the rows hold at least 1024 blocks, else 64.
+                               Changes only how the products are tiled and split */
 } seer_distill_opts;
 
 /* ABI version (SEER_ABI_VERSION of the built library). */

@@ -51,7 +51,7 @@ class AttnOpts(C.Structure):
 
 class DistillOpts(C.Structure):
     """seer_distill_opts (zero fields: defaults)."""
-    _fields_ = [("gemm_min_chunks", C.c_int32)]
+    _fields_ = [("gemm_min_chunks", C.c_int32), ("gemm_tile_n", C.c_int32)]
 
 
 def _opts_ref(opts, cls):

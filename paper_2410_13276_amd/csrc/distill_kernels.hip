@@ -214,8 +214,8 @@ __global__ __launch_bounds__(256) void loss_mean_kernel(const double* __restrict
   if (threadIdx.x == 0) loss[0] = (float)(s / (double)rows);
 }
 
-// 64x64 output tile per 256-thread workgroup (a 32x32 block per wavefront), K in
-// chunks of 32 staged through two LDS buffers: the next chunk's global loads
+// 64 x 64 NB output tile per 256-thread workgroup (NB 32x32 blocks per
+// wavefront, sharing its A operand), K in chunks of 32 staged through two LDS buffers: the next chunk's global loads
 // are in flight in registers while the current chunk's MFMAs run, one barrier
 // per chunk.  Each fp32 operand value is written to LDS as three bf16 parts
 // (hi = RNE(x), mid = RNE(x - hi), lo = RNE(x - hi - mid); both differences
@@ -225,8 +225,8 @@ __global__ __launch_bounds__(256) void loss_mean_kernel(const double* __restrict
 // per 32x32x16 step instead of 8 fp32 MFMAs (v_mfma_f32_32x32x2_f32) of 64.
 // The LDS tiles are [part][row][k] bf16 with k contiguous in rows of 64 bytes,
 // their four 16-byte chunks XOR-swizzled by (row / 4) % 4 so that 16 lanes
-// reading 16 rows hit 16 distinct bank groups (48 KiB for the two buffers:
-// three workgroups per CU), and a lane reads the 8 k values of one MFMA
+// reading 16 rows hit 16 distinct bank groups (48 KiB for the two buffers at
+// NB = 1: three workgroups per CU; 72 KiB at NB = 2: two), and a lane reads the 8 k values of one MFMA
 // operand (k = 16 s + 8 hf .. +7 of its row or column at step s) with one
 // 16-byte read per part.  Operand tiles are read from global memory along
 // whichever index has unit stride, so that loads coalesce for every layout
@@ -256,26 +256,30 @@ __device__ __forceinline__ void split3(float x, __bf16& hi, __bf16& mid, __bf16&
 // tri 2: rows near the start), then the batch index and split part, then the
 // column tile.  Launched batch by batch instead, each batch's heavy tiles
 // would come last and the final batches' would run alone at the end.
+template <int NB>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
+  constexpr int TN = kT * NB;  // output tile columns
   __shared__ __attribute__((aligned(16))) __bf16 sA[2][3][kT][kKb];
-  __shared__ __attribute__((aligned(16))) __bf16 sB[2][3][kT][kKb];
+  __shared__ __attribute__((aligned(16))) __bf16 sB[2][3][TN][kKb];
   const int t = threadIdx.x;
-  const int ntn = (g.N + kT - 1) / kT, ntm = (g.M + kT - 1) / kT, nzs = g.Z * splits;
+  const int ntn = (g.N + TN - 1) / TN, ntm = (g.M + kT - 1) / kT, nzs = g.Z * splits;
   const int lin = blockIdx.x;
   const int tn = lin % ntn;
   const int zs = (lin / ntn) % nzs;
   const int tq = lin / ntn / nzs;  // position in the row-tile order
   const int tm = g.tri == 1 ? ntm - 1 - tq : tq;
-  const int m0 = tm * kT, n0 = tn * kT;
+  const int m0 = tm * kT, n0 = tn * TN;
   const int z = zs / splits, sp = zs % splits;
   const float* A = g.A + (int64_t)z * g.saz;
   const float* B = g.B + (int64_t)(z / g.bdiv) * g.sbz;
   const int wave = t / kWave, lane = t % kWave;
   const int wm = wave / 2, wn = wave % 2;
   const int hf = lane / 32, col = lane % 32;
-  f32x16 acc;
+  f32x16 acc[NB];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[b][e] = 0.f;
 
   // k2 range that can hold non-zero A entries for this row tile
   int k2lo = 0, k2hi = g.K2;
@@ -298,9 +302,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
   const int64_t b_off = (int64_t)(n0 + br) * g.sbn + (int64_t)bk * g.sbk2;
   const int64_t a_du = a_mfast ? g.sak2 : 8 * g.sam;  // offset step per u
   const int64_t b_du = b_nfast ? g.sbk2 : 8 * g.sbn;
-  const bool full_mn = m0 + kT <= g.M && n0 + kT <= g.N;
+  const bool full_mn = m0 + kT <= g.M && n0 + TN <= g.N;
 
-  float ra[kLoads], rb[kLoads];
+  // B is fetched and stashed as NB column halves of 64, each mapped as A is
+  float ra[kLoads], rb[NB][kLoads];
   int k1 = 0, kc = 0;  // the chunk being fetched: K1 index, chunk within the k2 range
   if (c0 < c1) {
     k1 = (int)(c0 / nck);
@@ -313,17 +318,25 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
     const int kmax = k2hi - kk;  // k of this chunk below kmax hold data
     if (full_mn && kmax >= kKc) {
 #pragma unroll
-      for (int u = 0; u < kLoads; ++u) {
-        ra[u] = Ak[u * a_du];
-        rb[u] = Bk[u * b_du];
-      }
+      for (int u = 0; u < kLoads; ++u) ra[u] = Ak[u * a_du];
+#pragma unroll
+      for (int h = 0; h < NB; ++h)
+#pragma unroll
+        for (int u = 0; u < kLoads; ++u) rb[h][u] = Bk[(int64_t)(kT * h) * g.sbn + u * b_du];
     } else {
 #pragma unroll
       for (int u = 0; u < kLoads; ++u) {
         const bool aok = a_mfast ? (m0 + ar < g.M && ak + u < kmax) : (m0 + ar + 8 * u < g.M && ak < kmax);
-        const bool bok = b_nfast ? (n0 + br < g.N && bk + u < kmax) : (n0 + br + 8 * u < g.N && bk < kmax);
         ra[u] = aok ? Ak[u * a_du] : 0.f;
-        rb[u] = bok ? Bk[u * b_du] : 0.f;
+      }
+#pragma unroll
+      for (int h = 0; h < NB; ++h) {
+        const int nh = n0 + kT * h + br;
+#pragma unroll
+        for (int u = 0; u < kLoads; ++u) {
+          const bool bok = b_nfast ? (nh < g.N && bk + u < kmax) : (nh + 8 * u < g.N && bk < kmax);
+          rb[h][u] = bok ? Bk[(int64_t)(kT * h) * g.sbn + u * b_du] : 0.f;
+        }
       }
     }
     if (++kc == nck) {
@@ -332,7 +345,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
     }
   };
   // the 8 values of one operand into its LDS tile, split in three parts
-  auto stash_one = [&](__bf16 (&s)[3][kT][kKb], const float (&r)[kLoads], bool fast, int row, int k) {
+  auto stash_one = [&](auto& s, const float (&r)[kLoads], bool fast, int row, int k) {
     if (fast) {  // one row, k .. k + 7
       bf16x8 h, m, l;
 #pragma unroll
@@ -357,7 +370,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
   };
   auto stash = [&](int buf) {
     stash_one(sA[buf], ra, a_mfast, ar, ak);
-    stash_one(sB[buf], rb, b_nfast, br, bk);
+#pragma unroll
+    for (int h = 0; h < NB; ++h) stash_one(sB[buf], rb[h], b_nfast, kT * h + br, bk);
   };
   if (c0 < c1) {
     fetch();
@@ -371,39 +385,48 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int splits) {
   for (int64_t c = c0; c < c1; ++c) {
     const bool more = c + 1 < c1;
     if (more) fetch();
-    // wavefront (wm, wn) accumulates the 32x32 block at rows 32 wm, columns 32
-    // wn of the tile; lane (hf, col) supplies k = 16 st + 8 hf .. +7 of its row
-    // (A) and column (B) to MFMA step st
+    // wavefront (wm, wn) accumulates the NB 32x32 blocks at rows 32 wm,
+    // columns 32 (NB wn + b) of the tile; lane (hf, col) supplies k = 16 st +
+    // 8 hf .. +7 of its row (A) and column (B) to MFMA step st
 #pragma unroll
     for (int st = 0; st < kKc / 16; ++st) {
-      bf16x8 av[3], bv[3];
+      bf16x8 av[3];
 #pragma unroll
-      for (int p = 0; p < 3; ++p) {
+      for (int p = 0; p < 3; ++p)
         av[p] = *reinterpret_cast<const bf16x8*>(&sA[buf][p][32 * wm + col][swz(32 * wm + col, 16 * st + 8 * hf)]);
-        bv[p] = *reinterpret_cast<const bf16x8*>(&sB[buf][p][32 * wn + col][swz(32 * wn + col, 16 * st + 8 * hf)]);
-      }
 #pragma unroll
-      for (int q = 0; q < 6; ++q) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[PA[q]], bv[PB[q]], acc, 0, 0, 0);
+      for (int b = 0; b < NB; ++b) {
+        const int bn = 32 * (NB * wn + b) + col;
+        bf16x8 bv[3];
+#pragma unroll
+        for (int p = 0; p < 3; ++p)
+          bv[p] = *reinterpret_cast<const bf16x8*>(&sB[buf][p][bn][swz(bn, 16 * st + 8 * hf)]);
+#pragma unroll
+        for (int q = 0; q < 6; ++q)
+          acc[b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[PA[q]], bv[PB[q]], acc[b], 0, 0, 0);
+      }
     }
     if (more) stash(buf ^ 1);
     __syncthreads();
     buf ^= 1;
   }
-  const int n = n0 + 32 * wn + col;
-  if (n < g.N) {
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int n = n0 + 32 * (NB * wn + b) + col;
+    if (n >= g.N) continue;
     if (splits == 1) {
       float* C = g.C + (int64_t)z * g.scz;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int m = m0 + 32 * wm + 8 * (e / 4) + 4 * hf + (e % 4);
-        if (m < g.M) C[(int64_t)m * g.scm + n] = g.alpha * acc[e];
+        if (m < g.M) C[(int64_t)m * g.scm + n] = g.alpha * acc[b][e];
       }
     } else {
       float* P = g.part + ((int64_t)z * splits + sp) * g.M * g.N;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int m = m0 + 32 * wm + 8 * (e / 4) + 4 * hf + (e % 4);
-        if (m < g.M) P[(int64_t)m * g.N + n] = acc[e];
+        if (m < g.M) P[(int64_t)m * g.N + n] = acc[b][e];
       }
     }
   }
@@ -459,16 +482,30 @@ hipError_t launch_kl_rows(const KlArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Parts per output tile: enough workgroups to fill the chip (about 2048) when
-// the tiles alone are fewer, but at least a.min_chunks chunks of K per part on
-// the longest tile (8 by default; a smaller value lets tests split small
-// products).
+// Output tile width.  128 columns (each A chunk is then split into parts once
+// per 128 columns instead of once per 64, and every barrier covers twice the
+// MFMAs, at two workgroups per CU instead of three) when the product has that
+// many and a long contraction: measured with their split sums at 2048 blocks
+// (32 query / 8 KV heads, gate_dim 128) 0.50 -> 0.43 ms, at 1024 blocks (28 /
+// 4 heads) 0.164 -> 0.158 ms, but at 512 blocks 0.090 -> 0.098 ms (too few
+// tiles).
+static int gemm_tile_n(const GemmArgs& a) {
+  if (a.tile_n == kT || a.tile_n == 2 * kT) return a.tile_n;
+  return (a.N >= 2 * kT && a.K2 >= 32 * kKc) ? 2 * kT : kT;
+}
+
+// Parts per output tile: enough workgroups to fill the chip (about 2048 of
+// 64-column tiles, 1024 of 128-column ones) when the tiles alone are fewer,
+// but at least a.min_chunks chunks of K per part on the longest tile (8 by
+// default; a smaller value lets tests split small products).
 int gemm_splits(const GemmArgs& a) {
   if (a.M <= 0 || a.N <= 0 || a.Z <= 0) return 1;
   const int min_chunks = a.min_chunks >= 1 ? a.min_chunks : 8;
-  const int64_t tiles = (int64_t)((a.N + kT - 1) / kT) * ((a.M + kT - 1) / kT) * a.Z;
+  const int tn = gemm_tile_n(a);
+  const int64_t tiles = (int64_t)((a.N + tn - 1) / tn) * ((a.M + kT - 1) / kT) * a.Z;
   const int64_t chunks = (int64_t)a.K1 * ((a.K2 + kKc - 1) / kKc);
-  int64_t sp = (2048 + tiles - 1) / tiles;
+  const int64_t target = 2048 * kT / tn;  // workgroups (the same output area in flight)
+  int64_t sp = (target + tiles - 1) / tiles;
   sp = std::min<int64_t>(sp, chunks / min_chunks);
   sp = std::min<int64_t>(sp, 64);
   return (int)std::max<int64_t>(sp, 1);
@@ -483,9 +520,11 @@ hipError_t launch_gemm_f32(const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0 || a.Z <= 0) return hipSuccess;
   const int sp = gemm_splits(a);
   if (sp > 1 && a.part == nullptr) return hipErrorInvalidValue;
-  const int64_t tiles = (int64_t)((a.N + kT - 1) / kT) * ((a.M + kT - 1) / kT) * a.Z * sp;
+  const int tn = gemm_tile_n(a);
+  const int64_t tiles = (int64_t)((a.N + tn - 1) / tn) * ((a.M + kT - 1) / kT) * a.Z * sp;
   if (tiles > INT32_MAX) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(gemm_f32_kernel, dim3((unsigned)tiles), dim3(256), 0, s, a, sp);
+  if (tn == 2 * kT) hipLaunchKernelGGL(gemm_f32_kernel<2>, dim3((unsigned)tiles), dim3(256), 0, s, a, sp);
+  else hipLaunchKernelGGL(gemm_f32_kernel<1>, dim3((unsigned)tiles), dim3(256), 0, s, a, sp);
   if (sp > 1) {
     const int64_t n = (int64_t)a.Z * a.M * a.N;
     hipLaunchKernelGGL(gemm_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a, sp);

@@ -159,6 +159,7 @@ struct GemmArgs {
   float alpha;
   float* part;
   int min_chunks;  // K chunks per part at least (seer_distill_opts.gemm_min_chunks; 8 by default)
+  int tile_n;      // output tile columns: 64, 128, or 0 (chosen from the shape)
 };
 int gemm_splits(const GemmArgs& a);
 int64_t gemm_partial_elems(const GemmArgs& a);

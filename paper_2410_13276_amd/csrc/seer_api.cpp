@@ -118,7 +118,7 @@ struct DistillGemms {
   seer::GemmArgs dqg, dkg, dwq, dwk;
 };
 
-DistillGemms distill_gemms(int B, int Hq, int Hkv, int D, int Dg, int nb, bool ph, int min_chunks,
+DistillGemms distill_gemms(int B, int Hq, int Hkv, int D, int Dg, int nb, bool ph, int min_chunks, int tile_n,
                            const float* dl, const float* qg, const float* kg, const float* qp, const float* kp,
                            float* dqg, float* dkg, float* dwq, float* dwk, float* part) {
   const int G = Hq / Hkv;
@@ -182,7 +182,10 @@ DistillGemms distill_gemms(int B, int Hq, int Hkv, int D, int Dg, int nb, bool p
     g.sbz = 0; g.sbk1 = (int64_t)nb * Dg;
   }
   r.dwk = g;
-  for (seer::GemmArgs* x : {&r.dqg, &r.dkg, &r.dwq, &r.dwk}) x->min_chunks = min_chunks;
+  for (seer::GemmArgs* x : {&r.dqg, &r.dkg, &r.dwq, &r.dwk}) {
+    x->min_chunks = min_chunks;
+    x->tile_n = tile_n;
+  }
   return r;
 }
 
@@ -193,7 +196,7 @@ struct DistillLayout {
   size_t qg, kg, qs, ks, qp, kp, logits, dqg, dkg, row_loss, part, total;
 };
 
-DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g, int min_chunks) {
+DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g, int min_chunks, int tile_n) {
   const size_t nb = (size_t)blocks_of(d->seq_len, g->block);
   const size_t B = d->batch, Hq = d->heads_q, Hkv = d->heads_kv, D = d->head_dim, Dg = g->gate_dim;
   DistillLayout L;
@@ -214,7 +217,7 @@ DistillLayout distill_layout(const seer_attn_desc* d, const seer_gate_desc* g, i
   L.dkg = take(B * Hkv * nb * Dg * 4);
   L.row_loss = take((B * Hq * nb + seer::kLossParts) * 8);
   const DistillGemms gm = distill_gemms((int)B, (int)Hq, (int)Hkv, (int)D, (int)Dg, (int)nb, g->w_per_head != 0,
-                                        min_chunks, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                        min_chunks, tile_n, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                                         nullptr, nullptr, nullptr);
   int64_t part = 0;
   for (const seer::GemmArgs* a : {&gm.dqg, &gm.dkg, &gm.dwq, &gm.dwk})
@@ -671,10 +674,18 @@ static int distill_min_chunks(const seer_distill_opts* opts) {
   return (opts && opts->gemm_min_chunks >= 1) ? opts->gemm_min_chunks : 8;
 }
 
+// 0 (chosen from the shape), 64 or 128; -1: invalid
+static int distill_tile_n(const seer_distill_opts* opts) {
+  const int t = opts ? opts->gemm_tile_n : 0;
+  return (t == 0 || t == 64 || t == 128) ? t : -1;
+}
+
 size_t seer_gate_distill_workspace_bytes(const seer_attn_desc* desc, const seer_gate_desc* gate,
                                          const seer_distill_opts* opts) {
   if (check_gate_common(desc, gate) != SEER_OK) return 0;
-  return distill_layout(desc, gate, distill_min_chunks(opts)).total;
+  const int tile_n = distill_tile_n(opts);
+  if (tile_n < 0) return 0;
+  return distill_layout(desc, gate, distill_min_chunks(opts), tile_n).total;
 }
 
 seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* gate, const void* q,
@@ -687,7 +698,9 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   if (!q || !k || !wq || !wk || !gt || !loss || !dwq || !dwk) return SEER_ERR_INVALID_ARG;
   if (!aligned16(q) || !aligned16(k) || !aligned16(wq) || !aligned16(wk)) return SEER_ERR_INVALID_ARG;
   const int min_chunks = distill_min_chunks(opts);
-  const DistillLayout W = distill_layout(desc, gate, min_chunks);
+  const int tile_n = distill_tile_n(opts);
+  if (tile_n < 0) return SEER_ERR_INVALID_ARG;
+  const DistillLayout W = distill_layout(desc, gate, min_chunks, tile_n);
   if (!workspace || workspace_bytes < W.total) return SEER_ERR_WORKSPACE;
   if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0) return SEER_ERR_INVALID_ARG;
 
@@ -758,7 +771,7 @@ seer_status seer_gate_distill(const seer_attn_desc* desc, const seer_gate_desc* 
   ka.loss = loss;
   if ((s = from_hip(seer::launch_kl_rows(ka, st))) != SEER_OK) return s;
 
-  const DistillGemms gm = distill_gemms(B, Hq, Hkv, D, Dg, nb, gate->w_per_head != 0, min_chunks, dl, qg, kg, qp,
+  const DistillGemms gm = distill_gemms(B, Hq, Hkv, D, Dg, nb, gate->w_per_head != 0, min_chunks, tile_n, dl, qg, kg, qp,
                                         kp, dqg, dkg, dwq, dwk, reinterpret_cast<float*>(ws + W.part));
   if ((s = from_hip(seer::launch_gemm_f32(gm.dqg, st))) != SEER_OK) return s;
   if ((s = from_hip(seer::launch_gemm_f32(gm.dkg, st))) != SEER_OK) return s;

@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert seer.abi_version() == 4
+    assert seer.abi_version() == 5
     assert seer.status_str(0) == "SEER_OK"
     assert seer.status_str(3) == "SEER_ERR_WORKSPACE"
     assert seer.status_str(99) == "SEER_ERR_UNKNOWN"
@@ -202,24 +202,39 @@ def test_gate_distill_workspace_and_rejects_bad_args():
     assert call(gd=_gate(rope_theta=-2.0)) == seer.ERR_INVALID_ARG
 
 
-def _gemm_splits(M, N, K1, K2, Z, min_chunks=8):
-    """The split rule of the distillation products: about 2048 workgroups when
-    the 64x64 output tiles are fewer, at least `min_chunks` 32-wide K chunks per
-    part, at most 64 parts."""
-    tiles = -(-N // 64) * -(-M // 64) * Z
+def _gemm_tile_n(N, K2, tile_n=0):
+    """Output tile width of a distillation product: the option when set, else
+    128 columns for N >= 128 with a contraction of at least 1024, else 64."""
+    if tile_n in (64, 128):
+        return tile_n
+    return 128 if N >= 128 and K2 >= 1024 else 64
+
+
+def _gemm_splits(M, N, K1, K2, Z, min_chunks=8, tile_n=0):
+    """The split rule of the distillation products: about 2048 workgroups of
+    64x64 output tiles, or 1024 of 64x128 ones, when the tiles are fewer, at
+    least `min_chunks` 32-wide K chunks per part, at most 64 parts."""
+    tn = _gemm_tile_n(N, K2, tile_n)
+    tiles = -(-N // tn) * -(-M // 64) * Z
     chunks = K1 * -(-K2 // 32)
-    return max(1, min(-(-2048 // tiles), chunks // min_chunks, 64))
+    return max(1, min(-(-(2048 * 64 // tn) // tiles), chunks // min_chunks, 64))
 
 
-@pytest.mark.parametrize("min_chunks", [None, 1])
-def test_gate_distill_workspace_split_products(min_chunks):
-    """At 32k tokens (32 q / 8 kv heads) the backward products split their K
-    range; the workspace holds the largest product's parts (gemm_min_chunks
-    option: at least that many K chunks per part)."""
-    opts = None if min_chunks is None else C.byref(seer.DistillOpts(gemm_min_chunks=min_chunks))
+@pytest.mark.parametrize("nb,min_chunks,tile_n", [(512, None, 0), (512, 1, 0), (512, None, 128),
+                                                  (1024, None, 0), (1024, 2, 64), (2048, None, 0)])
+def test_gate_distill_workspace_split_products(nb, min_chunks, tile_n):
+    """32 q / 8 kv heads: the backward products split their K range; the
+    workspace holds the largest product's parts (gemm_min_chunks: at least that
+    many K chunks per part; gemm_tile_n: the output tile width)."""
+    fields = {}
+    if min_chunks is not None:
+        fields["gemm_min_chunks"] = min_chunks
+    if tile_n:
+        fields["gemm_tile_n"] = tile_n
+    opts = C.byref(seer.DistillOpts(**fields)) if fields else None
     mc = min_chunks or 8
     L = seer.lib()
-    B, Hq, Hkv, D, Dg, nb = 1, 32, 8, 128, 128, 512
+    B, Hq, Hkv, D, Dg = 1, 32, 8, 128, 128
     d, g = _desc(B=B, Hq=Hq, Hkv=Hkv, S=64 * nb, D=D), _gate()
     up = lambda x: (x + 255) // 256 * 256
     base = (up(Hq * nb * Dg * 4) + up(Hkv * nb * Dg * 4) + up(Hq * _sr(nb) * 3 * Dg * 2) + up(Hkv * _sr(nb) * 3 * Dg * 2)
@@ -228,11 +243,21 @@ def test_gate_distill_workspace_split_products(min_chunks):
     products = [(nb, Dg, 1, nb, Hq), (nb, Dg, Hq // Hkv, nb, Hkv), (D, Dg, 1, nb, Hq), (3 * D, Dg, 1, nb, Hkv)]
     part = 0
     for M, N, K1, K2, Z in products:
-        sp = _gemm_splits(M, N, K1, K2, Z, mc)
+        sp = _gemm_splits(M, N, K1, K2, Z, mc, tile_n)
         if sp > 1:
             part = max(part, Z * sp * M * N)
     assert part > 0
     assert L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g), opts) == base + up(4 * part)
+
+
+def test_gate_distill_rejects_bad_tile_width():
+    L = seer.lib()
+    d, g = _desc(B=1, Hq=2, Hkv=1, S=1024, D=64), _gate()
+    for t in (32, 96, 256, -64):
+        assert L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g),
+                                                   C.byref(seer.DistillOpts(gemm_tile_n=t))) == 0
+    assert L.seer_gate_distill_workspace_bytes(C.byref(d), C.byref(g),
+                                               C.byref(seer.DistillOpts(gemm_tile_n=64))) > 0
 
 
 def test_attn_workspace_bytes_formula():

@@ -75,11 +75,14 @@ def _weights(B, Hq, Hkv, D, Dg, per_head, seed):
 
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "x".join(map(str, c)))
-@pytest.mark.parametrize("min_chunks", [None, 1], ids=["default", "split"])
-def test_gate_distill_parity(case, min_chunks):
+@pytest.mark.parametrize("opts", [None, {"gemm_min_chunks": 1}, {"gemm_tile_n": 128},
+                                  {"gemm_tile_n": 128, "gemm_min_chunks": 1}],
+                         ids=["default", "split", "wide", "wide_split"])
+def test_gate_distill_parity(case, opts):
     """`split`: every backward product cut into as many K parts as it has
-    K chunks (empty parts included), summed by the reduction kernel."""
-    opts = None if min_chunks is None else {"gemm_min_chunks": min_chunks}
+    K chunks (empty parts included), summed by the reduction kernel.  `wide`:
+    128-column output tiles for every product (ragged where gate_dim < 128),
+    which the default takes only for long rows at gate_dim 128."""
     B, Hq, Hkv, S, D, dt, Dg, per_head, theta = case
     seed = stable_seed(case, "distill")
     _, q, k, _, _, _ = small_inputs(B, Hq, Hkv, S, D, dt, seed=seed, spikes=True)
