@@ -1489,7 +1489,7 @@ static void launch_nh_d(const KernelArgs& ka, int nh, bool sparse, bool ragged, 
 // leave too much idle time at their ends.  Measured at 131072 tokens (32 q / 8
 // KV heads, TopK 0.1), walking ascending: 17.29 ms unbatched, 16.92 ms with
 // every task batched, 16.65 ms with the heavier half batched; with the walk by
-// residue classes (same box, batched fraction none / 1/8 / 1/4 / 3/8 / 1/2 /
+// residue classes (one GPU, back to back; batched fraction none / 1/8 / 1/4 / 3/8 / 1/2 /
 // 3/4 / all): 14.47-14.53, 14.33-14.36, 14.24-14.33, 14.30-14.35, 14.41-14.51,
 // 14.67, 14.83 ms; 48.9 -> 48.2 ms (all batched) with per-head
 // densities spread over 5-40%; at 32768 tokens the batch ends' idle time
